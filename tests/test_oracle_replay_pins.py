@@ -1,0 +1,344 @@
+"""Pins for the oracle's replay, each against something other than itself:
+invariants the paper states (I1, I2, Prop. 1, work conservation of Sec.
+III-E), closed forms (token bucket, infinite capacity, repeated request,
+cyclic sweep, one-touch S3-FIFO), degenerate cases that reduce to the base
+policy, and Belady's offline optimum as an upper bound on hits (MIN itself
+pinned by exhaustive search)."""
+import heapq
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_01657_amd import tracegen as tg
+
+Q = tg.Q16
+POLICIES = [tg.POLICY_LRU, tg.POLICY_S3FIFO, tg.POLICY_PREFIXSHIELD]
+
+
+# ---------------------------------------------------------------- helpers
+
+def key_trace(reqs, groups=None, prefixes=None, contracts=None, n_groups=None, tick=None):
+    """reqs: list of key lists."""
+    keys = [k for r in reqs for k in r]
+    off = np.cumsum([0] + [len(r) for r in reqs]).astype(np.int64)
+    R = len(reqs)
+    groups = np.zeros(R, np.uint8) if groups is None else np.asarray(groups, np.uint8)
+    prefixes = np.arange(R, dtype=np.uint32) if prefixes is None else np.asarray(prefixes, np.uint32)
+    contracts = np.zeros(R, np.uint8) if contracts is None else np.asarray(contracts, np.uint8)
+    ng = n_groups or (int(groups.max()) + 1 if R else 1)
+    return tg.KeyTrace(np.asarray(keys, np.uint64), off, groups, contracts, prefixes, ng,
+                       int(prefixes.max()) + 1 if R else 1,
+                       tick=None if tick is None else np.asarray(tick, np.int64))
+
+
+def totals(res, field):
+    return sum(g[field] for g in res.groups)
+
+
+def belady_min_hits(seq, C):
+    """Offline optimal (furthest next use) hits for a demand-paged cache."""
+    INF = float("inf")
+    nxt = [INF] * len(seq)
+    last = {}
+    for i in range(len(seq) - 1, -1, -1):
+        nxt[i] = last.get(seq[i], INF)
+        last[seq[i]] = i
+    cache = {}
+    heap = []
+    hits = 0
+    for i, k in enumerate(seq):
+        if k in cache:
+            hits += 1
+        elif len(cache) >= C:
+            while True:
+                nu, kk = heapq.heappop(heap)
+                if kk in cache and cache[kk] == -nu:
+                    del cache[kk]
+                    break
+        cache[k] = nxt[i]
+        heapq.heappush(heap, (-nxt[i], k))
+    return hits
+
+
+def exhaustive_max_hits(seq, C):
+    best = 0
+    states = {frozenset(): 0}
+    for k in seq:
+        new = {}
+        for st, h in states.items():
+            if k in st:
+                cand = [(st, h + 1)]
+            elif len(st) < C:
+                cand = [(st | {k}, h)]
+            else:
+                cand = [((st - {v}) | {k}, h) for v in st]
+            for s2, h2 in cand:
+                if new.get(s2, -1) < h2:
+                    new[s2] = h2
+        states = new
+    return max(states.values()) if states else best
+
+
+def check_invariants(res, C, per_req=None):
+    gs = res.groups
+    for g in gs:
+        assert g["hits"] + g["misses"] == g["probes"]
+        assert g["charged"] == g["misses"] - g["dups"]          # I1: every new block charged once
+        assert g["debt_max_q16"] >= g["debt_end_q16"] >= 0
+        assert g["resident_max"] <= C and g["resident_end"] <= g["resident_max"]
+    ev = res.inst["evictions"]
+    assert sum(g["evicted_owned"] for g in gs) == ev == sum(g["evictions_caused"] for g in gs)
+    assert res.inst["resident_end"] == totals(res, "charged") - ev - totals(res, "orphans")
+    assert res.inst["resident_end"] == sum(g["resident_end"] for g in gs)
+    assert res.inst["resident_max"] <= C
+    if per_req is not None:
+        # work conservation (Sec. III-E): reclaim only what free space cannot cover
+        resident = 0
+        for h, m, e, orph in per_req.tolist():
+            assert e == max(0, resident - orph + m - C)
+            resident = resident - orph - e + m
+            assert resident <= C
+        assert resident == res.inst["resident_end"]
+
+
+# ---------------------------------------------------------------- MIN pins
+
+def test_belady_min_matches_exhaustive_search():
+    rng = np.random.default_rng(0)
+    for _ in range(150):
+        L = int(rng.integers(1, 11))
+        seq = [int(x) for x in rng.integers(0, 5, L)]
+        C = int(rng.integers(1, 4))
+        assert belady_min_hits(seq, C) == exhaustive_max_hits(seq, C)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_hits_bounded_by_belady(seed):
+    rng = np.random.default_rng(100 + seed)
+    kt = tg.random_key_trace(seed + 500, n_req=40, max_blocks=6, n_groups=int(rng.integers(1, 4)),
+                             key_universe=16)
+    C = int(rng.integers(2, 10))
+    for pol in POLICIES:
+        for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+            inst = tg.Instance(0, pol, C, contracts=[(Q // 3, 2 * Q)], flags=flags)
+            res = oracle.replay_key_trace(kt, inst, per_request=True)
+            check_invariants(res, C, res.per_request)
+            seq = []
+            for r in range(kt.n_req):
+                ks = [int(x) for x in kt.keys[kt.key_off[r]:kt.key_off[r + 1]]]
+                seq.extend(ks[:C])
+            assert totals(res, "hits") <= belady_min_hits(seq, C)
+
+
+def test_workload_invariants_and_belady():
+    tr = tg.onetouch_tiny(1000, 1200)
+    keys, off = oracle.hash_trace(tr)
+    seq = []
+    for r in range(tr.n_req):
+        seq.extend(int(x) for x in keys[off[r]:off[r + 1]])
+    for pol in POLICIES:
+        inst = tg.Instance(0, pol, 256)
+        res = oracle.replay_trace(tr, keys, off, inst, per_request=True)
+        check_invariants(res, 256, res.per_request)
+        assert totals(res, "hits") <= belady_min_hits(seq, 256)
+
+
+# ---------------------------------------------------------------- closed forms
+
+@pytest.mark.parametrize("pol", POLICIES)
+def test_infinite_capacity_misses_are_first_occurrences(pol):
+    tr = tg.conversations(77, 400, n_groups=4)
+    keys, off = oracle.hash_trace(tr)
+    C = len(np.unique(keys)) + 10
+    res = oracle.replay_trace(tr, keys, off, tg.Instance(0, pol, C))
+    seen = set()
+    want = [0] * tr.n_groups
+    for r in range(tr.n_req):
+        for k in keys[off[r]:off[r + 1]]:
+            if int(k) not in seen:
+                seen.add(int(k))
+                want[tr.group[r]] += 1
+    assert [g["misses"] for g in res.groups] == want
+    assert res.inst["evictions"] == 0 and totals(res, "orphans") == 0
+    assert res.inst["resident_end"] == len(seen)
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+def test_repeated_request(pol):
+    n, R = 37, 9
+    kt = key_trace([list(range(100, 100 + n))] * R, prefixes=[0] * R)
+    for C in (n, n + 5, 4 * n):
+        res = oracle.replay_key_trace(kt, tg.Instance(0, pol, C))
+        g = res.groups[0]
+        assert g["hits"] == (R - 1) * n and g["misses"] == n and res.inst["evictions"] == 0
+
+
+def test_cyclic_sweep_lru_zero_hits():
+    """K single-block prefixes visited cyclically with K > C: LRU never hits
+    (the mechanism behind StaticQuota's 0.00% in Sec. V-B)."""
+    for K, C in [(5, 4), (33, 32), (289, 255)]:
+        kt = key_trace([[i % K] for i in range(6 * K)], prefixes=[i % K for i in range(6 * K)])
+        res = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_LRU, C))
+        assert res.groups[0]["hits"] == 0
+        assert res.inst["evictions"] == 6 * K - C
+        # with capacity K every revisit hits
+        res = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_LRU, K))
+        assert res.groups[0]["hits"] == 5 * K
+
+
+@pytest.mark.parametrize("C", [1, 7, 64])
+def test_one_touch_s3fifo(C):
+    """Never-repeated keys: nothing reaches the main queue, every insert
+    beyond capacity evicts one block out of the small queue."""
+    rng = np.random.default_rng(C)
+    reqs = []
+    nxt = 0
+    for _ in range(200):
+        n = int(rng.integers(0, min(C, 6) + 1))
+        reqs.append(list(range(nxt, nxt + n))); nxt += n
+    kt = key_trace(reqs)
+    res = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_S3FIFO, C))
+    assert totals(res, "hits") == 0
+    assert res.inst["s3_moves"] == 0 and res.inst["s3_reinserts"] == 0
+    assert res.inst["evictions"] == max(0, nxt - C) == res.inst["s3_ghost_inserts"]
+
+
+def bucket_path(rho, beta, x, R):
+    """Balance after each request when one group creates x new blocks per
+    tick from t=0 (Eqs. 1-2): B_0 = beta - x, B_r = B_{r-1} + rho - x while
+    x >= rho (the refill never reaches the cap)."""
+    return [beta - x * Q + r * (rho - x * Q) for r in range(R)]
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+@pytest.mark.parametrize("rho_blocks,beta_blocks,x", [(1, 0, 3), (2, 5, 2), (0.5, 192, 7)])
+def test_token_bucket_closed_form(pol, rho_blocks, beta_blocks, x):
+    rho, beta = int(rho_blocks * Q), beta_blocks * Q
+    R = 60
+    reqs = [list(range(1000 * r, 1000 * r + x)) for r in range(R)]
+    kt = key_trace(reqs)
+    res = oracle.replay_key_trace(kt, tg.Instance(0, pol, 10_000, contracts=[(rho, beta)]))
+    path = bucket_path(rho, beta, x, R)
+    debts = [max(0, -b) for b in path]
+    g = res.groups[0]
+    assert g["charged"] == R * x
+    assert g["debt_end_q16"] == debts[-1]
+    assert g["debt_max_q16"] == max(debts)
+    assert g["debt_sum_q16"] == sum(debts)
+
+
+def test_proposition1_quiescent_clearance():
+    """Prop. 1: after creation stops at t0, debt is zero exactly from
+    t0 + ceil(d/rho) on (rho > 0)."""
+    rho, beta, x, t_create = Q // 3, 4 * Q, 5, 20
+    d = -bucket_path(rho, beta, x, t_create)[-1]
+    assert d > 0
+    tau = -(-d // rho)
+    for extra in (tau - 1, tau):
+        reqs = [list(range(1000 * r, 1000 * r + x)) for r in range(t_create)] + [[]] * extra
+        kt = key_trace(reqs)
+        res = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_PREFIXSHIELD, 10_000,
+                                                      contracts=[(rho, beta)]))
+        assert (res.groups[0]["debt_end_q16"] == 0) == (extra >= tau)
+
+
+def _replay_trace_two_groups(delay):
+    """Group 1 creates 6 prefixes (8 blocks each) in 6 ticks, waits `delay`
+    ticks (group 0 touches a tiny private prefix meanwhile), then replays
+    them twice."""
+    reqs, groups, prefixes = [], [], []
+    for i in range(6):
+        reqs.append([10_000 + 100 * i + j for j in range(8)]); groups.append(1); prefixes.append(10 + i)
+    for _ in range(delay):
+        reqs.append([1, 2]); groups.append(0); prefixes.append(0)
+    for _ in range(2):
+        for i in range(6):
+            reqs.append([10_000 + 100 * i + j for j in range(8)]); groups.append(1); prefixes.append(10 + i)
+    return key_trace(reqs, groups=groups, prefixes=prefixes, n_groups=2)
+
+
+def test_debt_gate_blocks_promotion_while_in_debt():
+    """I2 / Eq. 4: while D_g > eps no block of g is promoted; every eligible
+    hit is counted as gated.  Without the gate they are all promoted."""
+    rho, beta = Q // 4, 0
+    kt = _replay_trace_two_groups(delay=3)
+    gated = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_PREFIXSHIELD, 1000, contracts=[(rho, beta)]))
+    free = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_PREFIXSHIELD, 1000, contracts=[(rho, beta)],
+                                                   flags=tg.FLAG_NO_DEBT_GATE))
+    g1, f1 = gated.groups[1], free.groups[1]
+    assert g1["promotions"] == 0 and g1["gated"] == 6 * 8 * 2
+    assert f1["gated"] == 0 and f1["promotions"] == 6 * 8       # second replay is already REUSE
+    assert f1["hits"] == g1["hits"] == 2 * 6 * 8
+
+
+def test_gate_and_no_gate_converge_after_clearance():
+    """Sec. V-D: once the replaying group's debt has cleared, the gated and
+    ungated variants behave identically."""
+    rho, beta = Q // 4, 0
+    tau = -(-48 * Q // rho) + 6
+    kt = _replay_trace_two_groups(delay=tau + 5)
+    a = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_PREFIXSHIELD, 1000, contracts=[(rho, beta)]))
+    b = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_PREFIXSHIELD, 1000, contracts=[(rho, beta)],
+                                                flags=tg.FLAG_NO_DEBT_GATE))
+    assert a.groups[1] == b.groups[1] and a.inst == b.inst
+    assert a.groups[1]["promotions"] == 48 and a.groups[1]["gated"] == 0
+
+
+# ---------------------------------------------------------------- degeneracies
+
+def _strip(res):
+    out = []
+    for g in res.groups:
+        g = dict(g); g.pop("promotions"); g.pop("gated"); out.append(g)
+    return out, res.inst
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_single_group_no_segmentation_is_lru(seed):
+    """With one accounting group and no reuse segmentation, PrefixShield's
+    victim is always the group's oldest block: exactly LRU (Sec. V-A base)."""
+    kt = tg.random_key_trace(seed, n_req=60, max_blocks=7, n_groups=1, key_universe=20)
+    for C in (3, 8, 20):
+        for rho, beta in [(Q // 5, 0), (Q, 3 * Q), (50 * Q, 100 * Q)]:
+            lru = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_LRU, C, contracts=[(rho, beta)]))
+            ps = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_PREFIXSHIELD, C, contracts=[(rho, beta)],
+                                                         flags=tg.FLAG_NO_SEGMENTATION))
+            assert _strip(lru) == _strip(ps)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_no_debt_no_segmentation_is_lru(seed):
+    """When no group ever owes debt, the selector always falls back to the
+    global segment order; without segmentation that is global LRU."""
+    kt = tg.random_key_trace(seed, n_req=60, max_blocks=7, n_groups=4, key_universe=20)
+    big = [(Q, 10**6 * Q)]
+    for C in (4, 12):
+        lru = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_LRU, C, contracts=big))
+        ps = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_PREFIXSHIELD, C, contracts=big,
+                                                     flags=tg.FLAG_NO_SEGMENTATION))
+        assert _strip(lru) == _strip(ps)
+        assert all(g["debt_max_q16"] == 0 for g in ps.groups)
+
+
+@pytest.mark.parametrize("pol", POLICIES)
+def test_idle_peer_borrowing(pol):
+    """Work conservation (Sec. V-C, Table III): with the peer idle the active
+    group may fill the whole cache."""
+    rng = np.random.default_rng(3)
+    reqs = [list(rng.integers(0, 300, 6)) for _ in range(200)]
+    kt = key_trace(reqs, n_groups=2)
+    res = oracle.replay_key_trace(kt, tg.Instance(0, pol, 64, contracts=[(Q // 8, 0)]))
+    assert res.groups[0]["resident_max"] == 64 and res.groups[1]["resident_max"] == 0
+
+
+def test_victim_protected_under_one_touch():
+    """Directional check only (not a parity pin): on the one-touch recipe the
+    victim does better under PrefixShield than under LRU (Sec. V-B)."""
+    tr = tg.onetouch_tiny(1000, 4000)
+    keys, off = oracle.hash_trace(tr)
+    r_lru = oracle.replay_trace(tr, keys, off, tg.Instance(0, tg.POLICY_LRU, 256))
+    r_ps = oracle.replay_trace(tr, keys, off, tg.Instance(0, tg.POLICY_PREFIXSHIELD, 256))
+    assert r_ps.groups[0]["hits"] > r_lru.groups[0]["hits"]
+    assert r_ps.groups[1]["evicted_owned"] > r_lru.groups[1]["evicted_owned"]

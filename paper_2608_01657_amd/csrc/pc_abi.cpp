@@ -1,0 +1,373 @@
+// pc_abi.cpp -- the C ABI of libpcreplay (declared in include/pc.h): host
+// validation, workspace planning, descriptor upload and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "pc.h"
+#include "pc_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int32_t fail(int32_t code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+int32_t ok() {
+    g_err.clear();
+    return PC_OK;
+}
+int32_t hip_fail(hipError_t e, const char *what) {
+    return fail(PC_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+int ceil_log2(int64_t v) {
+    int b = 0;
+    while (((int64_t)1 << b) < v) ++b;
+    return b;
+}
+int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+// Usable dynamic LDS per workgroup on the current device (cached per device).
+int64_t lds_limit() {
+    static std::mutex mu;
+    static int64_t cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 65536;
+    std::lock_guard<std::mutex> lk(mu);
+    if (cache[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
+            v = 65536;
+        cache[dev] = v;
+    }
+    return cache[dev];
+}
+
+struct Plan {
+    std::vector<pcr::DevInst> di;
+    std::vector<pcr::DevTrace> dt;
+    std::vector<int32_t> order;      // LDS launch first, then the workspace launch
+    int32_t n_lds = 0;
+    int32_t lds_bytes = 0;
+    int64_t hdr_bytes = 0;
+    int64_t ws_bytes = 0;
+};
+
+constexpr int64_t kMaxRho = (int64_t)1 << 40;
+constexpr int64_t kMaxBeta = (int64_t)1 << 50;
+
+int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst,
+                          int32_t n_inst, int64_t lds_cap, Plan &P) {
+    if (n_traces < 0 || n_inst < 0) return fail(PC_EINVAL, "negative count");
+    if ((n_traces > 0 && !traces) || (n_inst > 0 && !inst)) return fail(PC_EINVAL, "null descriptor array");
+    P.dt.resize(n_traces);
+    for (int i = 0; i < n_traces; ++i) {
+        const pc_trace_desc &t = traces[i];
+        if (t.n_req < 0 || t.n_keys < 0 || t.n_prefix < 0 || t.max_req_blocks < 0)
+            return fail(PC_EINVAL, "trace %d: negative size", i);
+        if (t.n_groups < 1 || t.n_groups > PC_MAX_GROUPS)
+            return fail(PC_EINVAL, "trace %d: n_groups %d outside 1..64", i, t.n_groups);
+        if (t.n_req > 0 && (!t.d_key_off || !t.d_group || !t.d_contract || !t.d_prefix))
+            return fail(PC_EINVAL, "trace %d: null request array", i);
+        if (t.n_keys > 0 && !t.d_keys) return fail(PC_EINVAL, "trace %d: null keys", i);
+        if (t.n_req > 0 && t.n_prefix < 1) return fail(PC_EINVAL, "trace %d: n_prefix must be >= 1", i);
+        if (t.n_prefix > ((int64_t)1 << 32)) return fail(PC_EINVAL, "trace %d: n_prefix too large", i);
+        pcr::DevTrace &d = P.dt[i];
+        d.keys = t.d_keys;
+        d.key_off = t.d_key_off;
+        d.group = t.d_group;
+        d.contract = t.d_contract;
+        d.prefix = t.d_prefix;
+        d.tick = t.d_tick;
+        d.n_req = t.n_req;
+        d.n_keys = t.n_keys;
+        d.n_prefix = t.n_prefix;
+        d.n_groups = t.n_groups;
+        d.max_req_blocks = t.max_req_blocks;
+    }
+    P.di.resize(n_inst);
+    std::vector<int64_t> state_ws(n_inst, 0);
+    int64_t off = 0;
+    // header: DevInst[], DevTrace[], order[]
+    off = align_up(off + (int64_t)sizeof(pcr::DevInst) * n_inst, 256);
+    off = align_up(off + (int64_t)sizeof(pcr::DevTrace) * n_traces, 256);
+    off = align_up(off + (int64_t)sizeof(int32_t) * n_inst, 256);
+    P.hdr_bytes = off;
+    int64_t per_req = 0;
+    std::vector<int32_t> lds_ids, glb_ids;
+    std::vector<double> cost(n_inst, 0.0);
+    for (int i = 0; i < n_inst; ++i) {
+        const pc_instance_desc &s = inst[i];
+        if (s.trace < 0 || s.trace >= n_traces) return fail(PC_EINVAL, "instance %d: trace index %d", i, s.trace);
+        if (s.policy < PC_LRU || s.policy > PC_PREFIXSHIELD) return fail(PC_EINVAL, "instance %d: policy %d", i, s.policy);
+        if (s.capacity < 1 || s.capacity > PC_MAX_CAPACITY)
+            return fail(PC_EINVAL, "instance %d: capacity %d outside 1..%d", i, s.capacity, PC_MAX_CAPACITY);
+        if (s.flags & ~(PC_FLAG_NO_SEGMENTATION | PC_FLAG_NO_DEBT_GATE))
+            return fail(PC_EINVAL, "instance %d: unknown flags 0x%x", i, s.flags);
+        if (s.n_contracts < 1 || s.n_contracts > PC_MAX_CONTRACTS)
+            return fail(PC_EINVAL, "instance %d: n_contracts %d outside 1..4", i, s.n_contracts);
+        if (s.s3_small_permille < 0 || s.s3_small_permille > 1000 || s.s3_move_threshold < 0)
+            return fail(PC_EINVAL, "instance %d: S3-FIFO parameters", i);
+        if (s.reserved != 0) return fail(PC_EINVAL, "instance %d: reserved field must be 0", i);
+        if (s.eps_q16 < 0 || s.eps_q16 > kMaxBeta) return fail(PC_EINVAL, "instance %d: eps_q16 out of range", i);
+        const pc_trace_desc &t = traces[s.trace];
+        pcr::DevInst &d = P.di[i];
+        std::memset(&d, 0, sizeof(d));
+        d.trace = s.trace;
+        d.policy = s.policy;
+        d.capacity = s.capacity;
+        d.flags = s.flags;
+        d.n_contracts = s.n_contracts;
+        d.eps = s.eps_q16;
+        int64_t rmin = 0;
+        for (int c = 0; c < s.n_contracts; ++c) {
+            if (s.contract[c].rho_q16 <= 0 || s.contract[c].rho_q16 > kMaxRho)
+                return fail(PC_EINVAL, "instance %d contract %d: rho_q16 must be in 1..2^40", i, c);
+            if (s.contract[c].beta_q16 < 0 || s.contract[c].beta_q16 > kMaxBeta)
+                return fail(PC_EINVAL, "instance %d contract %d: beta_q16 must be in 0..2^50", i, c);
+            d.rho[c] = s.contract[c].rho_q16;
+            d.beta[c] = s.contract[c].beta_q16;
+            if (c == 0 || d.rho[c] < rmin) rmin = d.rho[c];
+        }
+        for (int c = 0; c < s.n_contracts; ++c) d.invw[c] = (rmin << 16) / d.rho[c];   // 1/w_c in Q16
+        int64_t scap = (int64_t)s.capacity * s.s3_small_permille / 1000;
+        if (scap < 1) scap = 1;
+        d.s_cap = (int32_t)scap;
+        d.g_cap = (int32_t)(s.capacity - scap);
+        d.move_thr = s.s3_move_threshold;
+        const int64_t maxn = std::min<int64_t>(t.max_req_blocks, s.capacity);
+        d.maxn = (int32_t)maxn;
+        d.pool = (int32_t)(s.capacity + maxn);
+        if (d.pool > 65534) return fail(PC_EINVAL, "instance %d: capacity + largest request exceeds 65534", i);
+        const int64_t nb = std::max<int64_t>(2, (int64_t)1 << ceil_log2((d.pool * 3 + 15) / 16));
+        d.nb_log2 = ceil_log2(nb);
+        d.log_log2 = ceil_log2(s.capacity + maxn + 128);
+        d.rs_log2 = std::max(6, ceil_log2(2 * maxn));
+        if (s.policy == PC_S3FIFO && d.g_cap > 0) {
+            d.gnb_log2 = std::max(1, ceil_log2((d.g_cap * 3 + 15) / 16));
+            d.gr_log2 = ceil_log2((int64_t)d.g_cap + 64);
+        }
+        d.n_prefix_words = (int32_t)((t.n_prefix + 31) / 32);
+        // state region (identical layout in LDS or in the workspace)
+        int64_t so = 0;
+        auto take = [&](int64_t bytes) { int64_t o = so; so = align_up(so + bytes, 16); return (int32_t)o; };
+        d.o_key = take(8LL * d.pool);
+        d.o_stamp = take(4LL * d.pool);
+        d.o_meta = take(4LL * d.pool);
+        d.o_table = take(32LL << d.nb_log2);
+        d.o_evown = take(8LL * 64);
+        d.o_rset = take(4LL << d.rs_log2);
+        d.o_res = take(4LL * 64);
+        d.o_cnt = take(4LL * 192);
+        d.o_cur = take(4LL * 196);
+        d.o_tpos = take(2LL * d.pool);
+        d.o_free = take(2LL * d.pool);
+        d.o_log = take(2LL << d.log_log2);
+        d.o_posslot = take(2LL * std::max<int64_t>(maxn, 1));
+        d.state_bytes = (int32_t)so;
+        d.in_lds = so <= lds_cap ? 1 : 0;
+        (d.in_lds ? lds_ids : glb_ids).push_back(i);
+        if (d.in_lds) P.lds_bytes = std::max(P.lds_bytes, d.state_bytes);
+        cost[i] = (double)t.n_keys * (s.policy == PC_LRU ? 1.0 : 1.4) + (double)t.n_req * 16.0;
+        d.per_req_off = per_req;
+        per_req += 4 * t.n_req;
+    }
+    // global regions per instance
+    for (int i = 0; i < n_inst; ++i) {
+        pcr::DevInst &d = P.di[i];
+        if (!d.in_lds) { d.ws_state = off; off = align_up(off + d.state_bytes, 256); }
+        d.ws_bits = off;
+        off = align_up(off + 8LL * d.n_prefix_words, 256);
+        if (d.policy == PC_PREFIXSHIELD) { d.ws_pfx = off; off = align_up(off + 4LL * d.pool, 256); }
+        if (d.policy == PC_S3FIFO && d.g_cap > 0) {
+            d.ws_gtable = off;
+            off = align_up(off + (32LL << d.gnb_log2), 256);
+            d.ws_gring = off;
+            off = align_up(off + (8LL << d.gr_log2), 256);
+        }
+    }
+    P.ws_bytes = std::max<int64_t>(off, 256);
+    auto by_cost = [&](int32_t a, int32_t b) { return cost[a] > cost[b] || (cost[a] == cost[b] && a < b); };
+    std::sort(lds_ids.begin(), lds_ids.end(), by_cost);
+    std::sort(glb_ids.begin(), glb_ids.end(), by_cost);
+    P.order = lds_ids;
+    P.order.insert(P.order.end(), glb_ids.begin(), glb_ids.end());
+    P.n_lds = (int32_t)lds_ids.size();
+    return PC_OK;
+}
+
+// Pinned staging for descriptor uploads, reused once the previous copy is done.
+struct Staging {
+    std::mutex mu;
+    void *buf = nullptr;
+    size_t cap = 0;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+};
+Staging g_stage;
+
+}  // namespace
+
+extern "C" {
+
+const char *pc_last_error(void) { return g_err.c_str(); }
+
+int32_t pc_block_offsets(const int32_t *d_req_len, int64_t n_req, int32_t block_size, int64_t *d_key_off,
+                         void *stream) {
+    if (block_size != PC_BLOCK_TOKENS) return fail(PC_EUNSUPPORTED, "block_size %d (only 16)", block_size);
+    if (n_req < 0) return fail(PC_EINVAL, "n_req < 0");
+    if (!d_key_off || (n_req > 0 && !d_req_len)) return fail(PC_EINVAL, "null pointer");
+    hipError_t e = pcr::launch_block_offsets(d_req_len, n_req, d_key_off, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "block offsets launch");
+    return ok();
+}
+
+int32_t pc_hash_blocks(const int32_t *d_tokens, int64_t n_tokens, const int64_t *d_req_tok_off,
+                       const int32_t *d_req_len, const int32_t *d_req_ns, const int64_t *d_key_off, int64_t n_req,
+                       int32_t block_size, uint64_t *d_keys, int64_t n_keys, int32_t *d_status, void *stream) {
+    if (block_size != PC_BLOCK_TOKENS) return fail(PC_EUNSUPPORTED, "block_size %d (only 16)", block_size);
+    if (n_req < 0 || n_tokens < 0 || n_keys < 0) return fail(PC_EINVAL, "negative size");
+    if (!d_status) return fail(PC_EINVAL, "null status pointer");
+    if (n_req > 0 && (!d_req_tok_off || !d_req_len || !d_req_ns || !d_key_off))
+        return fail(PC_EINVAL, "null request array");
+    if (n_tokens > 0 && !d_tokens) return fail(PC_EINVAL, "null tokens");
+    if (n_keys > 0 && !d_keys) return fail(PC_EINVAL, "null keys");
+    if (((uintptr_t)d_tokens & 15) != 0) return fail(PC_EINVAL, "d_tokens must be 16-byte aligned");
+    hipError_t e = pcr::launch_hash(d_tokens, n_tokens, d_req_tok_off, d_req_len, d_req_ns, d_key_off, n_req, d_keys,
+                                    n_keys, d_status, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "hash launch");
+    return ok();
+}
+
+int64_t pc_replay_workspace_bytes(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst,
+                                  int32_t n_inst) {
+    Plan P;
+    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_limit(), P);
+    if (rc != PC_OK) return rc;
+    ok();
+    return P.ws_bytes;
+}
+
+int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst, int32_t n_inst,
+                        void *d_workspace, int64_t workspace_bytes, void *d_stats, int32_t *d_per_request,
+                        void *stream) {
+    Plan P;
+    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_limit(), P);
+    if (rc != PC_OK) return rc;
+    if (n_inst == 0) return ok();
+    if (!d_workspace || !d_stats) return fail(PC_EINVAL, "null workspace or stats");
+    if (((uintptr_t)d_workspace & 255) != 0) return fail(PC_EINVAL, "workspace must be 256-byte aligned");
+    if (workspace_bytes < P.ws_bytes)
+        return fail(PC_ENOMEM, "workspace %lld bytes < required %lld", (long long)workspace_bytes, (long long)P.ws_bytes);
+    hipStream_t s = (hipStream_t)stream;
+    uint8_t *ws = (uint8_t *)d_workspace;
+    const size_t o_inst = 0;
+    const size_t o_tr = align_up((int64_t)sizeof(pcr::DevInst) * n_inst, 256);
+    const size_t o_ord = align_up((int64_t)o_tr + (int64_t)sizeof(pcr::DevTrace) * n_traces, 256);
+    const size_t nbytes = (size_t)P.hdr_bytes;
+    {
+        std::lock_guard<std::mutex> lk(g_stage.mu);
+        hipError_t e;
+        if (g_stage.pending) {
+            e = hipEventSynchronize(g_stage.done);
+            if (e != hipSuccess) return hip_fail(e, "staging wait");
+            g_stage.pending = false;
+        }
+        if (g_stage.cap < nbytes) {
+            if (g_stage.buf) (void)hipHostFree(g_stage.buf);
+            g_stage.buf = nullptr;
+            g_stage.cap = 0;
+            e = hipHostMalloc(&g_stage.buf, nbytes, hipHostMallocDefault);
+            if (e != hipSuccess) return hip_fail(e, "pinned staging allocation");
+            g_stage.cap = nbytes;
+        }
+        if (!g_stage.done) {
+            e = hipEventCreateWithFlags(&g_stage.done, hipEventDisableTiming);
+            if (e != hipSuccess) return hip_fail(e, "event create");
+        }
+        uint8_t *h = (uint8_t *)g_stage.buf;
+        std::memset(h, 0, nbytes);
+        std::memcpy(h + o_inst, P.di.data(), sizeof(pcr::DevInst) * n_inst);
+        if (n_traces) std::memcpy(h + o_tr, P.dt.data(), sizeof(pcr::DevTrace) * n_traces);
+        std::memcpy(h + o_ord, P.order.data(), sizeof(int32_t) * n_inst);
+        e = hipMemcpyAsync(ws, h, nbytes, hipMemcpyHostToDevice, s);
+        if (e != hipSuccess) return hip_fail(e, "descriptor upload");
+        e = hipEventRecord(g_stage.done, s);
+        if (e != hipSuccess) return hip_fail(e, "event record");
+        g_stage.pending = true;
+    }
+    const pcr::DevInst *d_inst = (const pcr::DevInst *)(ws + o_inst);
+    const pcr::DevTrace *d_tr = (const pcr::DevTrace *)(ws + o_tr);
+    const int32_t *d_ord = (const int32_t *)(ws + o_ord);
+    hipError_t e;
+    if (P.n_lds > 0) {
+        e = pcr::launch_replay(d_inst, d_tr, d_ord, P.n_lds, P.lds_bytes, true, ws, (int64_t *)d_stats, d_per_request, s);
+        if (e != hipSuccess) return hip_fail(e, "replay launch (LDS)");
+    }
+    if (n_inst - P.n_lds > 0) {
+        e = pcr::launch_replay(d_inst, d_tr, d_ord + P.n_lds, n_inst - P.n_lds, 0, false, ws, (int64_t *)d_stats,
+                               d_per_request, s);
+        if (e != hipSuccess) return hip_fail(e, "replay launch (workspace)");
+    }
+    return ok();
+}
+
+int32_t pc_get_stats(const void *d_stats, int32_t n_inst, int32_t instance, pc_group_stats *groups_out,
+                     int32_t max_groups, pc_instance_stats *inst_out, void *stream) {
+    if (!d_stats || n_inst < 0) return fail(PC_EINVAL, "null stats or negative n_inst");
+    if (instance < -1 || instance >= n_inst) return fail(PC_EINVAL, "instance %d out of range", instance);
+    if (max_groups < 0 || max_groups > PC_MAX_GROUPS) return fail(PC_EINVAL, "max_groups outside 0..64");
+    if ((max_groups > 0 && !groups_out) || !inst_out) return fail(PC_EINVAL, "null output");
+    const int32_t first = instance < 0 ? 0 : instance;
+    const int32_t count = instance < 0 ? n_inst : 1;
+    std::vector<int64_t> buf((size_t)count * pcr::kRecordWords);
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+    if (count > 0) {
+        e = hipMemcpy(buf.data(), (const int64_t *)d_stats + (size_t)first * pcr::kRecordWords,
+                      buf.size() * sizeof(int64_t), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e, "stats copy");
+    }
+    for (int32_t i = 0; i < count; ++i) {
+        const int64_t *rec = buf.data() + (size_t)i * pcr::kRecordWords;
+        for (int32_t gidx = 0; gidx < max_groups; ++gidx) {
+            const int64_t *g = rec + gidx * pcr::kGroupFields;
+            pc_group_stats &o = groups_out[(size_t)i * max_groups + gidx];
+            o.requests = (uint64_t)g[0]; o.probes = (uint64_t)g[1]; o.hits = (uint64_t)g[2]; o.misses = (uint64_t)g[3];
+            o.charged = (uint64_t)g[4]; o.evicted_owned = (uint64_t)g[5]; o.evictions_caused = (uint64_t)g[6];
+            o.promotions = (uint64_t)g[7]; o.gated = (uint64_t)g[8]; o.orphans = (uint64_t)g[9];
+            o.dups = (uint64_t)g[10]; o.truncated = (uint64_t)g[11];
+            o.debt_end_q16 = g[12]; o.debt_max_q16 = g[13]; o.debt_sum_q16 = g[14];
+            o.resident_end = g[15]; o.resident_max = g[16];
+        }
+        const int64_t *q = rec + pcr::kInstOffset;
+        pc_instance_stats &o = inst_out[i];
+        o.evictions = (uint64_t)q[0]; o.s3_moves = (uint64_t)q[1]; o.s3_reinserts = (uint64_t)q[2];
+        o.s3_ghost_hits = (uint64_t)q[3]; o.s3_ghost_inserts = (uint64_t)q[4];
+        o.resident_end = q[5]; o.resident_max = q[6];
+        o.status = (int32_t)(uint32_t)q[7];
+        o.reserved = 0;
+    }
+    return ok();
+}
+
+}  // extern "C"
+
+static_assert(sizeof(pc_group_stats) == 136, "pc_group_stats layout");
+static_assert(sizeof(pc_instance_stats) == 64, "pc_instance_stats layout");
+static_assert(PC_STATS_RECORD_BYTES == pcr::kRecordWords * 8, "stats record size");

@@ -1,0 +1,265 @@
+// pc_hash.hip -- block cutting and chained block keys on gfx950.
+//
+// Block cutting (Sec. III-B: only full KV blocks count): request r owns
+// floor(len_r / 16) keys at CSR offset key_off[r].
+//
+// PCH64 keys (the paper keeps the engine's native content hash, Sec. III-A
+// and Sec. IV, so the key function is this library's own):
+//   d_k   = sum_{i<8} ((t[16k+2i] + K[2i]) mod 2^32) * ((t[16k+2i+1] + K[2i+1]) mod 2^32)
+//   c_k   = fmix64(d_k)
+//   H_k   = A * H_{k-1} + c_k  (mod 2^64),  H_-1 = fmix64(ns + 1)
+//   key_k = fmix64(H_k)
+// The chain is an affine recurrence, so a wavefront computes 64 consecutive
+// H_k with a log-step scan over lanes instead of a serial loop.
+#include "pc_internal.h"
+
+namespace pcr {
+
+namespace {
+
+__constant__ uint32_t kNH[16] = {
+    0x3504f334u, 0x5db3d743u, 0x1e3779bau, 0x52a7fa9eu,
+    0x28872940u, 0x4d82b447u, 0x0fc1ecd6u, 0x2df0668du,
+    0x65ddceafu, 0x314d1496u, 0x48ac80aeu, 0x0a97f66du,
+    0x33999334u, 0x475a2544u, 0x6d861707u, 0x23daa40fu};
+
+constexpr uint64_t kA = 0x9E3779B97F4A7C15ull;
+
+constexpr uint64_t pow_a(int e) {
+    uint64_t r = 1, b = kA;
+    while (e) {
+        if (e & 1) r *= b;
+        b *= b;
+        e >>= 1;
+    }
+    return r;
+}
+constexpr uint64_t kA1 = pow_a(1), kA2 = pow_a(2), kA4 = pow_a(4), kA8 = pow_a(8),
+                   kA16 = pow_a(16), kA32 = pow_a(32);
+
+__device__ __forceinline__ uint64_t fmix64(uint64_t z) {
+    z ^= z >> 33;
+    z *= 0xff51afd7ed558ccdull;
+    z ^= z >> 33;
+    z *= 0xc4ceb9fe1a85ec53ull;
+    z ^= z >> 33;
+    return z;
+}
+
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+    uint32_t lo = __shfl((int)(uint32_t)v, src);
+    uint32_t hi = __shfl((int)(uint32_t)(v >> 32), src);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int d) {
+    uint32_t lo = __shfl_up((int)(uint32_t)v, d);
+    uint32_t hi = __shfl_up((int)(uint32_t)(v >> 32), d);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+    uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+// x + x[quad_perm(ctrl)] within each group of 4 lanes (DPP, no LDS)
+template <int kCtrl>
+__device__ __forceinline__ uint64_t quad_add(uint64_t x) {
+    int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, kCtrl, 0xF, 0xF, false);
+    int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), kCtrl, 0xF, 0xF, false);
+    return x + (((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// 4 int32 starting at element e of `base` (16-byte aligned), zero beyond lim
+__device__ __forceinline__ uint4 load4(const int32_t *__restrict__ base, int64_t e, int64_t lim) {
+    if (e + 4 <= lim) return *reinterpret_cast<const uint4 *>(base + e);
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (e < lim) v.x = (uint32_t)base[e];
+    if (e + 1 < lim) v.y = (uint32_t)base[e + 1];
+    if (e + 2 < lim) v.z = (uint32_t)base[e + 2];
+    if (e + 3 < lim) v.w = (uint32_t)base[e + 3];
+    return v;
+}
+
+// ---------------------------------------------------------------- offsets
+constexpr int kScanChunk = 4096;
+constexpr int kScanThreads = 256;
+
+__device__ __forceinline__ int64_t nblocks_of(int32_t len) { return len > 0 ? (int64_t)(len / 16) : 0; }
+
+__device__ int64_t block_incl_scan(int64_t v, int64_t *sh /* [kScanThreads/64] */) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    for (int d = 1; d < 64; d <<= 1) {
+        int64_t u = (int64_t)shfl_up64((uint64_t)v, d);
+        if (lane >= d) v += u;
+    }
+    if (lane == 63) sh[w] = v;
+    __syncthreads();
+    int64_t add = 0;
+    for (int i = 0; i < w; ++i) add += sh[i];
+    __syncthreads();
+    return v + add;
+}
+
+// A: sum of chunk b -> key_off[min((b+1)*CH, n)]
+__global__ __launch_bounds__(kScanThreads) void offsets_reduce(const int32_t *__restrict__ len, int64_t n,
+                                                               int64_t *__restrict__ key_off) {
+    __shared__ int64_t sh[kScanThreads / 64];
+    const int64_t b = blockIdx.x, start = b * kScanChunk;
+    int64_t s = 0;
+    for (int i = threadIdx.x; i < kScanChunk; i += kScanThreads) {
+        int64_t e = start + i;
+        if (e < n) s += nblocks_of(len[e]);
+    }
+    s = block_incl_scan(s, sh);
+    if (threadIdx.x == kScanThreads - 1) {
+        int64_t pos = start + kScanChunk < n ? start + kScanChunk : n;
+        key_off[pos] = s;
+    }
+}
+
+// B: inclusive scan of the chunk sums in place; key_off[0] = 0
+__global__ __launch_bounds__(kScanThreads) void offsets_chunks(int64_t n, int64_t nchunks,
+                                                               int64_t *__restrict__ key_off) {
+    __shared__ int64_t sh[kScanThreads / 64];
+    __shared__ int64_t last;
+    int64_t carry = 0;
+    for (int64_t c0 = 0; c0 < nchunks; c0 += kScanThreads) {
+        int64_t c = c0 + threadIdx.x;
+        int64_t pos = 0;
+        int64_t v = 0;
+        if (c < nchunks) {
+            pos = (c + 1) * kScanChunk < n ? (c + 1) * kScanChunk : n;
+            v = key_off[pos];
+        }
+        int64_t incl = block_incl_scan(v, sh);
+        if (c < nchunks) key_off[pos] = carry + incl;
+        if (threadIdx.x == kScanThreads - 1) last = incl;
+        __syncthreads();
+        carry += last;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) key_off[0] = 0;
+}
+
+// C: exclusive scan inside each chunk, starting from the chunk's offset
+__global__ __launch_bounds__(kScanThreads) void offsets_fill(const int32_t *__restrict__ len, int64_t n,
+                                                             int64_t *__restrict__ key_off) {
+    __shared__ int64_t vals[kScanChunk];
+    __shared__ int64_t sh[kScanThreads / 64];
+    const int64_t b = blockIdx.x, start = b * kScanChunk;
+    const int64_t base_off = b == 0 ? 0 : key_off[start];
+    for (int i = threadIdx.x; i < kScanChunk; i += kScanThreads) {
+        int64_t e = start + i;
+        vals[i] = e < n ? nblocks_of(len[e]) : 0;
+    }
+    __syncthreads();
+    constexpr int kPer = kScanChunk / kScanThreads;
+    int64_t loc = 0;
+    for (int i = 0; i < kPer; ++i) loc += vals[threadIdx.x * kPer + i];
+    int64_t incl = block_incl_scan(loc, sh);
+    int64_t run = base_off + incl - loc;
+    for (int i = 0; i < kPer; ++i) {
+        int64_t v = vals[threadIdx.x * kPer + i];
+        vals[threadIdx.x * kPer + i] = run;
+        run += v;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kScanChunk; i += kScanThreads) {
+        int64_t e = start + i;
+        if (e < n) key_off[e] = vals[i];
+    }
+}
+
+// ---------------------------------------------------------------- keys
+constexpr int kHashWaves = 4;
+
+__global__ __launch_bounds__(64 * kHashWaves) void hash_kernel(
+    const int32_t *__restrict__ tokens, int64_t n_tokens, const int64_t *__restrict__ tok_off,
+    const int32_t *__restrict__ req_len, const int32_t *__restrict__ req_ns,
+    const int64_t *__restrict__ key_off, int64_t n_req, uint64_t *__restrict__ keys, int64_t n_keys,
+    int32_t *__restrict__ status) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * kHashWaves + (threadIdx.x >> 6);
+    if (r >= n_req) return;
+    const int64_t off = tok_off[r];
+    const int32_t len = req_len[r];
+    const int64_t ko = key_off[r];
+    const int64_t nb = len > 0 ? len / 16 : 0;
+    if (len < 0 || off < 0 || off + (int64_t)len > n_tokens || ko < 0 || ko + nb > n_keys) {
+        if (lane == 0) atomicExch(status, -1);
+        return;
+    }
+    if (nb == 0) return;
+    const int a = (int)(off & 3);                       // misalignment (wave-uniform)
+    const int32_t *base = tokens + (off - a);           // 16-byte aligned
+    const int64_t lim = n_tokens - (off - a);
+    const int r4 = lane & 3, bq = lane >> 2;
+    const uint32_t k0 = kNH[4 * r4], k1 = kNH[4 * r4 + 1], k2 = kNH[4 * r4 + 2], k3 = kNH[4 * r4 + 3];
+    uint64_t H = fmix64((uint64_t)(uint32_t)req_ns[r] + 1u);
+    const int src = 4 * (lane & 15) + (lane >> 4);      // lane holding block `lane`'s digest
+
+    for (int64_t it = 0; it < nb; it += 64) {
+        const int nblk = (int)((nb - it) < 64 ? (nb - it) : 64);
+        uint64_t dsel = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int blk = 16 * q + bq;                 // block within this 64-block step
+            uint64_t part = 0;
+            if (blk < nblk) {
+                const int64_t e = 16 * (it + blk) + 4 * r4;   // aligned element index
+                uint4 v = load4(base, e, lim);
+                uint32_t t0, t1, t2, t3;
+                if (a == 0) {
+                    t0 = v.x; t1 = v.y; t2 = v.z; t3 = v.w;
+                } else {
+                    uint4 w = load4(base, e + 4, lim);
+                    if (a == 1) { t0 = v.y; t1 = v.z; t2 = v.w; t3 = w.x; }
+                    else if (a == 2) { t0 = v.z; t1 = v.w; t2 = w.x; t3 = w.y; }
+                    else { t0 = v.w; t1 = w.x; t2 = w.y; t3 = w.z; }
+                }
+                part = (uint64_t)(t0 + k0) * (uint64_t)(t1 + k1) + (uint64_t)(t2 + k2) * (uint64_t)(t3 + k3);
+            }
+            part = quad_add<0xB1>(part);   // quad_perm [1,0,3,2]
+            part = quad_add<0x4E>(part);   // quad_perm [2,3,0,1]
+            if (q == r4) dsel = part;      // lane 4b+q keeps block 16q+b
+        }
+        const uint64_t c = fmix64(dsel);
+        uint64_t v = shfl64(c, src);       // lane L now holds c of block it+L
+        if (lane == 0) v += kA1 * H;
+        uint64_t u;
+        u = shfl_up64(v, 1);  if (lane >= 1)  v += kA1 * u;
+        u = shfl_up64(v, 2);  if (lane >= 2)  v += kA2 * u;
+        u = shfl_up64(v, 4);  if (lane >= 4)  v += kA4 * u;
+        u = shfl_up64(v, 8);  if (lane >= 8)  v += kA8 * u;
+        u = shfl_up64(v, 16); if (lane >= 16) v += kA16 * u;
+        u = shfl_up64(v, 32); if (lane >= 32) v += kA32 * u;
+        if (lane < nblk) keys[ko + it + lane] = fmix64(v);
+        H = readlane64(v, nblk - 1);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_block_offsets(const int32_t *len, int64_t n_req, int64_t *key_off, hipStream_t s) {
+    const int64_t nchunks = (n_req + kScanChunk - 1) / kScanChunk;
+    if (nchunks > 0) {
+        hipLaunchKernelGGL(offsets_reduce, dim3((unsigned)nchunks), dim3(kScanThreads), 0, s, len, n_req, key_off);
+    }
+    hipLaunchKernelGGL(offsets_chunks, dim3(1), dim3(kScanThreads), 0, s, n_req, nchunks, key_off);
+    if (nchunks > 0) {
+        hipLaunchKernelGGL(offsets_fill, dim3((unsigned)nchunks), dim3(kScanThreads), 0, s, len, n_req, key_off);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_hash(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_off, const int32_t *len,
+                       const int32_t *ns, const int64_t *key_off, int64_t n_req, uint64_t *keys,
+                       int64_t n_keys, int32_t *status, hipStream_t s) {
+    if (n_req <= 0) return hipSuccess;
+    const int64_t blocks = (n_req + kHashWaves - 1) / kHashWaves;
+    hipLaunchKernelGGL(hash_kernel, dim3((unsigned)blocks), dim3(64 * kHashWaves), 0, s, tokens, n_tokens,
+                       tok_off, len, ns, key_off, n_req, keys, n_keys, status);
+    return hipGetLastError();
+}
+
+}  // namespace pcr

@@ -1,0 +1,1072 @@
+// pc_replay.hip -- batched replay of multi-tenant prefix-cache instances on
+// gfx950, one 64-lane wavefront per instance.
+//
+// Per request (Alg. 1 hooks and Alg. 2 reclamation of the paper):
+//   OnRequest           prior-reference bit of (g,p), recorded
+//   lookup              longest leading run of resident blocks; later
+//                       repeats of a key inside the request are misses
+//   pin + OnTouch       S3-FIFO frequency, or the debt-gated promotion of
+//                       Eq. 4 using the debt before this request's charge
+//   reclamation         truly free slots first, then e victims: LRU order,
+//                       S3-FIFO small/main/ghost, or PrefixShield's
+//                       projected-debt argmax (Eqs. 5-8) with the
+//                       reuse-segmented order inside the group (Eq. 9)
+//   OnCacheFullBlocks   charge n_r (Eqs. 1-2), initial class, admission
+//   release             blocks back to the free queue, deepest first
+//   accounting          raw debt D_g (Eq. 3) and occupancy of every group
+//
+// State layout (one instance):
+//   key[pool] u64, stamp[pool] u32, meta[pool] u32, tpos[pool] u16,
+//   fstack[pool] u16   -- slots; pool = capacity + largest request
+//   table[8*NB] u32    -- 2-choice bucketized hash, entry = tag16 | slot16
+//   log[R] u16         -- free-queue log: slot of each appended entry; an
+//                         entry at absolute position q is live iff its slot
+//                         has the in-log bit and stamp == q
+//   posslot, rset      -- per-request position->slot map, duplicate set
+//   evown, res, cnt, cur -- per-group counters and queue cursors
+// It lives in dynamic LDS when it fits (capacities up to ~4K blocks) and in
+// the workspace otherwise; the code is the same, instantiated twice.
+//
+// All victims of one request are chosen in bulk: LRU takes the first e live
+// log entries with one ballot per 64 entries; PrefixShield turns the
+// per-victim argmax of Eq. 7 into runs (the winner keeps winning while its
+// projected debt stays above every other candidate's) and drains each run
+// from the group's per-segment cursors; S3-FIFO processes its queue heads
+// 64 at a time, cutting each batch where the sequential rule would switch
+// queues.  Each shortcut reproduces the one-victim-at-a-time definition
+// exactly.
+#include "pc_internal.h"
+
+namespace pcr {
+namespace {
+
+#define DEV __device__ __forceinline__
+
+constexpr int64_t kScale = 65536;
+
+DEV int lane_id() { return (int)__lane_id(); }
+DEV uint64_t ballot(bool p) { return __ballot(p); }
+DEV int popc(uint64_t m) { return __popcll(m); }
+DEV int mbcnt(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+DEV int first_lane(uint64_t m) { return __ffsll((unsigned long long)m) - 1; }   // m != 0
+DEV int last_lane(uint64_t m) { return 63 - __clzll((unsigned long long)m); }  // m != 0
+DEV void wsync() { __syncthreads(); }
+DEV uint32_t bcast32(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
+DEV int64_t bcast64(int64_t v, int l) {
+    uint32_t lo = bcast32((uint32_t)(uint64_t)v, l);
+    uint32_t hi = bcast32((uint32_t)((uint64_t)v >> 32), l);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+DEV int64_t xor64(int64_t v, int m) {
+    uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)(uint64_t)v, m);
+    uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)((uint64_t)v >> 32), m);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+DEV int64_t wave_max64(int64_t v) {
+    for (int m = 32; m; m >>= 1) { int64_t u = xor64(v, m); v = u > v ? u : v; }
+    return bcast64(v, 0);
+}
+DEV uint32_t wave_min32(uint32_t v) {
+    for (int m = 32; m; m >>= 1) { uint32_t u = (uint32_t)__shfl_xor((int)v, m); v = u < v ? u : v; }
+    return bcast32(v, 0);
+}
+DEV uint32_t wave_sum32(uint32_t v) {
+    for (int m = 32; m; m >>= 1) v += (uint32_t)__shfl_xor((int)v, m);
+    return bcast32(v, 0);
+}
+
+// Key -> (two buckets, 16-bit tag, duplicate-set home).  Keys are already
+// hash outputs, but the ABI accepts any uint64, so mix once more.
+struct TH {
+    uint32_t b1, b2, tag, rhome;
+};
+DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rsmask) {
+    uint64_t m = k ^ (k >> 31);
+    m *= 0x7fb5d329728ea185ull;
+    m ^= m >> 27;
+    m *= 0x81dadef4bc2dd44dull;
+    m ^= m >> 33;
+    TH h;
+    h.b1 = (uint32_t)m & nbmask;
+    h.b2 = (uint32_t)(m >> 20) & nbmask;
+    if (h.b2 == h.b1) h.b2 = h.b1 ^ 1u;
+    h.tag = (uint32_t)(m >> 48);
+    h.rhome = (uint32_t)(m >> 32) & rsmask;
+    return h;
+}
+
+DEV uint32_t owner_of(uint32_t mt) { return mt & kOwnerMask; }
+DEV uint32_t contract_of(uint32_t mt) { return (mt >> kContractShift) & 3u; }
+DEV uint32_t cls_of(uint32_t mt) { return (mt >> kClsShift) & 3u; }
+DEV uint32_t freq_of(uint32_t mt) { return (mt >> kFreqShift) & 3u; }
+
+template <bool kLds>
+struct Replayer {
+    // ---------------- configuration (wave-uniform)
+    const DevInst &I;
+    const DevTrace &T;
+    int policy, C, pool, flags, G, K, nseg;
+    int64_t eps;
+    uint32_t nbmask, rsmask, lmask, R, gnbmask, grmask;
+    int64_t s_cap, g_cap, move_thr;
+    int64_t rho[4], beta[4], invw[4];
+    // ---------------- arrays
+    uint64_t *key;
+    uint32_t *stamp, *meta, *table, *rset, *cnt, *cur, *res;
+    uint16_t *tpos, *fstack, *log, *posslot;
+    unsigned long long *evown;
+    uint32_t *pfx, *bits, *gtable;
+    uint64_t *gring;
+    // ---------------- uniform state
+    uint32_t head, tail;
+    int32_t top;            // free-stack size
+    int32_t resident;       // resident blocks (excludes blocks being created)
+    int32_t s_size, s_unp, m_unp;
+    uint32_t gseq, curS, curM;
+    int32_t rmax;
+    uint64_t ev_total, s3_moves, s3_reins, s3_ghits, s3_gins;
+    int32_t err;
+    // ---------------- per-lane group state (lane x = group x)
+    int64_t bal[4], last[4];
+    uint64_t c_req, c_probe, c_hit, c_miss, c_charged, c_evc, c_promo, c_gated, c_orph, c_dup, c_trunc;
+    int64_t d_max, d_sum;
+    int32_t r_max;
+
+    DEV Replayer(const DevInst &inst, const DevTrace &tr, uint8_t *sbase, uint8_t *ws) : I(inst), T(tr) {
+        policy = I.policy;
+        C = I.capacity;
+        pool = I.pool;
+        flags = I.flags;
+        G = T.n_groups;
+        K = I.n_contracts;
+        nseg = (policy == kPS && !(flags & kFlagNoSeg)) ? 3 : 1;
+        eps = I.eps;
+        nbmask = (1u << I.nb_log2) - 1u;
+        rsmask = (1u << I.rs_log2) - 1u;
+        R = 1u << I.log_log2;
+        lmask = R - 1u;
+        gnbmask = (1u << I.gnb_log2) - 1u;
+        grmask = (1u << I.gr_log2) - 1u;
+        s_cap = I.s_cap;
+        g_cap = I.g_cap;
+        move_thr = I.move_thr;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) { rho[c] = I.rho[c]; beta[c] = I.beta[c]; invw[c] = I.invw[c]; }
+        key = reinterpret_cast<uint64_t *>(sbase + I.o_key);
+        stamp = reinterpret_cast<uint32_t *>(sbase + I.o_stamp);
+        meta = reinterpret_cast<uint32_t *>(sbase + I.o_meta);
+        table = reinterpret_cast<uint32_t *>(sbase + I.o_table);
+        rset = reinterpret_cast<uint32_t *>(sbase + I.o_rset);
+        cnt = reinterpret_cast<uint32_t *>(sbase + I.o_cnt);
+        cur = reinterpret_cast<uint32_t *>(sbase + I.o_cur);
+        res = reinterpret_cast<uint32_t *>(sbase + I.o_res);
+        tpos = reinterpret_cast<uint16_t *>(sbase + I.o_tpos);
+        fstack = reinterpret_cast<uint16_t *>(sbase + I.o_free);
+        log = reinterpret_cast<uint16_t *>(sbase + I.o_log);
+        posslot = reinterpret_cast<uint16_t *>(sbase + I.o_posslot);
+        evown = reinterpret_cast<unsigned long long *>(sbase + I.o_evown);
+        pfx = reinterpret_cast<uint32_t *>(ws + I.ws_pfx);
+        bits = reinterpret_cast<uint32_t *>(ws + I.ws_bits);
+        gtable = reinterpret_cast<uint32_t *>(ws + I.ws_gtable);
+        gring = reinterpret_cast<uint64_t *>(ws + I.ws_gring);
+    }
+
+    // ============================================================ debt (lane x)
+    // Eq. 1, exactly: min(beta, B + rho*dt) with the product in 128 bits.
+    DEV int64_t eff(int c, int64_t t) const {
+        const int64_t dt = t - last[c];
+        const uint64_t gap = (uint64_t)(beta[c] - bal[c]);
+        const uint64_t lo = (uint64_t)rho[c] * (uint64_t)dt;
+        const uint64_t hi = __umul64hi((uint64_t)rho[c], (uint64_t)dt);
+        if (hi != 0 || lo >= gap) return beta[c];
+        return bal[c] + (int64_t)lo;
+    }
+    DEV int64_t raw_debt(int64_t t) const {   // Eq. 3
+        int64_t d = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if (c < K) { int64_t b = eff(c, t); if (b < 0) d -= b; }
+        return d;
+    }
+    DEV int64_t norm_debt(int64_t t) const {  // Eq. 5, 1/w_c in Q16
+        int64_t d = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if (c < K) {
+                int64_t b = eff(c, t);
+                if (b < 0) {
+                    uint64_t a = (uint64_t)(-b), w = (uint64_t)invw[c];
+                    uint64_t lo = a * w, hi = __umul64hi(a, w);
+                    d += (int64_t)((hi << 48) | (lo >> 16));
+                }
+            }
+        return d;
+    }
+    DEV int64_t decrement(int64_t t) const {  // Eq. 8: 1/W_g
+        int64_t m = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if (c < K && eff(c, t) < 0 && (m == 0 || invw[c] < m)) m = invw[c];
+        return m;
+    }
+
+    // ============================================================ free stack
+    DEV void free_push(bool p, uint32_t slot) {
+        const uint64_t m = ballot(p);
+        if (p) fstack[top + mbcnt(m)] = (uint16_t)slot;
+        top += popc(m);
+    }
+    DEV uint32_t free_pop(bool p) {
+        const uint64_t m = ballot(p);
+        uint32_t s = kNoSlot;
+        if (p) s = fstack[top - 1 - mbcnt(m)];
+        top -= popc(m);
+        return s;
+    }
+
+    // ============================================================ main table
+    DEV int tfind(uint64_t k, const TH &h, uint32_t &pos) const {
+        const uint4 *t4 = reinterpret_cast<const uint4 *>(table);
+        uint4 a0 = t4[2 * h.b1], a1 = t4[2 * h.b1 + 1], c0 = t4[2 * h.b2], c1 = t4[2 * h.b2 + 1];
+        uint32_t e[16] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w,
+                          c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            if (e[i] != kEmpty && (e[i] >> 16) == h.tag) {
+                uint32_t s = e[i] & 0xFFFFu;
+                if (key[s] == k) {
+                    pos = (i < 8 ? 8 * h.b1 + i : 8 * h.b2 + (i - 8));
+                    return (int)s;
+                }
+            }
+        }
+        return -1;
+    }
+    // Parallel insert of a new entry; false when both buckets are full.
+    DEV bool tinsert(uint32_t *tb, uint32_t val, const TH &h, uint32_t &pos) {
+        const uint4 *t4 = reinterpret_cast<const uint4 *>(tb);
+        uint4 a0 = t4[2 * h.b1], a1 = t4[2 * h.b1 + 1], c0 = t4[2 * h.b2], c1 = t4[2 * h.b2 + 1];
+        uint32_t e[16] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w,
+                          c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+        int n1 = 0, n2 = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) { n1 += e[i] == kEmpty; n2 += e[8 + i] == kEmpty; }
+        const bool second_first = n2 > n1;
+        for (int pass = 0; pass < 2; ++pass) {
+            const bool use2 = (pass == 0) == second_first;
+            const uint32_t b = use2 ? h.b2 : h.b1;
+            for (int w = 0; w < 8; ++w) {
+                if (e[(use2 ? 8 : 0) + w] != kEmpty) continue;
+                uint32_t old = atomicCAS(&tb[8 * b + w], kEmpty, val);
+                if (old == kEmpty) { pos = 8 * b + w; return true; }
+            }
+        }
+        return false;
+    }
+
+    // ============================================================ ghost (S3)
+    DEV bool gfind_clear(uint64_t k, const TH &h) {
+        for (int bi = 0; bi < 2; ++bi) {
+            const uint32_t b = bi ? h.b2 : h.b1;
+            for (int w = 0; w < 8; ++w) {
+                uint32_t e = gtable[8 * b + w];
+                if (e != kEmpty && (e >> 16) == h.tag && gring[e & grmask] == k) {
+                    gtable[8 * b + w] = kEmpty;
+                    return true;
+                }
+            }
+        }
+        return false;
+    }
+    DEV void gclear_exact(uint32_t val, const TH &h) {
+        for (int bi = 0; bi < 2; ++bi) {
+            const uint32_t b = bi ? h.b2 : h.b1;
+            for (int w = 0; w < 8; ++w)
+                if (gtable[8 * b + w] == val) { gtable[8 * b + w] = kEmpty; return; }
+        }
+    }
+    // Serial cuckoo displacement for an entry that found both buckets full.
+    template <bool kMain>
+    DEV bool kick(uint32_t val, uint64_t k) {
+        uint32_t *tb = kMain ? table : gtable;
+        const uint32_t msk = kMain ? nbmask : gnbmask;
+        uint32_t cv = val;
+        uint64_t ck = k;
+        uint32_t from = 0xFFFFFFFFu;
+        for (int it = 0; it < 512; ++it) {
+            TH h = thash(ck, msk, rsmask);
+            for (int bi = 0; bi < 2; ++bi) {
+                const uint32_t b = bi ? h.b2 : h.b1;
+                for (int w = 0; w < 8; ++w)
+                    if (tb[8 * b + w] == kEmpty) {
+                        tb[8 * b + w] = cv;
+                        if (kMain) tpos[cv & 0xFFFFu] = (uint16_t)(8 * b + w);
+                        return true;
+                    }
+            }
+            uint32_t b = (h.b1 == from) ? h.b2 : h.b1;
+            if (from == 0xFFFFFFFFu && (it & 1)) b = h.b2;
+            const uint32_t w = (uint32_t)(it * 5 + (ck >> 7)) & 7u;
+            const uint32_t victim = tb[8 * b + w];
+            tb[8 * b + w] = cv;
+            if (kMain) tpos[cv & 0xFFFFu] = (uint16_t)(8 * b + w);
+            cv = victim;
+            ck = kMain ? key[victim & 0xFFFFu] : gring[victim & grmask];
+            from = b;
+        }
+        return false;
+    }
+    // Run kicks for every lane of `over`, one lane at a time.
+    template <bool kMain>
+    DEV void kick_lanes(uint64_t over, uint32_t val, uint64_t k) {
+        wsync();
+        while (over) {
+            const int l = first_lane(over);
+            over &= over - 1;
+            const uint32_t v = bcast32(val, l);
+            const uint64_t kk = (uint64_t)bcast64((int64_t)k, l);
+            bool ok = true;
+            if (lane_id() == 0) ok = kick<kMain>(v, kk);
+            if (!bcast32(ok ? 1u : 0u, 0)) err = PC_EINTERNAL_CODE;
+            wsync();
+        }
+    }
+    static constexpr int32_t PC_EINTERNAL_CODE = -5;
+
+    // ============================================================ eviction core
+    DEV void evict_lanes(bool v, uint32_t s) {
+        if (v) {
+            const uint32_t mt = meta[s];
+            const uint32_t o = owner_of(mt);
+            atomicAdd(&evown[o], 1ull);
+            atomicSub(&res[o], 1u);
+            table[tpos[s]] = kEmpty;
+            meta[s] = 0;
+        }
+        const int nv = popc(ballot(v));
+        free_push(v, s);
+        resident -= nv;
+        ev_total += (uint64_t)nv;
+    }
+
+    // Compaction of the free-queue log: live entries keep their order and
+    // are renumbered from `head`; all cursors restart at `head`.
+    DEV void compact() {
+        wsync();
+        const int lane = lane_id();
+        uint32_t nw = head;
+        for (uint32_t p0 = head; p0 < tail; p0 += 64) {
+            const uint32_t pos = p0 + lane;
+            const bool valid = pos < tail;
+            uint32_t s = valid ? log[pos & lmask] : 0;
+            const bool live = valid && (meta[s] & kInLog) && stamp[s] == pos;
+            const uint64_t lm = ballot(live);
+            wsync();
+            if (live) {
+                const uint32_t np = nw + (uint32_t)mbcnt(lm);
+                log[np & lmask] = (uint16_t)s;
+                stamp[s] = np;
+            }
+            nw += (uint32_t)popc(lm);
+            wsync();
+        }
+        tail = nw;
+        if (policy == kPS)
+            for (int i = lane; i < 196; i += 64) cur[i] = head;
+        curS = curM = head;
+        wsync();
+    }
+    DEV void ensure_room(uint32_t k) {
+        if (tail + k - head <= R) return;
+        if (policy == kPS) {   // lowest cursor of a non-empty queue bounds every live entry
+            uint32_t m = tail;
+            for (int i = lane_id(); i < 192; i += 64) {
+                if (cnt[i] > 0 && cur[i] < m) m = cur[i];
+            }
+            m = wave_min32(m);
+            if (m > head) head = m;
+        } else if (policy == kS3) {
+            uint32_t m = curS < curM ? curS : curM;
+            if (m > head) head = m;
+        }
+        if (tail + k - head > R) compact();
+    }
+
+    // ---------------------------------------------------------------- LRU
+    DEV void evict_lru(int e) {
+        const int lane = lane_id();
+        int rem = e;
+        while (rem > 0 && err == 0) {
+            const uint32_t pos = head + lane;
+            const bool valid = pos < tail;
+            const uint32_t s = valid ? log[pos & lmask] : 0;
+            const bool live = valid && (meta[s] & kInLog) && stamp[s] == pos;
+            const uint64_t lm = ballot(live);
+            const bool v = live && mbcnt(lm) < rem;
+            const uint64_t vm = ballot(v);
+            const int nv = popc(vm);
+            wsync();
+            evict_lanes(v, s);
+            if (nv == rem) head = head + (uint32_t)last_lane(vm) + 1;
+            else head = (head + 64 < tail) ? head + 64 : tail;
+            rem -= nv;
+            if (nv == 0 && head >= tail) err = PC_EINTERNAL_CODE;
+            wsync();
+        }
+    }
+
+    // ---------------------------------------------------------------- PrefixShield
+    // Take k victims from queue (x, s) (x < 0: any owner) in free-queue order.
+    DEV void ps_take(int x, int s, int k) {
+        const int lane = lane_id();
+        const int ci = x >= 0 ? 3 * x + s : 192 + s;
+        uint32_t c = cur[ci];
+        int rem = k;
+        while (rem > 0 && err == 0) {
+            const uint32_t pos = c + lane;
+            const bool valid = pos < tail;
+            const uint32_t sl = valid ? log[pos & lmask] : 0;
+            const uint32_t mt = valid ? meta[sl] : 0;
+            const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
+            const bool match = live && (x < 0 || (int)owner_of(mt) == x) && (nseg == 1 || (int)cls_of(mt) == s);
+            const uint64_t mm = ballot(match);
+            const bool v = match && mbcnt(mm) < rem;
+            const uint64_t vm = ballot(v);
+            const int nv = popc(vm);
+            wsync();
+            if (v) atomicSub(&cnt[3 * owner_of(mt) + s], 1u);
+            evict_lanes(v, sl);
+            if (nv == rem) c = c + (uint32_t)last_lane(vm) + 1;
+            else c = (c + 64 < tail) ? c + 64 : tail;
+            rem -= nv;
+            if (nv == 0 && c >= tail) err = PC_EINTERNAL_CODE;
+            wsync();
+        }
+        if (lane == 0) cur[ci] = c;
+        wsync();
+    }
+    // Oldest live entry of queue (x, s); advances that queue's cursor to it.
+    DEV uint32_t ps_headpos(int x, int s) {
+        const int lane = lane_id();
+        const int ci = 3 * x + s;
+        uint32_t c = cur[ci];
+        uint32_t found = 0xFFFFFFFFu;
+        while (c < tail) {
+            const uint32_t pos = c + lane;
+            const bool valid = pos < tail;
+            const uint32_t sl = valid ? log[pos & lmask] : 0;
+            const uint32_t mt = valid ? meta[sl] : 0;
+            const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
+            const bool match = live && (int)owner_of(mt) == x && (nseg == 1 || (int)cls_of(mt) == s);
+            const uint64_t mm = ballot(match);
+            if (mm) { found = c + (uint32_t)first_lane(mm); c = found; break; }
+            c = (c + 64 < tail) ? c + 64 : tail;
+        }
+        wsync();
+        if (lane == 0) cur[ci] = c;
+        wsync();
+        return found;
+    }
+    DEV void evict_ps(int e, int64_t t) {
+        const int lane = lane_id();
+        const bool grp = lane < G;
+        int64_t P = 0, D = 0;
+        uint32_t avail = 0;
+        if (grp) {
+            P = norm_debt(t);
+            D = decrement(t);
+            avail = cnt[3 * lane] + cnt[3 * lane + 1] + cnt[3 * lane + 2];
+        }
+        int rem = e;
+        while (rem > 0 && err == 0) {
+            const bool inE = grp && avail > 0 && P > eps;      // Eq. 6
+            const uint64_t Em = ballot(inE);
+            if (!Em) break;
+            const int64_t pm = wave_max64(inE ? P : -1);       // Eq. 7
+            uint64_t tied = ballot(inE && P == pm);
+            int gs;
+            if (popc(tied) == 1) {
+                gs = first_lane(tied);
+            } else {   // ties: lowest non-empty segment, then oldest head entry
+                uint32_t seg = 3;
+                if (grp) {
+                    for (int s = nseg - 1; s >= 0; --s)
+                        if (cnt[3 * lane + s] > 0) seg = (uint32_t)s;
+                }
+                const uint32_t mseg = wave_min32(((tied >> lane) & 1) ? seg : 3u);
+                tied &= ballot(seg == mseg);
+                if (popc(tied) == 1) {
+                    gs = first_lane(tied);
+                } else {
+                    uint32_t best = 0xFFFFFFFFu;
+                    gs = first_lane(tied);
+                    for (uint64_t tm = tied; tm; tm &= tm - 1) {
+                        const int x = first_lane(tm);
+                        const uint32_t hp = ps_headpos(x, (int)mseg);
+                        if (hp < best) { best = hp; gs = x; }
+                    }
+                }
+            }
+            const int64_t Pg = bcast64(P, gs), Dg = bcast64(D, gs);
+            const int ag = (int)bcast32(avail, gs);
+            const int64_t p2 = wave_max64((inE && lane != gs) ? P : -1);
+            const int64_t thr = p2 > eps ? p2 : eps;
+            // picks g* keeps winning strictly: P - i*D > max(second, eps)
+            int64_t k1 = Pg > thr ? (Pg - thr + Dg - 1) / Dg : 0;
+            int64_t k = k1 > 1 ? k1 : 1;
+            if (k > rem) k = rem;
+            if (k > ag) k = ag;
+            int kk = (int)k;
+            for (int s = 0; s < nseg && kk > 0; ++s) {
+                const int cs = (int)(nseg == 1 ? (cnt[3 * gs] + cnt[3 * gs + 1] + cnt[3 * gs + 2])
+                                               : cnt[3 * gs + s]);
+                const int tk = cs < kk ? cs : kk;
+                if (tk > 0) {
+                    if (nseg == 1) ps_take_noseg(gs, tk);
+                    else ps_take(gs, s, tk);
+                }
+                kk -= tk;
+            }
+            if (lane == gs) {
+                P -= k * Dg;
+                if (P < 0) P = 0;
+                avail -= (uint32_t)k;
+            }
+            rem -= (int)k;
+        }
+        // no indebted candidate owner: global segment order (Eq. 9 fallback)
+        for (int s = 0; s < nseg && rem > 0 && err == 0; ++s) {
+            uint32_t cs = 0;
+            if (grp) cs = nseg == 1 ? cnt[3 * lane] + cnt[3 * lane + 1] + cnt[3 * lane + 2] : cnt[3 * lane + s];
+            const int tot = (int)wave_sum32(cs);
+            const int tk = tot < rem ? tot : rem;
+            if (tk > 0) {
+                if (nseg == 1) ps_take_any_noseg(tk);
+                else ps_take(-1, s, tk);
+            }
+            rem -= tk;
+        }
+        if (rem > 0) err = PC_EINTERNAL_CODE;
+    }
+    // Without segmentation the group queue holds every class.
+    DEV void ps_take_noseg(int x, int k) { ps_take_filtered(x, k, 3 * x); }
+    DEV void ps_take_any_noseg(int k) { ps_take_filtered(-1, k, 192); }
+    DEV void ps_take_filtered(int x, int k, int ci) {
+        const int lane = lane_id();
+        uint32_t c = cur[ci];
+        int rem = k;
+        while (rem > 0 && err == 0) {
+            const uint32_t pos = c + lane;
+            const bool valid = pos < tail;
+            const uint32_t sl = valid ? log[pos & lmask] : 0;
+            const uint32_t mt = valid ? meta[sl] : 0;
+            const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
+            const bool match = live && (x < 0 || (int)owner_of(mt) == x);
+            const uint64_t mm = ballot(match);
+            const bool v = match && mbcnt(mm) < rem;
+            const uint64_t vm = ballot(v);
+            const int nv = popc(vm);
+            wsync();
+            if (v) atomicSub(&cnt[3 * owner_of(mt)], 1u);   // single segment: counted at index 0
+            evict_lanes(v, sl);
+            if (nv == rem) c = c + (uint32_t)last_lane(vm) + 1;
+            else c = (c + 64 < tail) ? c + 64 : tail;
+            rem -= nv;
+            if (nv == 0 && c >= tail) err = PC_EINTERNAL_CODE;
+            wsync();
+        }
+        if (lane == 0) cur[ci] = c;
+        wsync();
+    }
+
+    // ---------------------------------------------------------------- S3-FIFO
+    // Ghost insertion of the keys of lanes `v`, in lane order.  The ghost
+    // keeps the last g_cap insertions: entries older than the batch that
+    // leave the window are removed, and batch entries that would already
+    // have left it by the batch's end are never inserted.
+    DEV void ghost_insert(bool v, uint64_t k) {
+        const uint64_t vm = ballot(v);
+        const int nv = popc(vm);
+        s3_gins += (uint64_t)nv;
+        if (g_cap > 0 && nv > 0) {
+            const uint32_t seq = gseq + (uint32_t)mbcnt(vm);
+            const uint32_t gend = gseq + (uint32_t)nv;
+            if (v && (int64_t)seq >= g_cap) {
+                const uint32_t x = seq - (uint32_t)g_cap;
+                if (x < gseq) {
+                    const uint32_t xp = x & grmask;
+                    const uint64_t kx = gring[xp];
+                    const TH hx = thash(kx, gnbmask, rsmask);
+                    gclear_exact((hx.tag << 16) | xp, hx);
+                }
+            }
+            wsync();
+            const bool ins = v && (int64_t)seq + g_cap >= (int64_t)gend;
+            const TH h = thash(k, gnbmask, rsmask);
+            const uint32_t val = (h.tag << 16) | (seq & grmask);
+            bool ok = true;
+            uint32_t pos;
+            if (v) gring[seq & grmask] = k;
+            if (ins) ok = tinsert(gtable, val, h, pos);
+            const uint64_t over = ballot(ins && !ok);
+            if (over) kick_lanes<false>(over, val, k);
+            wsync();
+        }
+        gseq += (uint32_t)nv;
+    }
+    DEV void evict_s3(int e) {
+        const int lane = lane_id();
+        const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+        int rem = e;
+        uint32_t spS = curS, spM = curM;
+        uint32_t keptS = 0xFFFFFFFFu, keptM = 0xFFFFFFFFu;
+        while (rem > 0 && err == 0) {
+            if (tail + 64 - head > R) {
+                ensure_room(64);
+                spS = curS; spM = curM;
+                keptS = keptM = 0xFFFFFFFFu;
+            }
+            const bool useS = (s_size >= s_cap && s_unp > 0) || (m_unp == 0);
+            const uint32_t sp = useS ? spS : spM;
+            const uint32_t lim = tail;
+            if (sp >= lim) { err = PC_EINTERNAL_CODE; break; }
+            const uint32_t pos = sp + lane;
+            const bool valid = pos < lim;
+            const uint32_t sl = valid ? log[pos & lmask] : 0;
+            const uint32_t mt = valid ? meta[sl] : 0;
+            const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
+            const bool inQ = live && (useS ? !(mt & kQMain) : (mt & kQMain) != 0);
+            const bool cand = inQ && !(mt & kPin);
+            const uint64_t candm = ballot(cand);
+            const int crk = mbcnt(candm);
+            const uint32_t f = freq_of(mt);
+            bool ok;
+            bool mv = false;
+            if (useS) {
+                mv = cand && (int64_t)f >= move_thr;
+                const uint64_t mvm = ballot(mv);
+                const int mb = popc(mvm & below);
+                const int eb = popc(candm & ~mvm & below);
+                const bool useS_i = ((int64_t)(s_size - crk) >= s_cap && (s_unp - crk) > 0) || (m_unp + mb == 0);
+                ok = cand && useS_i && eb < rem;
+            } else {
+                mv = cand && f > 0;   // reinsertion
+                const uint64_t mvm = ballot(mv);
+                const int eb = popc(candm & ~mvm & below);
+                ok = cand && eb < rem && (m_unp - eb) > 0;
+            }
+            const uint64_t bad = candm & ~ballot(ok);
+            const int stop = bad ? first_lane(bad) : 64;
+            const bool proc = cand && lane < stop;
+            const bool pmove = proc && mv, pev = proc && !mv;
+            const uint64_t pmm = ballot(pmove), pem = ballot(pev);
+            const int nmv = popc(pmm), nev = popc(pem);
+            // live entries of this queue that stay behind the scan point
+            const uint64_t keptm = ballot(inQ && !proc && lane < stop);
+            const uint64_t stopm = bad ? (1ull << stop) : 0ull;
+            const uint64_t km = keptm | stopm;
+            if (km) {
+                const uint32_t kp = sp + (uint32_t)first_lane(km);
+                if (useS) { if (kp < keptS) keptS = kp; } else { if (kp < keptM) keptM = kp; }
+            }
+            wsync();
+            // moves / reinsertions: append to the log tail in queue order
+            if (pmove) {
+                const uint32_t np = tail + (uint32_t)mbcnt(pmm);
+                log[np & lmask] = (uint16_t)sl;
+                stamp[sl] = np;
+                uint32_t m2 = mt & ~(3u << kFreqShift);
+                if (useS) m2 |= kQMain;
+                else m2 |= (f - 1) << kFreqShift;
+                meta[sl] = m2;
+            }
+            tail += (uint32_t)nmv;
+            if (useS) {
+                ghost_insert(pev, key[sl]);
+                s_size -= nmv + nev;
+                s_unp -= nmv + nev;
+                m_unp += nmv;
+                s3_moves += (uint64_t)nmv;
+            } else {
+                m_unp -= nev;
+                s3_reins += (uint64_t)nmv;
+            }
+            evict_lanes(pev, sl);
+            rem -= nev;
+            const uint32_t adv = stop < 64 ? (uint32_t)stop : ((lim - sp) < 64 ? (lim - sp) : 64u);
+            if (adv == 0) err = PC_EINTERNAL_CODE;   // a scan that cannot advance is a bug, never a hang
+            if (useS) spS = sp + adv; else spM = sp + adv;
+            wsync();
+        }
+        curS = keptS < spS ? keptS : spS;
+        curM = keptM < spM ? keptM : spM;
+        const uint32_t m = curS < curM ? curS : curM;
+        if (m > head) head = m;
+    }
+
+    // ============================================================ one request
+    DEV bool request(int64_t r, int64_t &tprev) {
+        const int lane = lane_id();
+        const int g = T.group[r];
+        const int c = T.contract[r];
+        const uint32_t p = T.prefix[r];
+        const int64_t t = T.tick ? T.tick[r] : r;
+        const int64_t ko = T.key_off[r];
+        const int64_t nfull = T.key_off[r + 1] - ko;
+        if (g >= G || c >= K || (int64_t)p >= T.n_prefix || ko < 0 || nfull < 0 ||
+            ko + nfull > T.n_keys || nfull > T.max_req_blocks || t < 0 || t < tprev)
+            return false;
+        tprev = t;
+        const int n = (int)(nfull < C ? nfull : C);
+        const bool me = lane == g;
+
+        // ---- OnRequest (Alg. 1): prior reference of (g,p), then record it
+        const uint32_t w = p >> 5, bit = 1u << (p & 31);
+        const uint32_t refw = bits[w], admw = bits[I.n_prefix_words + w];
+        const bool q1 = (refw & bit) != 0, adm = (admw & bit) != 0;
+        if (lane == 0 && !q1) bits[w] = refw | bit;
+        if (me) { c_req += 1; c_probe += (uint64_t)n; c_trunc += (uint64_t)(nfull - n); }
+        const bool proven = q1 && adm;
+        int64_t dg = 0;
+        if (policy == kPS) dg = bcast64(me ? raw_debt(t) : 0, g);   // before this request's charge
+        const bool gate_open = dg <= eps || (flags & kFlagNoGate);
+
+        // ---- lookup, duplicates, pin + OnTouch, orphans, new slots
+        for (uint32_t i = lane; i <= rsmask; i += 64) rset[i] = kEmpty;
+        wsync();
+        int hend = n, nhit = 0, nnew = 0, ndup = 0, norph = 0;
+        int npromo = 0, ngated = 0;
+        for (int base = 0; base < n; base += 64) {
+            const int j = base + lane;
+            const bool act = j < n;
+            const uint64_t k = act ? T.keys[ko + j] : 0ull;
+            const TH h = thash(k, nbmask, rsmask);
+            const uint32_t mine = (h.tag << 16) | (uint32_t)j;
+            uint32_t rpos = 0;
+            if (act) {   // first occurrence in the request keeps the smallest position
+                uint32_t idx = h.rhome;
+                for (;;) {
+                    const uint32_t old = atomicCAS(&rset[idx], kEmpty, mine);
+                    if (old == kEmpty) { rpos = idx; break; }
+                    if ((old >> 16) == h.tag && T.keys[ko + (old & 0xFFFFu)] == k) {
+                        atomicMin(&rset[idx], mine);
+                        rpos = idx;
+                        break;
+                    }
+                    idx = (idx + 1) & rsmask;
+                }
+            }
+            wsync();
+            const bool dup = act && rset[rpos] != mine;
+            const bool nd = act && !dup;
+            uint32_t tp = 0;
+            const int fs = nd ? tfind(k, h, tp) : -1;
+            const bool found = fs >= 0;
+            const uint64_t missm = ballot(nd && !found);
+            if (hend == n && missm) hend = base + first_lane(missm);
+            const bool isHit = found && j < hend;
+            const bool isOrph = found && j >= hend;
+            const bool isNew = nd && !found;
+            const uint32_t slot = (uint32_t)fs;
+            uint32_t mt = (found) ? meta[slot] : 0u;
+            // Eq. 4: proven reuse of a block matching (g, c, p), not yet REUSE
+            bool elig = false;
+            if (policy == kPS && isHit && proven && (int)owner_of(mt) == g && (int)contract_of(mt) == c &&
+                cls_of(mt) != (uint32_t)kReuse)
+                elig = pfx[slot] == p;
+            if (policy == kPS) {
+                const int ne = popc(ballot(elig));
+                if (gate_open) npromo += ne; else ngated += ne;
+            }
+            // hits: pin, touch
+            if (isHit) {
+                uint32_t m2 = mt | kPin;
+                if (policy == kS3) {
+                    const uint32_t f = freq_of(mt);
+                    m2 = (m2 & ~(3u << kFreqShift)) | ((f < 3 ? f + 1 : 3u) << kFreqShift);
+                } else {
+                    m2 &= ~kInLog;
+                    if (policy == kPS) {
+                        atomicSub(&cnt[3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt))], 1u);
+                        if (elig && gate_open) m2 = (m2 & ~(3u << kClsShift)) | ((uint32_t)kReuse << kClsShift);
+                    }
+                }
+                meta[slot] = m2;
+                posslot[j] = (uint16_t)slot;
+            }
+            if (policy == kS3) {
+                const bool inM = (mt & kQMain) != 0;
+                s_unp -= popc(ballot(isHit && !inM));
+                m_unp -= popc(ballot(isHit && inM));
+                s_unp -= popc(ballot(isOrph && !inM));
+                m_unp -= popc(ballot(isOrph && inM));
+                s_size -= popc(ballot(isOrph && !inM));
+            }
+            // orphans: the old block leaves, its slot is reused for the new one
+            if (isOrph) {
+                const uint32_t o = owner_of(mt);
+                atomicSub(&res[o], 1u);
+                if (policy == kPS) atomicSub(&cnt[3 * o + (nseg == 1 ? 0u : cls_of(mt))], 1u);
+                meta[slot] = kPin;
+                posslot[j] = (uint16_t)slot;
+            }
+            const int no = popc(ballot(isOrph));
+            norph += no;
+            resident -= no;
+            // brand-new keys: a free slot and a table entry
+            const uint32_t ns = free_pop(isNew);
+            uint32_t tpn = 0;
+            bool ok = true;
+            if (isNew) {
+                key[ns] = k;
+                meta[ns] = kPin;
+                posslot[j] = (uint16_t)ns;
+                ok = tinsert(table, (h.tag << 16) | ns, h, tpn);
+                if (ok) tpos[ns] = (uint16_t)tpn;
+            }
+            const uint64_t over = ballot(isNew && !ok);
+            if (over) kick_lanes<true>(over, (h.tag << 16) | ns, k);
+            if (act && dup) posslot[j] = kNoSlot;
+            nhit += popc(ballot(isHit));
+            nnew += popc(ballot(isNew)) + no;
+            ndup += popc(ballot(act && dup));
+            wsync();
+        }
+        const int h = nhit, m = nnew;
+        if (me) {
+            c_hit += (uint64_t)h;
+            c_miss += (uint64_t)(n - h);
+            c_dup += (uint64_t)ndup;
+            c_orph += (uint64_t)norph;
+            c_promo += (uint64_t)npromo;
+            c_gated += (uint64_t)ngated;
+        }
+
+        // ---- reclamation (Alg. 2): truly free blocks first
+        int e = m - (C - resident);
+        if (e < 0) e = 0;
+        if (e > 0) {
+            if (policy == kLRU) evict_lru(e);
+            else if (policy == kPS) evict_ps(e, t);
+            else evict_s3(e);
+        }
+        if (me) c_evc += (uint64_t)e;
+
+        // ---- OnCacheFullBlocks: charge n_r = m (Eq. 2), class, admission
+        uint32_t cls_new = kNormal;
+        if (m > 0) {
+            uint32_t cl = 0;
+            if (me) {
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc)
+                    if (cc == c) {
+                        const int64_t B = eff(cc, t) - (int64_t)m * kScale;
+                        bal[cc] = B;
+                        last[cc] = t;
+                        cl = (B < -eps || !adm) ? (uint32_t)kProb : (uint32_t)kNormal;
+                    }
+                c_charged += (uint64_t)m;
+            }
+            cls_new = bcast32(cl, g);
+            if (lane == 0 && !adm) bits[I.n_prefix_words + w] = admw | bit;
+        }
+
+        // ---- insert the new blocks (deepest first in queue order)
+        if (policy == kS3 && m > 0) ensure_room((uint32_t)m);
+        const uint32_t mbase = ((uint32_t)g) | ((uint32_t)c << kContractShift) | (cls_new << kClsShift) | kRes | kPin;
+        int before = 0;
+        int n_ins_S = 0, n_ins_M = 0;
+        for (int base = hend; base < n; base += 64) {
+            const int j = base + lane;
+            const bool act = j < n;
+            const uint32_t slot = act ? posslot[j] : kNoSlot;
+            const bool nw = act && slot != kNoSlot;
+            const uint64_t nm = ballot(nw);
+            if (nw) {
+                meta[slot] = mbase;
+                if (policy == kPS) pfx[slot] = p;
+            }
+            if (policy == kS3) {
+                bool gh = false;
+                const uint64_t kk = nw ? key[slot] : 0ull;
+                if (nw && g_cap > 0) gh = gfind_clear(kk, thash(kk, gnbmask, rsmask));
+                const uint32_t rank = (uint32_t)(m - 1 - (before + mbcnt(nm)));
+                if (nw) {
+                    const uint32_t np = tail + rank;
+                    log[np & lmask] = (uint16_t)slot;
+                    stamp[slot] = np;
+                    meta[slot] = mbase | kInLog | (gh ? kQMain : 0u);
+                }
+                const int ng = popc(ballot(nw && gh));
+                n_ins_M += ng;
+                n_ins_S += popc(nm) - ng;
+            }
+            before += popc(nm);
+            wsync();
+        }
+        if (m > 0) {
+            if (lane == 0) atomicAdd(&res[g], (uint32_t)m);
+            resident += m;
+            if (policy == kS3) {
+                tail += (uint32_t)m;
+                s_size += n_ins_S;
+                s3_ghits += (uint64_t)n_ins_M;
+            }
+        }
+        wsync();
+
+        // ---- release: back to the free queue, deepest first
+        const int nrel = n - ndup;
+        if (policy != kS3 && nrel > 0) ensure_room((uint32_t)nrel);
+        int seen = 0;
+        for (int base = 0; base < n; base += 64) {
+            const int j = base + lane;
+            const bool act = j < n;
+            const uint32_t slot = act ? posslot[j] : kNoSlot;
+            const bool rl = act && slot != kNoSlot;
+            const uint64_t rm = ballot(rl);
+            uint32_t mt = rl ? meta[slot] : 0u;
+            if (policy == kS3) {
+                const bool inM = (mt & kQMain) != 0;
+                if (rl) meta[slot] = mt & ~kPin;
+                s_unp += popc(ballot(rl && !inM));
+                m_unp += popc(ballot(rl && inM));
+            } else if (rl) {
+                const uint32_t np = tail + (uint32_t)(nrel - 1 - (seen + mbcnt(rm)));
+                log[np & lmask] = (uint16_t)slot;
+                stamp[slot] = np;
+                meta[slot] = (mt & ~kPin) | kInLog | kRes;
+                if (policy == kPS) atomicAdd(&cnt[3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt))], 1u);
+            }
+            seen += popc(rm);
+        }
+        if (policy != kS3) tail += (uint32_t)nrel;
+        wsync();
+
+        // ---- accounting for every group
+        if (lane < G) {
+            const int64_t d = raw_debt(t);
+            d_sum = (int64_t)((uint64_t)d_sum + (uint64_t)d);
+            if (d > d_max) d_max = d;
+            const int32_t rr = (int32_t)res[lane];
+            if (rr > r_max) r_max = rr;
+        }
+        if (resident > rmax) rmax = resident;
+        last_h = h; last_m = m; last_e = e; last_o = norph;
+        return true;
+    }
+    int last_h, last_m, last_e, last_o;
+
+    // ============================================================ run
+    DEV void init() {
+        const int lane = lane_id();
+        const uint32_t nte = 8u * (nbmask + 1u);
+        for (uint32_t i = lane; i < nte; i += 64) table[i] = kEmpty;
+        for (int i = lane; i < pool; i += 64) {
+            meta[i] = 0;
+            fstack[i] = (uint16_t)(pool - 1 - i);
+        }
+        for (int i = lane; i < 64; i += 64) { evown[i] = 0ull; res[i] = 0u; }
+        for (int i = lane; i < 196; i += 64) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
+        for (int i = lane; i < 2 * I.n_prefix_words; i += 64) bits[i] = 0u;
+        if (policy == kS3) {
+            const uint32_t nge = 8u * (gnbmask + 1u);
+            for (uint32_t i = lane; i < nge; i += 64) gtable[i] = kEmpty;
+        }
+        head = tail = 0;
+        top = pool;
+        resident = 0;
+        s_size = s_unp = m_unp = 0;
+        gseq = curS = curM = 0;
+        rmax = 0;
+        ev_total = s3_moves = s3_reins = s3_ghits = s3_gins = 0;
+        err = 0;
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) { bal[cc] = cc < K ? beta[cc] : 0; last[cc] = 0; }
+        c_req = c_probe = c_hit = c_miss = c_charged = c_evc = c_promo = c_gated = c_orph = c_dup = c_trunc = 0;
+        d_max = d_sum = 0;
+        r_max = 0;
+        wsync();
+    }
+
+    DEV void run(int64_t *st, int32_t *per_req) {
+        init();
+        const int lane = lane_id();
+        int32_t status = 0;
+        int64_t tprev = 0, tlast = 0;
+        const int64_t nreq = T.n_req;
+        for (int64_t r = 0; r < nreq; ++r) {
+            if (!request(r, tprev)) { status = -1; break; }
+            if (err) { status = err; break; }
+            tlast = tprev;
+            if (per_req && I.per_req_off >= 0 && lane == 0) {
+                int32_t *o = per_req + I.per_req_off + 4 * r;
+                o[0] = last_h; o[1] = last_m; o[2] = last_e; o[3] = last_o;
+            }
+        }
+        wsync();
+        // stats record: 64 groups x 17 int64, then the instance block
+        const bool ok = status == 0;
+        const bool grp = lane < G;
+        int64_t *o = st + lane * kGroupFields;
+        const int64_t dend = (grp && ok && nreq > 0) ? raw_debt(tlast) : 0;
+        const uint64_t ev_own = grp ? evown[lane] : 0ull;
+        const uint32_t rr = grp ? res[lane] : 0u;
+        int64_t v[kGroupFields] = {(int64_t)c_req, (int64_t)c_probe, (int64_t)c_hit, (int64_t)c_miss,
+                                   (int64_t)c_charged, (int64_t)ev_own, (int64_t)c_evc, (int64_t)c_promo,
+                                   (int64_t)c_gated, (int64_t)c_orph, (int64_t)c_dup, (int64_t)c_trunc,
+                                   dend, d_max, d_sum, (int64_t)rr, (int64_t)r_max};
+#pragma unroll
+        for (int f = 0; f < kGroupFields; ++f) o[f] = (ok && grp) ? v[f] : 0;
+        if (lane == 0) {
+            int64_t *q = st + kInstOffset;
+            q[0] = ok ? (int64_t)ev_total : 0;
+            q[1] = ok ? (int64_t)s3_moves : 0;
+            q[2] = ok ? (int64_t)s3_reins : 0;
+            q[3] = ok ? (int64_t)s3_ghits : 0;
+            q[4] = ok ? (int64_t)s3_gins : 0;
+            q[5] = ok ? (int64_t)resident : 0;
+            q[6] = ok ? (int64_t)rmax : 0;
+            q[7] = (int64_t)(uint32_t)status;   // status in the low 32 bits
+        }
+    }
+};
+
+template <bool kLds>
+__global__ __launch_bounds__(64) void replay_kernel(const DevInst *__restrict__ insts,
+                                                    const DevTrace *__restrict__ traces,
+                                                    const int32_t *__restrict__ order, uint8_t *ws,
+                                                    int64_t *stats, int32_t *per_req) {
+    extern __shared__ __align__(16) uint8_t smem[];
+    const int id = order[blockIdx.x];
+    const DevInst &I = insts[id];
+    const DevTrace &T = traces[I.trace];
+    uint8_t *sbase;
+    if constexpr (kLds) sbase = smem;
+    else sbase = ws + I.ws_state;
+    Replayer<kLds> rp(I, T, sbase, ws);
+    rp.run(stats + (int64_t)id * kRecordWords, per_req);
+}
+
+}  // namespace
+
+hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order, int32_t n_launch,
+                         int32_t lds_bytes, bool in_lds, uint8_t *ws, int64_t *stats, int32_t *per_req,
+                         hipStream_t s) {
+    if (n_launch <= 0) return hipSuccess;
+    if (in_lds) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel<true>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(replay_kernel<true>, dim3((unsigned)n_launch), dim3(64), (size_t)lds_bytes, s, d_inst,
+                           d_traces, d_order, ws, stats, per_req);
+    } else {
+        hipLaunchKernelGGL(replay_kernel<false>, dim3((unsigned)n_launch), dim3(64), 0, s, d_inst, d_traces,
+                           d_order, ws, stats, per_req);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace pcr

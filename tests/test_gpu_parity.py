@@ -1,0 +1,162 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle, bit-exact.
+
+Keys: every key of every request.  Replay: every per-group and per-instance
+counter, and the per-request (hits, new, evictions, orphans) quadruples.
+Inputs are seeded synthetic traces (tracegen) or crafted key arrays."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import assert_same, gpu_hash, replay_gpu, run_key_traces
+from paper_2608_01657_amd import device as dv
+from paper_2608_01657_amd import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+POLICIES = [tg.POLICY_LRU, tg.POLICY_S3FIFO, tg.POLICY_PREFIXSHIELD]
+
+
+def _edge_trace(seed=9):
+    """Lengths around block boundaries, unaligned views, full int32 ids."""
+    rng = np.random.default_rng(seed)
+    lens = [0, 1, 15, 16, 17, 31, 32, 33, 63, 64, 65, 1023, 1024, 1025, 4096 + 7, 16384, 16384 + 15]
+    lens += [int(x) for x in rng.integers(0, 3000, 60)]
+    total = sum(lens) + 64
+    toks = rng.integers(-2**31, 2**31, total, dtype=np.int64).astype(np.int32)
+    offs, pos = [], 0
+    for i, L in enumerate(lens):
+        pos += i % 4          # every alignment of the view start
+        offs.append(pos)
+        pos += L
+    toks = np.concatenate([toks, rng.integers(0, 32000, pos + 16, dtype=np.int64).astype(np.int32)])[:pos + 16]
+    R = len(lens)
+    return tg.Trace("edge", toks, np.array(offs, np.int64), np.array(lens, np.int32),
+                    (np.arange(R) % 7).astype(np.uint8), np.zeros(R, np.uint8), np.arange(R, dtype=np.uint32),
+                    7, R)
+
+
+def _check_hash(trace):
+    _, keys, off = gpu_hash(trace)
+    okeys, ooff = oracle.hash_trace(trace)
+    assert np.array_equal(off, ooff)
+    assert keys.shape == okeys.shape
+    bad = np.nonzero(keys != okeys)[0]
+    assert bad.size == 0, f"{bad.size} keys differ, first at {bad[:5]}"
+
+
+def test_hash_edge_cases():
+    _check_hash(_edge_trace())
+
+
+def test_hash_tail_of_buffer():
+    """The last request ends exactly at the end of the token buffer."""
+    rng = np.random.default_rng(3)
+    for extra in range(4):
+        L = 16 * 37 + extra
+        toks = rng.integers(0, 32000, L + 3).astype(np.int32)
+        tr = tg.Trace("tail", toks, np.array([3], np.int64), np.array([L], np.int32), np.zeros(1, np.uint8),
+                      np.zeros(1, np.uint8), np.zeros(1, np.uint32), 1, 1)
+        _check_hash(tr)
+
+
+@pytest.mark.parametrize("name", ["tiny", "onetouch4096", "twopass", "chat"])
+def test_hash_workloads(name):
+    n = {"tiny": 4000, "onetouch4096": 3000, "twopass": 3000, "chat": 5000}[name]
+    traces, _ = tg.workload(name, seeds=[0], n_requests=n)
+    _check_hash(traces[0])
+
+
+@pytest.mark.parametrize("chunk", range(4))
+def test_replay_random_key_traces(chunk):
+    """Crafted keys with frequent hits, orphans, duplicates and truncation;
+    every policy and flag, 1-3 contracts, ticks, eps, S3 parameters."""
+    kts, per = [], []
+    for seed in range(chunk * 25, chunk * 25 + 25):
+        rng = np.random.default_rng(seed)
+        nc = int(rng.integers(1, 4))
+        kt = tg.random_key_trace(seed, n_req=int(rng.integers(1, 120)), max_blocks=int(rng.integers(1, 80)),
+                                 n_groups=int(rng.integers(1, 6)), n_prefix=12, n_contracts=nc,
+                                 key_universe=int(rng.integers(4, 200)), with_ticks=bool(seed % 2))
+        insts = []
+        for pol in POLICIES:
+            for flags in ([0, 1, 2, 3] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                cap = int(rng.integers(1, 90))
+                contracts = [(int(rng.integers(1, 3 * tg.Q16)), int(rng.integers(0, 40)) * tg.Q16)
+                             for _ in range(nc)]
+                insts.append(tg.Instance(0, pol, cap, contracts=contracts, flags=flags,
+                                         eps_q16=int(rng.choice([0, tg.Q16 // 2, 3 * tg.Q16])),
+                                         s3_small_permille=int(rng.choice([100, 250, 500])),
+                                         s3_move_threshold=int(rng.choice([1, 2]))))
+        kts.append(kt)
+        per.append(insts)
+    run_key_traces(kts, per)
+
+
+def test_replay_many_groups():
+    """64 accounting groups, several contracts with different refill rates
+    (normalized debt, Eq. 5), ties in projected debt."""
+    kts, per = [], []
+    for seed in range(6):
+        rng = np.random.default_rng(1000 + seed)
+        kt = tg.random_key_trace(1000 + seed, n_req=300, max_blocks=12, n_groups=64, n_prefix=128,
+                                 n_contracts=4, key_universe=60)
+        insts = []
+        for pol in POLICIES:
+            for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                contracts = [(tg.Q16 // (c + 1), int(rng.integers(0, 4)) * tg.Q16) for c in range(4)]
+                insts.append(tg.Instance(0, pol, int(rng.integers(8, 200)), contracts=contracts, flags=flags))
+        kts.append(kt)
+        per.append(insts)
+    run_key_traces(kts, per)
+
+
+def _workload_parity(name, seeds, n_requests, per_request=False, **kw):
+    traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests, **kw)
+    dts = []
+    okeys = []
+    for tr in traces:
+        t, keys, off = gpu_hash(tr)
+        ok_, ooff = oracle.hash_trace(tr)
+        assert np.array_equal(keys, ok_) and np.array_equal(off, ooff)
+        dts.append(t)
+        okeys.append((ok_, ooff))
+    res, pr = replay_gpu(dts, insts, per_request=per_request)
+    for k, inst in enumerate(insts):
+        o = oracle.replay_trace(traces[inst.trace], okeys[inst.trace][0], okeys[inst.trace][1], inst,
+                                per_request=per_request)
+        assert_same(res[k], o, f"{name} instance {k} {inst.label}")
+        if per_request:
+            assert np.array_equal(pr[k], o.per_request)
+    return res
+
+
+def test_replay_tiny_workload_full():
+    _workload_parity("tiny", [0], None, per_request=True)
+
+
+def test_replay_tiny_workload_variants():
+    tr = tg.onetouch_tiny(1000, 4000)
+    keys, off = oracle.hash_trace(tr)
+    kt = tg.KeyTrace(keys, off, tr.group, tr.contract, tr.prefix, tr.n_groups, tr.n_prefix)
+    per = [[tg.Instance(0, pol, cap, contracts=[(rho, 64 * tg.Q16)], flags=fl)
+            for pol in POLICIES for cap in (16, 100, 256, 1000)
+            for fl in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0])
+            for rho in (tg.Q16 // 8, 8 * tg.Q16)]]
+    run_key_traces([kt], per)
+
+
+def test_replay_onetouch4096_short():
+    _workload_parity("onetouch4096", [0, 1], 4000, per_request=True)
+
+
+def test_replay_twopass_short():
+    _workload_parity("twopass", [0], 6000)
+
+
+def test_replay_delayed_short():
+    _workload_parity("delayed", [0], 8000)
+
+
+def test_replay_chat_all_capacities():
+    """Includes capacities whose state does not fit in LDS (workspace path)."""
+    _workload_parity("chat", [0], 4000, per_request=True)

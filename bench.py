@@ -1,0 +1,182 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched prefix-cache replay hot path on one MI355X.
+
+One step = the whole path over one batch of synthetic traces, inputs already
+resident in HBM: block offsets and chained keys for every trace (hashing),
+then replay of every instance (LRU, S3-FIFO, PrefixShield) from an empty
+cache.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload onetouch4096|scale1024|...]
+
+value = block probes / s of the whole step (requests/s is reported beside it).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+HASH_BYTES_PER_BLOCK = 64 + 8  # 16 int32 tokens in, one uint64 key out
+HASH_BYTES_PER_REQ = 8 + 4 + 4 + 8 + 8   # tok_off, len, ns, key_off read, key_off write
+REPLAY_BYTES_PER_PROBE = 8     # the key
+REPLAY_BYTES_PER_REQ = 8 + 1 + 1 + 4     # key offset, group, contract, prefix id
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="onetouch4096")
+    ap.add_argument("--seeds", type=int, default=None, help="number of traces (default: the workload's)")
+    ap.add_argument("--requests", type=int, default=None, help="requests per trace (default: the workload's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-requests", type=int, default=25000)
+    ap.add_argument("--parity-check", action="store_true",
+                    help="compare one instance per policy against the oracle (slow; off by default)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build measures one GPU only; replay instances are independent and "
+              "would shard across GPUs with no collective, but no multi-GPU run is part of it.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2608_01657_amd import device as dv
+    from paper_2608_01657_amd import tracegen as tg
+
+    t0 = time.time()
+    seeds = list(range(args.seeds)) if args.seeds else None
+    traces, insts = tg.workload(args.workload, seeds=seeds, n_requests=args.requests)
+    gen_s = time.time() - t0
+    print(f"[bench] generated {len(traces)} traces, {len(insts)} instances in {gen_s:.1f}s", file=sys.stderr,
+          flush=True)
+
+    dts = [dv.upload(tr) for tr in traces]
+    for t in dts:
+        dv.cut_and_hash(t)              # sizes the key buffers
+    torch.cuda.synchronize()
+    for t in dts:
+        assert int(t.status.item()) == 0
+    batch = dv.ReplayBatch(dts, insts)
+    stream = torch.cuda.current_stream()
+
+    n_req_total = sum(traces[i.trace].n_req for i in insts)
+    n_blocks_hash = sum(t.n_keys for t in dts)
+    n_req_hash = sum(t.n_req for t in dts)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        for t in dts:
+            dv.cut_and_hash(t, n_keys=t.n_keys)
+        if ev:
+            ev[1].record(stream)
+        batch.launch()
+        if ev:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    hash_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    replay_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    step_ms = wall * 1000.0 / args.steps
+
+    res = batch.results()
+    assert all(st == 0 for _, _, st in res), "an instance reported an error status"
+    probes = sum(sum(g["probes"] for g in gr) for gr, _, _ in res)
+    hits = sum(sum(g["hits"] for g in gr) for gr, _, _ in res)
+
+    # roofline: replay kernel (dominant) against HBM with its algorithmic bytes
+    replay_bytes = probes * REPLAY_BYTES_PER_PROBE + n_req_total * REPLAY_BYTES_PER_REQ
+    replay_gbs = replay_bytes / (replay_ms * 1e-3) / 1e9
+    hash_bytes = n_blocks_hash * HASH_BYTES_PER_BLOCK + n_req_hash * HASH_BYTES_PER_REQ
+    hash_gbs = hash_bytes / (hash_ms * 1e-3) / 1e9
+    dominant = "replay" if replay_ms >= hash_ms else "hash"
+    roof = {"kernel": "replay_kernel<true>" if dominant == "replay" else "hash_kernel",
+            "bound": "hbm",
+            "achieved": round(replay_gbs if dominant == "replay" else hash_gbs, 3),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round((replay_gbs if dominant == "replay" else hash_gbs) / HBM_PEAK_GBS, 6),
+            "traffic": None,
+            "bytes_per_launch": int(replay_bytes if dominant == "replay" else hash_bytes),
+            "avg_launch_ms": round(replay_ms if dominant == "replay" else hash_ms, 4)}
+    roof_hash = {"kernel": "hash_kernel (+ block offsets)", "bound": "hbm", "achieved": round(hash_gbs, 2),
+                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(hash_gbs / HBM_PEAK_GBS, 4),
+                 "bytes_per_launch": int(hash_bytes), "avg_ms": round(hash_ms, 4),
+                 "tokens_per_s": (n_blocks_hash * 16) / (hash_ms * 1e-3)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(traces, insts, args.cpu_sample_requests)
+
+    value = probes / (step_ms * 1e-3)
+    out = {
+        "metric": "block probes/sec (batched replay, 1 GPU)",
+        "value": value,
+        "unit": "probes/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "traces": len(traces), "instances": len(insts),
+                   "requests_per_trace": traces[0].n_req, "capacity_blocks": sorted({i.capacity for i in insts}),
+                   "block_tokens": 16, "policies": sorted({tg.POLICY_NAMES[i.policy] for i in insts})},
+        "requests_per_s": n_req_total / (step_ms * 1e-3),
+        "replay_probes_per_s": probes / (replay_ms * 1e-3),
+        "replay_requests_per_s": n_req_total / (replay_ms * 1e-3),
+        "hash_ms": hash_ms, "replay_ms": replay_ms,
+        "probes_per_step": probes, "hits_per_step": hits, "requests_per_step": n_req_total,
+        "roofline": roof,
+        "roofline_hash": roof_hash,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+def cpu_baseline(traces, insts, sample_requests):
+    """The oracle (plain single-threaded C per instance) on the host cores:
+    hash of the first `sample_requests` requests of every trace, then replay
+    of every instance over them, one thread per task."""
+    import oracle
+    from paper_2608_01657_amd import tracegen as tg
+
+    cores = min(16, os.cpu_count() or 1)
+    sub = []
+    for tr in traces:
+        n = min(sample_requests, tr.n_req)
+        sub.append(tg.Trace(tr.name, tr.tokens, tr.tok_off[:n], tr.length[:n], tr.group[:n], tr.contract[:n],
+                            tr.prefix[:n], tr.n_groups, tr.n_prefix, None if tr.tick is None else tr.tick[:n]))
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=cores) as ex:
+        hashed = list(ex.map(oracle.hash_trace, sub))
+        results = list(ex.map(lambda i: oracle.replay_trace(sub[i.trace], hashed[i.trace][0],
+                                                             hashed[i.trace][1], i), insts))
+    wall = time.perf_counter() - t0
+    probes = sum(sum(g["probes"] for g in r.groups) for r in results)
+    return {"value": probes / wall, "unit": "probes/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {sub[0].n_req} requests of each of the {len(sub)} traces, all {len(insts)} "
+                      f"instances: oracle hash + replay, {probes} probes in {wall:.2f}s wall"}
+
+
+if __name__ == "__main__":
+    main()

@@ -52,7 +52,11 @@ DEV int mbcnt(uint64_t m) {
 }
 DEV int first_lane(uint64_t m) { return __ffsll((unsigned long long)m) - 1; }   // m != 0
 DEV int last_lane(uint64_t m) { return 63 - __clzll((unsigned long long)m); }  // m != 0
-DEV void wsync() { __syncthreads(); }
+// Lanes of one wavefront exchange data through LDS/global memory.  A wave's
+// memory instructions execute in program order, so a wavefront-scope fence
+// (no instruction, no wait) is enough to keep the compiler from reordering
+// one lane's store after another lane's later load.
+DEV void wsync() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
 DEV uint32_t bcast32(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
 DEV int64_t bcast64(int64_t v, int l) {
     uint32_t lo = bcast32((uint32_t)(uint64_t)v, l);
@@ -97,6 +101,16 @@ DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rsmask) {
     return h;
 }
 
+// Optional per-phase cycle accounting (build with -DPC_PROFILE); the totals
+// land in the stats slot of group 63.  Nothing is skipped either way.
+#ifdef PC_PROFILE
+#define PROF_T(var) const uint64_t var = __builtin_amdgcn_s_memtime()
+#define PROF_ADD(i, a, b) prof[i] += (b) - (a)
+#else
+#define PROF_T(var)
+#define PROF_ADD(i, a, b)
+#endif
+
 DEV uint32_t owner_of(uint32_t mt) { return mt & kOwnerMask; }
 DEV uint32_t contract_of(uint32_t mt) { return (mt >> kContractShift) & 3u; }
 DEV uint32_t cls_of(uint32_t mt) { return (mt >> kClsShift) & 3u; }
@@ -133,6 +147,9 @@ struct Replayer {
     uint64_t c_req, c_probe, c_hit, c_miss, c_charged, c_evc, c_promo, c_gated, c_orph, c_dup, c_trunc;
     int64_t d_max, d_sum;
     int32_t r_max;
+#ifdef PC_PROFILE
+    uint64_t prof[8];
+#endif
 
     DEV Replayer(const DevInst &inst, const DevTrace &tr, uint8_t *sbase, uint8_t *ws) : I(inst), T(tr) {
         policy = I.policy;
@@ -708,6 +725,7 @@ struct Replayer {
 
     // ============================================================ one request
     DEV bool request(int64_t r, int64_t &tprev) {
+        PROF_T(p0);
         const int lane = lane_id();
         const int g = T.group[r];
         const int c = T.contract[r];
@@ -734,6 +752,8 @@ struct Replayer {
         const bool gate_open = dg <= eps || (flags & kFlagNoGate);
 
         // ---- lookup, duplicates, pin + OnTouch, orphans, new slots
+        PROF_T(p1);
+        PROF_ADD(0, p0, p1);
         for (uint32_t i = lane; i <= rsmask; i += 64) rset[i] = kEmpty;
         wsync();
         int hend = n, nhit = 0, nnew = 0, ndup = 0, norph = 0;
@@ -845,6 +865,8 @@ struct Replayer {
         }
 
         // ---- reclamation (Alg. 2): truly free blocks first
+        PROF_T(p2);
+        PROF_ADD(1, p1, p2);
         int e = m - (C - resident);
         if (e < 0) e = 0;
         if (e > 0) {
@@ -855,6 +877,8 @@ struct Replayer {
         if (me) c_evc += (uint64_t)e;
 
         // ---- OnCacheFullBlocks: charge n_r = m (Eq. 2), class, admission
+        PROF_T(p3);
+        PROF_ADD(2, p2, p3);
         uint32_t cls_new = kNormal;
         if (m > 0) {
             uint32_t cl = 0;
@@ -874,6 +898,8 @@ struct Replayer {
         }
 
         // ---- insert the new blocks (deepest first in queue order)
+        PROF_T(p4);
+        PROF_ADD(3, p3, p4);
         if (policy == kS3 && m > 0) ensure_room((uint32_t)m);
         const uint32_t mbase = ((uint32_t)g) | ((uint32_t)c << kContractShift) | (cls_new << kClsShift) | kRes | kPin;
         int before = 0;
@@ -918,6 +944,8 @@ struct Replayer {
         wsync();
 
         // ---- release: back to the free queue, deepest first
+        PROF_T(p5);
+        PROF_ADD(4, p4, p5);
         const int nrel = n - ndup;
         if (policy != kS3 && nrel > 0) ensure_room((uint32_t)nrel);
         int seen = 0;
@@ -946,6 +974,8 @@ struct Replayer {
         wsync();
 
         // ---- accounting for every group
+        PROF_T(p6);
+        PROF_ADD(5, p5, p6);
         if (lane < G) {
             const int64_t d = raw_debt(t);
             d_sum = (int64_t)((uint64_t)d_sum + (uint64_t)d);
@@ -955,6 +985,8 @@ struct Replayer {
         }
         if (resident > rmax) rmax = resident;
         last_h = h; last_m = m; last_e = e; last_o = norph;
+        PROF_T(p7);
+        PROF_ADD(6, p6, p7);
         return true;
     }
     int last_h, last_m, last_e, last_o;
@@ -988,6 +1020,9 @@ struct Replayer {
         c_req = c_probe = c_hit = c_miss = c_charged = c_evc = c_promo = c_gated = c_orph = c_dup = c_trunc = 0;
         d_max = d_sum = 0;
         r_max = 0;
+#ifdef PC_PROFILE
+        for (int i = 0; i < 8; ++i) prof[i] = 0;
+#endif
         wsync();
     }
 
@@ -1031,6 +1066,9 @@ struct Replayer {
             q[6] = ok ? (int64_t)rmax : 0;
             q[7] = (int64_t)(uint32_t)status;   // status in the low 32 bits
         }
+#ifdef PC_PROFILE
+        if (lane < 8) st[63 * kGroupFields + lane] = (int64_t)prof[lane];
+#endif
     }
 };
 

@@ -151,33 +151,37 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         d.move_thr = s.s3_move_threshold;
         const int64_t maxn = std::min<int64_t>(t.max_req_blocks, s.capacity);
         d.maxn = (int32_t)maxn;
-        d.pool = (int32_t)(s.capacity + maxn);
-        if (d.pool > 65534) return fail(PC_EINVAL, "instance %d: capacity + largest request exceeds 65534", i);
-        const int64_t nb = std::max<int64_t>(2, (int64_t)1 << ceil_log2((d.pool * 3 + 15) / 16));
-        d.nb_log2 = ceil_log2(nb);
+        // main table: 8-entry buckets, load <= 2/3
+        d.nb_log2 = std::max(1, ceil_log2((int64_t)s.capacity * 3 / 16 + 1));
         d.log_log2 = ceil_log2(s.capacity + maxn + 128);
         d.rs_log2 = std::max(6, ceil_log2(2 * maxn));
         if (s.policy == PC_S3FIFO && d.g_cap > 0) {
-            d.gnb_log2 = std::max(1, ceil_log2((d.g_cap * 3 + 15) / 16));
+            d.gnb_log2 = std::max(1, ceil_log2((int64_t)d.g_cap * 3 / 16 + 1));
             d.gr_log2 = ceil_log2((int64_t)d.g_cap + 64);
         }
         d.n_prefix_words = (int32_t)((t.n_prefix + 31) / 32);
         // state region (identical layout in LDS or in the workspace)
         int64_t so = 0;
         auto take = [&](int64_t bytes) { int64_t o = so; so = align_up(so + bytes, 16); return (int32_t)o; };
-        d.o_key = take(8LL * d.pool);
-        d.o_stamp = take(4LL * d.pool);
-        d.o_meta = take(4LL * d.pool);
+        const int64_t C = s.capacity;
+        const int64_t mx = std::max<int64_t>(maxn, 1);
+        d.o_key = take(8 * C);
+        d.o_stamp = take(4 * C);
+        d.o_meta = take(4 * C);
         d.o_table = take(32LL << d.nb_log2);
-        d.o_evown = take(8LL * 64);
-        d.o_rset = take(4LL << d.rs_log2);
-        d.o_res = take(4LL * 64);
-        d.o_cnt = take(4LL * 192);
-        d.o_cur = take(4LL * 196);
-        d.o_tpos = take(2LL * d.pool);
-        d.o_free = take(2LL * d.pool);
         d.o_log = take(2LL << d.log_log2);
-        d.o_posslot = take(2LL * std::max<int64_t>(maxn, 1));
+        d.o_rkeys = take(8 * mx);
+        d.o_rset = take(4LL << d.rs_log2);
+        d.o_posslot = take(2 * mx);
+        d.o_vlist = take(2 * mx);
+        d.o_evown = take(8LL * 64);
+        d.o_res = take(4LL * 64);
+        if (s.policy == PC_PREFIXSHIELD) {
+            d.o_pfx = take(4 * C);
+            d.o_cnt = take(4LL * 192);
+            d.o_cur = take(4LL * 196);
+        }
+        if (s.policy == PC_S3FIFO && d.g_cap > 0) d.o_gtable = take(32LL << d.gnb_log2);
         d.state_bytes = (int32_t)so;
         d.in_lds = so <= lds_cap ? 1 : 0;
         (d.in_lds ? lds_ids : glb_ids).push_back(i);
@@ -192,10 +196,7 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         if (!d.in_lds) { d.ws_state = off; off = align_up(off + d.state_bytes, 256); }
         d.ws_bits = off;
         off = align_up(off + 8LL * d.n_prefix_words, 256);
-        if (d.policy == PC_PREFIXSHIELD) { d.ws_pfx = off; off = align_up(off + 4LL * d.pool, 256); }
         if (d.policy == PC_S3FIFO && d.g_cap > 0) {
-            d.ws_gtable = off;
-            off = align_up(off + (32LL << d.gnb_log2), 256);
             d.ws_gring = off;
             off = align_up(off + (8LL << d.gr_log2), 256);
         }

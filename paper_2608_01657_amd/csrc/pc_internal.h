@@ -33,33 +33,30 @@ constexpr int kGroupFields = 17;
 constexpr int kInstOffset = 64 * kGroupFields;
 constexpr int kRecordWords = 64 * kGroupFields + 8;
 
-// Per-instance plan computed on the host.  All byte offsets are relative to
-// the instance's state base: dynamic LDS when in_lds, else the workspace
-// region at ws_state.  Arrays marked "global" always live in the workspace.
+// Per-instance plan computed on the host.  State offsets are byte offsets
+// from the instance's state base: dynamic LDS when in_lds, else the
+// workspace region at ws_state.  The ghost ring and the prefix bitmaps always
+// live in the workspace.
 struct DevInst {
     int32_t trace, policy, capacity, flags;
     int32_t n_contracts, s_cap, g_cap, move_thr;
     int64_t eps;
     int64_t rho[4], beta[4], invw[4];
-    int32_t pool;          // slots = capacity + maxn
     int32_t maxn;          // max probes in one request (<= capacity)
     int32_t nb_log2;       // main table buckets (8 entries each)
     int32_t log_log2;      // free-queue log ring entries
     int32_t rs_log2;       // per-request duplicate-detection set entries
-    int32_t gnb_log2;      // S3 ghost table buckets (global)
-    int32_t gr_log2;       // S3 ghost ring entries (global)
+    int32_t gnb_log2;      // S3 ghost table buckets
+    int32_t gr_log2;       // S3 ghost ring entries
     int32_t in_lds;        // 1: state in dynamic LDS
     int32_t state_bytes;   // size of the state region
     int32_t n_prefix_words;
     // state-region offsets (bytes)
-    int32_t o_key, o_tpos, o_stamp, o_meta, o_table, o_log, o_posslot, o_rset, o_free;
-    int32_t o_evown, o_res, o_cnt, o_cur;
-    int32_t pad0;
+    int32_t o_key, o_stamp, o_meta, o_table, o_log, o_posslot, o_rset, o_rkeys, o_vlist;
+    int32_t o_pfx, o_gtable, o_evown, o_res, o_cnt, o_cur;
     // workspace offsets (bytes from workspace base)
     int64_t ws_state;      // state region when !in_lds
-    int64_t ws_pfx;        // uint32 [pool] logical prefix id per slot (PrefixShield)
     int64_t ws_bits;       // uint32 [2 * n_prefix_words]: referenced, admitted
-    int64_t ws_gtable;     // uint32 [8 << gnb_log2] (S3)
     int64_t ws_gring;      // uint64 [1 << gr_log2] (S3)
     int64_t per_req_off;   // int32 element offset into the per-request output, or -1
 };

@@ -12,29 +12,30 @@
 //                       projected-debt argmax (Eqs. 5-8) with the
 //                       reuse-segmented order inside the group (Eq. 9)
 //   OnCacheFullBlocks   charge n_r (Eqs. 1-2), initial class, admission
-//   release             blocks back to the free queue, deepest first
+//   insert + release    new blocks take the victims' slots; every block of
+//                       the request returns to the free queue deepest first
 //   accounting          raw debt D_g (Eq. 3) and occupancy of every group
 //
-// State layout (one instance):
-//   key[pool] u64, stamp[pool] u32, meta[pool] u32, tpos[pool] u16,
-//   fstack[pool] u16   -- slots; pool = capacity + largest request
-//   table[8*NB] u32    -- 2-choice bucketized hash, entry = tag16 | slot16
-//   log[R] u16         -- free-queue log: slot of each appended entry; an
-//                         entry at absolute position q is live iff its slot
-//                         has the in-log bit and stamp == q
-//   posslot, rset      -- per-request position->slot map, duplicate set
-//   evown, res, cnt, cur -- per-group counters and queue cursors
-// It lives in dynamic LDS when it fits (capacities up to ~4K blocks) and in
-// the workspace otherwise; the code is the same, instantiated twice.
+// State of one instance (capacity C, largest request n_max):
+//   key[C] u64, stamp[C] u32, meta[C] u32     -- one slot per cached block
+//   table[8*NB] u32  2-choice bucketized hash, entry = tag16 | slot16
+//   log[R] u16       free-queue log: the slot of each appended entry; an
+//                    entry at absolute position q is live iff its slot has
+//                    the in-log bit and stamp == q
+//   rkeys, rset, posslot, vlist   per-request keys, duplicate set,
+//                    position -> slot, victims' slots
+//   pfx[C] (PrefixShield), ghost table (S3-FIFO), per-group counters
+// All of it sits in dynamic LDS when it fits (C up to 4096 blocks), else in
+// the workspace; the code is the same, instantiated twice.  The ghost ring
+// (keys of S3-FIFO's ghost entries) and the prefix bitmaps stay in HBM.
 //
-// All victims of one request are chosen in bulk: LRU takes the first e live
-// log entries with one ballot per 64 entries; PrefixShield turns the
-// per-victim argmax of Eq. 7 into runs (the winner keeps winning while its
-// projected debt stays above every other candidate's) and drains each run
-// from the group's per-segment cursors; S3-FIFO processes its queue heads
-// 64 at a time, cutting each batch where the sequential rule would switch
-// queues.  Each shortcut reproduces the one-victim-at-a-time definition
-// exactly.
+// Victims of one request are chosen in bulk: LRU takes the first e live log
+// entries with one ballot per 64 entries; PrefixShield turns the per-victim
+// argmax of Eq. 7 into runs (the winner keeps winning while its projected
+// debt stays above every other candidate's) and drains each run from the
+// group's per-segment cursor; S3-FIFO processes queue heads 64 at a time and
+// cuts each batch where the one-at-a-time rule would switch queues.  Each
+// shortcut reproduces the one-victim-at-a-time definition exactly.
 #include "pc_internal.h"
 
 namespace pcr {
@@ -43,6 +44,8 @@ namespace {
 #define DEV __device__ __forceinline__
 
 constexpr int64_t kScale = 65536;
+constexpr uint16_t kNewMark = 0xFFFE;      // posslot: new block, slot not yet assigned
+constexpr int32_t kErrInternal = -5;
 
 DEV int lane_id() { return (int)__lane_id(); }
 DEV uint64_t ballot(bool p) { return __ballot(p); }
@@ -63,6 +66,11 @@ DEV int64_t bcast64(int64_t v, int l) {
     uint32_t hi = bcast32((uint32_t)((uint64_t)v >> 32), l);
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
+DEV uint64_t shfl64(uint64_t v, int src) {
+    uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src);
+    uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src);
+    return ((uint64_t)hi << 32) | lo;
+}
 DEV int64_t xor64(int64_t v, int m) {
     uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)(uint64_t)v, m);
     uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)((uint64_t)v >> 32), m);
@@ -80,26 +88,42 @@ DEV uint32_t wave_sum32(uint32_t v) {
     for (int m = 32; m; m >>= 1) v += (uint32_t)__shfl_xor((int)v, m);
     return bcast32(v, 0);
 }
+// Keep a wave-uniform value in a VGPR (it is only used in per-lane arithmetic)
+// so it does not occupy scalar registers.
+template <typename T>
+DEV T in_vgpr(T x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
 
-// Key -> (two buckets, 16-bit tag, duplicate-set home).  Keys are already
-// hash outputs, but the ABI accepts any uint64, so mix once more.
+// Key -> two buckets, 16-bit tag, duplicate-set home.  Keys are usually hash
+// outputs already, but the ABI accepts any uint64, so mix with 32-bit ops.
 struct TH {
     uint32_t b1, b2, tag, rhome;
 };
 DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rsmask) {
-    uint64_t m = k ^ (k >> 31);
-    m *= 0x7fb5d329728ea185ull;
-    m ^= m >> 27;
-    m *= 0x81dadef4bc2dd44dull;
-    m ^= m >> 33;
+    const uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
+    uint32_t x = lo * 0x85EBCA6Bu ^ hi;
+    x ^= x >> 15;
+    x *= 0x2C1B3C6Du;
+    x ^= x >> 13;
+    uint32_t y = (hi * 0xC2B2AE35u) ^ (lo + 0x27D4EB2Fu);
+    y ^= y >> 16;
+    y *= 0x9E3779B1u;
+    y ^= x >> 7;
     TH h;
-    h.b1 = (uint32_t)m & nbmask;
-    h.b2 = (uint32_t)(m >> 20) & nbmask;
+    h.b1 = x & nbmask;
+    h.b2 = y & nbmask;
     if (h.b2 == h.b1) h.b2 = h.b1 ^ 1u;
-    h.tag = (uint32_t)(m >> 48);
-    h.rhome = (uint32_t)(m >> 32) & rsmask;
+    h.tag = y >> 16;
+    h.rhome = (x >> 11) & rsmask;
     return h;
 }
+
+DEV uint32_t owner_of(uint32_t mt) { return mt & kOwnerMask; }
+DEV uint32_t contract_of(uint32_t mt) { return (mt >> kContractShift) & 3u; }
+DEV uint32_t cls_of(uint32_t mt) { return (mt >> kClsShift) & 3u; }
+DEV uint32_t freq_of(uint32_t mt) { return (mt >> kFreqShift) & 3u; }
 
 // Optional per-phase cycle accounting (build with -DPC_PROFILE); the totals
 // land in the stats slot of group 63.  Nothing is skipped either way.
@@ -111,42 +135,49 @@ DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rsmask) {
 #define PROF_ADD(i, a, b)
 #endif
 
-DEV uint32_t owner_of(uint32_t mt) { return mt & kOwnerMask; }
-DEV uint32_t contract_of(uint32_t mt) { return (mt >> kContractShift) & 3u; }
-DEV uint32_t cls_of(uint32_t mt) { return (mt >> kClsShift) & 3u; }
-DEV uint32_t freq_of(uint32_t mt) { return (mt >> kFreqShift) & 3u; }
+// Descriptor of one request (loaded one request ahead).
+struct Req {
+    int32_t g, c;
+    uint32_t p;
+    int64_t t, ko, nfull;
+};
 
 template <bool kLds>
 struct Replayer {
     // ---------------- configuration (wave-uniform)
     const DevInst &I;
     const DevTrace &T;
-    int policy, C, pool, flags, G, K, nseg;
+    int policy, C, flags, G, K, nseg, maxn;
     int64_t eps;
     uint32_t nbmask, rsmask, lmask, R, gnbmask, grmask;
-    int64_t s_cap, g_cap, move_thr;
-    int64_t rho[4], beta[4], invw[4];
+    int32_t s_cap, g_cap, move_thr;
+    int64_t rho[4], beta[4], invw[4];   // kept in VGPRs
     // ---------------- arrays
-    uint64_t *key;
-    uint32_t *stamp, *meta, *table, *rset, *cnt, *cur, *res;
-    uint16_t *tpos, *fstack, *log, *posslot;
+    uint64_t *key, *rkeys;
+    uint32_t *stamp, *meta, *table, *rset, *cnt, *cur, *res, *pfx, *gtable;
+    uint16_t *log, *posslot, *vlist;
     unsigned long long *evown;
-    uint32_t *pfx, *bits, *gtable;
+    uint32_t *bits;
     uint64_t *gring;
     // ---------------- uniform state
-    uint32_t head, tail;
-    int32_t top;            // free-stack size
-    int32_t resident;       // resident blocks (excludes blocks being created)
+    uint32_t head, tail;      // live log window [head, tail)
+    int32_t hwm;              // slots [hwm, C) have never been used
+    int32_t nvict;            // victims of the current request
+    int32_t resident;         // resident blocks (excludes blocks being created)
     int32_t s_size, s_unp, m_unp;
     uint32_t gseq, curS, curM;
     int32_t rmax;
-    uint64_t ev_total, s3_moves, s3_reins, s3_ghits, s3_gins;
     int32_t err;
-    // ---------------- per-lane group state (lane x = group x)
+    // ghost ring keys prefetched for the next expiry batch
+    uint64_t gpre;
+    uint32_t gpre_base;
+    // ---------------- statistics and group state (VGPRs; lane x = group x)
+    uint64_t ev_total, s3_moves, s3_reins, s3_ghits, s3_gins;
     int64_t bal[4], last[4];
     uint64_t c_req, c_probe, c_hit, c_miss, c_charged, c_evc, c_promo, c_gated, c_orph, c_dup, c_trunc;
     int64_t d_max, d_sum;
     int32_t r_max;
+    int last_h, last_m, last_e, last_o;
 #ifdef PC_PROFILE
     uint64_t prof[8];
 #endif
@@ -154,10 +185,10 @@ struct Replayer {
     DEV Replayer(const DevInst &inst, const DevTrace &tr, uint8_t *sbase, uint8_t *ws) : I(inst), T(tr) {
         policy = I.policy;
         C = I.capacity;
-        pool = I.pool;
         flags = I.flags;
         G = T.n_groups;
         K = I.n_contracts;
+        maxn = I.maxn;
         nseg = (policy == kPS && !(flags & kFlagNoSeg)) ? 3 : 1;
         eps = I.eps;
         nbmask = (1u << I.nb_log2) - 1u;
@@ -170,8 +201,13 @@ struct Replayer {
         g_cap = I.g_cap;
         move_thr = I.move_thr;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) { rho[c] = I.rho[c]; beta[c] = I.beta[c]; invw[c] = I.invw[c]; }
+        for (int c = 0; c < 4; ++c) {
+            rho[c] = in_vgpr(I.rho[c]);
+            beta[c] = in_vgpr(I.beta[c]);
+            invw[c] = in_vgpr(I.invw[c]);
+        }
         key = reinterpret_cast<uint64_t *>(sbase + I.o_key);
+        rkeys = reinterpret_cast<uint64_t *>(sbase + I.o_rkeys);
         stamp = reinterpret_cast<uint32_t *>(sbase + I.o_stamp);
         meta = reinterpret_cast<uint32_t *>(sbase + I.o_meta);
         table = reinterpret_cast<uint32_t *>(sbase + I.o_table);
@@ -179,14 +215,13 @@ struct Replayer {
         cnt = reinterpret_cast<uint32_t *>(sbase + I.o_cnt);
         cur = reinterpret_cast<uint32_t *>(sbase + I.o_cur);
         res = reinterpret_cast<uint32_t *>(sbase + I.o_res);
-        tpos = reinterpret_cast<uint16_t *>(sbase + I.o_tpos);
-        fstack = reinterpret_cast<uint16_t *>(sbase + I.o_free);
+        pfx = reinterpret_cast<uint32_t *>(sbase + I.o_pfx);
+        gtable = reinterpret_cast<uint32_t *>(sbase + I.o_gtable);
         log = reinterpret_cast<uint16_t *>(sbase + I.o_log);
         posslot = reinterpret_cast<uint16_t *>(sbase + I.o_posslot);
+        vlist = reinterpret_cast<uint16_t *>(sbase + I.o_vlist);
         evown = reinterpret_cast<unsigned long long *>(sbase + I.o_evown);
-        pfx = reinterpret_cast<uint32_t *>(ws + I.ws_pfx);
         bits = reinterpret_cast<uint32_t *>(ws + I.ws_bits);
-        gtable = reinterpret_cast<uint32_t *>(ws + I.ws_gtable);
         gring = reinterpret_cast<uint64_t *>(ws + I.ws_gring);
     }
 
@@ -229,80 +264,51 @@ struct Replayer {
         return m;
     }
 
-    // ============================================================ free stack
-    DEV void free_push(bool p, uint32_t slot) {
-        const uint64_t m = ballot(p);
-        if (p) fstack[top + mbcnt(m)] = (uint16_t)slot;
-        top += popc(m);
+    // ============================================================ tables
+    // Both buckets of a key: 16 entries.
+    DEV void load_buckets(const uint32_t *tb, const TH &h, uint32_t e[16]) const {
+        const uint4 *t4 = reinterpret_cast<const uint4 *>(tb);
+        const uint4 a0 = t4[2 * h.b1], a1 = t4[2 * h.b1 + 1], c0 = t4[2 * h.b2], c1 = t4[2 * h.b2 + 1];
+        e[0] = a0.x; e[1] = a0.y; e[2] = a0.z; e[3] = a0.w; e[4] = a1.x; e[5] = a1.y; e[6] = a1.z; e[7] = a1.w;
+        e[8] = c0.x; e[9] = c0.y; e[10] = c0.z; e[11] = c0.w; e[12] = c1.x; e[13] = c1.y; e[14] = c1.z; e[15] = c1.w;
     }
-    DEV uint32_t free_pop(bool p) {
-        const uint64_t m = ballot(p);
-        uint32_t s = kNoSlot;
-        if (p) s = fstack[top - 1 - mbcnt(m)];
-        top -= popc(m);
+    DEV uint32_t epos(const TH &h, int i) const { return i < 8 ? 8 * h.b1 + i : 8 * h.b2 + (i - 8); }
+    // slot of key k in the main table, or -1
+    DEV int tfind(uint64_t k, const TH &h) const {
+        uint32_t e[16];
+        load_buckets(table, h, e);
+        int s = -1;
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            if (s < 0 && e[i] != kEmpty && (e[i] >> 16) == h.tag && key[e[i] & 0xFFFFu] == k) s = (int)(e[i] & 0xFFFFu);
         return s;
     }
-
-    // ============================================================ main table
-    DEV int tfind(uint64_t k, const TH &h, uint32_t &pos) const {
-        const uint4 *t4 = reinterpret_cast<const uint4 *>(table);
-        uint4 a0 = t4[2 * h.b1], a1 = t4[2 * h.b1 + 1], c0 = t4[2 * h.b2], c1 = t4[2 * h.b2 + 1];
-        uint32_t e[16] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w,
-                          c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+    // clear the entry holding exactly `val` (if present)
+    DEV void tclear_exact(uint32_t *tb, uint32_t val, const TH &h) {
+        uint32_t e[16];
+        load_buckets(tb, h, e);
+        int at = -1;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            if (e[i] != kEmpty && (e[i] >> 16) == h.tag) {
-                uint32_t s = e[i] & 0xFFFFu;
-                if (key[s] == k) {
-                    pos = (i < 8 ? 8 * h.b1 + i : 8 * h.b2 + (i - 8));
-                    return (int)s;
-                }
-            }
-        }
-        return -1;
+        for (int i = 0; i < 16; ++i)
+            if (at < 0 && e[i] == val) at = i;
+        if (at >= 0) tb[epos(h, at)] = kEmpty;
     }
     // Parallel insert of a new entry; false when both buckets are full.
-    DEV bool tinsert(uint32_t *tb, uint32_t val, const TH &h, uint32_t &pos) {
-        const uint4 *t4 = reinterpret_cast<const uint4 *>(tb);
-        uint4 a0 = t4[2 * h.b1], a1 = t4[2 * h.b1 + 1], c0 = t4[2 * h.b2], c1 = t4[2 * h.b2 + 1];
-        uint32_t e[16] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w,
-                          c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+    DEV bool tinsert(uint32_t *tb, uint32_t val, const TH &h) {
+        uint32_t e[16];
+        load_buckets(tb, h, e);
         int n1 = 0, n2 = 0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) { n1 += e[i] == kEmpty; n2 += e[8 + i] == kEmpty; }
-        const bool second_first = n2 > n1;
+        const int first = n2 > n1 ? 8 : 0;
         for (int pass = 0; pass < 2; ++pass) {
-            const bool use2 = (pass == 0) == second_first;
-            const uint32_t b = use2 ? h.b2 : h.b1;
+            const int base = pass == 0 ? first : 8 - first;
             for (int w = 0; w < 8; ++w) {
-                if (e[(use2 ? 8 : 0) + w] != kEmpty) continue;
-                uint32_t old = atomicCAS(&tb[8 * b + w], kEmpty, val);
-                if (old == kEmpty) { pos = 8 * b + w; return true; }
+                if (e[base + w] != kEmpty) continue;
+                if (atomicCAS(&tb[epos(h, base + w)], kEmpty, val) == kEmpty) return true;
             }
         }
         return false;
-    }
-
-    // ============================================================ ghost (S3)
-    DEV bool gfind_clear(uint64_t k, const TH &h) {
-        for (int bi = 0; bi < 2; ++bi) {
-            const uint32_t b = bi ? h.b2 : h.b1;
-            for (int w = 0; w < 8; ++w) {
-                uint32_t e = gtable[8 * b + w];
-                if (e != kEmpty && (e >> 16) == h.tag && gring[e & grmask] == k) {
-                    gtable[8 * b + w] = kEmpty;
-                    return true;
-                }
-            }
-        }
-        return false;
-    }
-    DEV void gclear_exact(uint32_t val, const TH &h) {
-        for (int bi = 0; bi < 2; ++bi) {
-            const uint32_t b = bi ? h.b2 : h.b1;
-            for (int w = 0; w < 8; ++w)
-                if (gtable[8 * b + w] == val) { gtable[8 * b + w] = kEmpty; return; }
-        }
     }
     // Serial cuckoo displacement for an entry that found both buckets full.
     template <bool kMain>
@@ -313,29 +319,22 @@ struct Replayer {
         uint64_t ck = k;
         uint32_t from = 0xFFFFFFFFu;
         for (int it = 0; it < 512; ++it) {
-            TH h = thash(ck, msk, rsmask);
-            for (int bi = 0; bi < 2; ++bi) {
-                const uint32_t b = bi ? h.b2 : h.b1;
-                for (int w = 0; w < 8; ++w)
-                    if (tb[8 * b + w] == kEmpty) {
-                        tb[8 * b + w] = cv;
-                        if (kMain) tpos[cv & 0xFFFFu] = (uint16_t)(8 * b + w);
-                        return true;
-                    }
+            const TH h = thash(ck, msk, rsmask);
+            for (int i = 0; i < 16; ++i) {
+                const uint32_t p = epos(h, i);
+                if (tb[p] == kEmpty) { tb[p] = cv; return true; }
             }
             uint32_t b = (h.b1 == from) ? h.b2 : h.b1;
             if (from == 0xFFFFFFFFu && (it & 1)) b = h.b2;
-            const uint32_t w = (uint32_t)(it * 5 + (ck >> 7)) & 7u;
+            const uint32_t w = (uint32_t)(it * 5 + (uint32_t)(ck >> 7)) & 7u;
             const uint32_t victim = tb[8 * b + w];
             tb[8 * b + w] = cv;
-            if (kMain) tpos[cv & 0xFFFFu] = (uint16_t)(8 * b + w);
             cv = victim;
             ck = kMain ? key[victim & 0xFFFFu] : gring[victim & grmask];
             from = b;
         }
         return false;
     }
-    // Run kicks for every lane of `over`, one lane at a time.
     template <bool kMain>
     DEV void kick_lanes(uint64_t over, uint32_t val, uint64_t k) {
         wsync();
@@ -346,24 +345,27 @@ struct Replayer {
             const uint64_t kk = (uint64_t)bcast64((int64_t)k, l);
             bool ok = true;
             if (lane_id() == 0) ok = kick<kMain>(v, kk);
-            if (!bcast32(ok ? 1u : 0u, 0)) err = PC_EINTERNAL_CODE;
+            if (!bcast32(ok ? 1u : 0u, 0)) err = kErrInternal;
             wsync();
         }
     }
-    static constexpr int32_t PC_EINTERNAL_CODE = -5;
 
     // ============================================================ eviction core
     DEV void evict_lanes(bool v, uint32_t s) {
+        const uint64_t vm = ballot(v);
         if (v) {
             const uint32_t mt = meta[s];
             const uint32_t o = owner_of(mt);
             atomicAdd(&evown[o], 1ull);
             atomicSub(&res[o], 1u);
-            table[tpos[s]] = kEmpty;
+            const uint64_t k = key[s];
+            const TH h = thash(k, nbmask, rsmask);
+            tclear_exact(table, (h.tag << 16) | s, h);
             meta[s] = 0;
+            vlist[nvict + mbcnt(vm)] = (uint16_t)s;
         }
-        const int nv = popc(ballot(v));
-        free_push(v, s);
+        const int nv = popc(vm);
+        nvict += nv;
         resident -= nv;
         ev_total += (uint64_t)nv;
     }
@@ -377,7 +379,7 @@ struct Replayer {
         for (uint32_t p0 = head; p0 < tail; p0 += 64) {
             const uint32_t pos = p0 + lane;
             const bool valid = pos < tail;
-            uint32_t s = valid ? log[pos & lmask] : 0;
+            const uint32_t s = valid ? log[pos & lmask] : 0;
             const bool live = valid && (meta[s] & kInLog) && stamp[s] == pos;
             const uint64_t lm = ballot(live);
             wsync();
@@ -399,13 +401,12 @@ struct Replayer {
         if (tail + k - head <= R) return;
         if (policy == kPS) {   // lowest cursor of a non-empty queue bounds every live entry
             uint32_t m = tail;
-            for (int i = lane_id(); i < 192; i += 64) {
+            for (int i = lane_id(); i < 192; i += 64)
                 if (cnt[i] > 0 && cur[i] < m) m = cur[i];
-            }
             m = wave_min32(m);
             if (m > head) head = m;
         } else if (policy == kS3) {
-            uint32_t m = curS < curM ? curS : curM;
+            const uint32_t m = curS < curM ? curS : curM;
             if (m > head) head = m;
         }
         if (tail + k - head > R) compact();
@@ -429,16 +430,16 @@ struct Replayer {
             if (nv == rem) head = head + (uint32_t)last_lane(vm) + 1;
             else head = (head + 64 < tail) ? head + 64 : tail;
             rem -= nv;
-            if (nv == 0 && head >= tail) err = PC_EINTERNAL_CODE;
+            if (nv == 0 && head >= tail) err = kErrInternal;
             wsync();
         }
     }
 
     // ---------------------------------------------------------------- PrefixShield
-    // Take k victims from queue (x, s) (x < 0: any owner) in free-queue order.
-    DEV void ps_take(int x, int s, int k) {
+    // Take k victims from queue ci in free-queue order.  x < 0: any owner;
+    // s < 0: any class (no segmentation).
+    DEV void ps_take(int x, int s, int ci, int k) {
         const int lane = lane_id();
-        const int ci = x >= 0 ? 3 * x + s : 192 + s;
         uint32_t c = cur[ci];
         int rem = k;
         while (rem > 0 && err == 0) {
@@ -447,18 +448,18 @@ struct Replayer {
             const uint32_t sl = valid ? log[pos & lmask] : 0;
             const uint32_t mt = valid ? meta[sl] : 0;
             const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
-            const bool match = live && (x < 0 || (int)owner_of(mt) == x) && (nseg == 1 || (int)cls_of(mt) == s);
+            const bool match = live && (x < 0 || (int)owner_of(mt) == x) && (s < 0 || (int)cls_of(mt) == s);
             const uint64_t mm = ballot(match);
             const bool v = match && mbcnt(mm) < rem;
             const uint64_t vm = ballot(v);
             const int nv = popc(vm);
             wsync();
-            if (v) atomicSub(&cnt[3 * owner_of(mt) + s], 1u);
+            if (v) atomicSub(&cnt[3 * owner_of(mt) + (s < 0 ? 0u : (uint32_t)s)], 1u);
             evict_lanes(v, sl);
             if (nv == rem) c = c + (uint32_t)last_lane(vm) + 1;
             else c = (c + 64 < tail) ? c + 64 : tail;
             rem -= nv;
-            if (nv == 0 && c >= tail) err = PC_EINTERNAL_CODE;
+            if (nv == 0 && c >= tail) err = kErrInternal;
             wsync();
         }
         if (lane == 0) cur[ci] = c;
@@ -467,7 +468,7 @@ struct Replayer {
     // Oldest live entry of queue (x, s); advances that queue's cursor to it.
     DEV uint32_t ps_headpos(int x, int s) {
         const int lane = lane_id();
-        const int ci = 3 * x + s;
+        const int ci = 3 * x + (s < 0 ? 0 : s);
         uint32_t c = cur[ci];
         uint32_t found = 0xFFFFFFFFu;
         while (c < tail) {
@@ -476,7 +477,7 @@ struct Replayer {
             const uint32_t sl = valid ? log[pos & lmask] : 0;
             const uint32_t mt = valid ? meta[sl] : 0;
             const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
-            const bool match = live && (int)owner_of(mt) == x && (nseg == 1 || (int)cls_of(mt) == s);
+            const bool match = live && (int)owner_of(mt) == x && (s < 0 || (int)cls_of(mt) == s);
             const uint64_t mm = ballot(match);
             if (mm) { found = c + (uint32_t)first_lane(mm); c = found; break; }
             c = (c + 64 < tail) ? c + 64 : tail;
@@ -503,25 +504,20 @@ struct Replayer {
             if (!Em) break;
             const int64_t pm = wave_max64(inE ? P : -1);       // Eq. 7
             uint64_t tied = ballot(inE && P == pm);
-            int gs;
-            if (popc(tied) == 1) {
-                gs = first_lane(tied);
-            } else {   // ties: lowest non-empty segment, then oldest head entry
+            int gs = first_lane(tied);
+            if (popc(tied) > 1) {   // ties: lowest non-empty segment, then oldest head entry
                 uint32_t seg = 3;
-                if (grp) {
+                if (grp)
                     for (int s = nseg - 1; s >= 0; --s)
                         if (cnt[3 * lane + s] > 0) seg = (uint32_t)s;
-                }
-                const uint32_t mseg = wave_min32(((tied >> lane) & 1) ? seg : 3u);
-                tied &= ballot(seg == mseg);
-                if (popc(tied) == 1) {
-                    gs = first_lane(tied);
-                } else {
+                const int mseg = (int)wave_min32(((tied >> lane) & 1) ? seg : 3u);
+                tied &= ballot(seg == (uint32_t)mseg);
+                gs = first_lane(tied);
+                if (popc(tied) > 1) {
                     uint32_t best = 0xFFFFFFFFu;
-                    gs = first_lane(tied);
                     for (uint64_t tm = tied; tm; tm &= tm - 1) {
                         const int x = first_lane(tm);
-                        const uint32_t hp = ps_headpos(x, (int)mseg);
+                        const uint32_t hp = ps_headpos(x, nseg == 1 ? -1 : mseg);
                         if (hp < best) { best = hp; gs = x; }
                     }
                 }
@@ -530,21 +526,21 @@ struct Replayer {
             const int ag = (int)bcast32(avail, gs);
             const int64_t p2 = wave_max64((inE && lane != gs) ? P : -1);
             const int64_t thr = p2 > eps ? p2 : eps;
-            // picks g* keeps winning strictly: P - i*D > max(second, eps)
-            int64_t k1 = Pg > thr ? (Pg - thr + Dg - 1) / Dg : 0;
+            // g* keeps winning strictly while P - i*D > max(second, eps)
+            const int64_t k1 = Pg > thr ? (Pg - thr + Dg - 1) / Dg : 0;
             int64_t k = k1 > 1 ? k1 : 1;
             if (k > rem) k = rem;
             if (k > ag) k = ag;
-            int kk = (int)k;
-            for (int s = 0; s < nseg && kk > 0; ++s) {
-                const int cs = (int)(nseg == 1 ? (cnt[3 * gs] + cnt[3 * gs + 1] + cnt[3 * gs + 2])
-                                               : cnt[3 * gs + s]);
-                const int tk = cs < kk ? cs : kk;
-                if (tk > 0) {
-                    if (nseg == 1) ps_take_noseg(gs, tk);
-                    else ps_take(gs, s, tk);
+            if (nseg == 1) {
+                ps_take(gs, -1, 3 * gs, (int)k);
+            } else {
+                int kk = (int)k;
+                for (int s = 0; s < 3 && kk > 0; ++s) {
+                    const int cs = (int)cnt[3 * gs + s];
+                    const int tk = cs < kk ? cs : kk;
+                    if (tk > 0) ps_take(gs, s, 3 * gs + s, tk);
+                    kk -= tk;
                 }
-                kk -= tk;
             }
             if (lane == gs) {
                 P -= k * Dg;
@@ -556,49 +552,22 @@ struct Replayer {
         // no indebted candidate owner: global segment order (Eq. 9 fallback)
         for (int s = 0; s < nseg && rem > 0 && err == 0; ++s) {
             uint32_t cs = 0;
-            if (grp) cs = nseg == 1 ? cnt[3 * lane] + cnt[3 * lane + 1] + cnt[3 * lane + 2] : cnt[3 * lane + s];
+            if (grp) cs = cnt[3 * lane + (nseg == 1 ? 0 : s)];
             const int tot = (int)wave_sum32(cs);
             const int tk = tot < rem ? tot : rem;
-            if (tk > 0) {
-                if (nseg == 1) ps_take_any_noseg(tk);
-                else ps_take(-1, s, tk);
-            }
+            if (tk > 0) ps_take(-1, nseg == 1 ? -1 : s, 192 + s, tk);
             rem -= tk;
         }
-        if (rem > 0) err = PC_EINTERNAL_CODE;
-    }
-    // Without segmentation the group queue holds every class.
-    DEV void ps_take_noseg(int x, int k) { ps_take_filtered(x, k, 3 * x); }
-    DEV void ps_take_any_noseg(int k) { ps_take_filtered(-1, k, 192); }
-    DEV void ps_take_filtered(int x, int k, int ci) {
-        const int lane = lane_id();
-        uint32_t c = cur[ci];
-        int rem = k;
-        while (rem > 0 && err == 0) {
-            const uint32_t pos = c + lane;
-            const bool valid = pos < tail;
-            const uint32_t sl = valid ? log[pos & lmask] : 0;
-            const uint32_t mt = valid ? meta[sl] : 0;
-            const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
-            const bool match = live && (x < 0 || (int)owner_of(mt) == x);
-            const uint64_t mm = ballot(match);
-            const bool v = match && mbcnt(mm) < rem;
-            const uint64_t vm = ballot(v);
-            const int nv = popc(vm);
-            wsync();
-            if (v) atomicSub(&cnt[3 * owner_of(mt)], 1u);   // single segment: counted at index 0
-            evict_lanes(v, sl);
-            if (nv == rem) c = c + (uint32_t)last_lane(vm) + 1;
-            else c = (c + 64 < tail) ? c + 64 : tail;
-            rem -= nv;
-            if (nv == 0 && c >= tail) err = PC_EINTERNAL_CODE;
-            wsync();
-        }
-        if (lane == 0) cur[ci] = c;
-        wsync();
+        if (rem > 0) err = kErrInternal;
     }
 
     // ---------------------------------------------------------------- S3-FIFO
+    DEV void ghost_prefetch() {
+        if (g_cap > 0) {
+            gpre_base = gseq;
+            gpre = gring[(gseq - (uint32_t)g_cap + (uint32_t)lane_id()) & grmask];
+        }
+    }
     // Ghost insertion of the keys of lanes `v`, in lane order.  The ghost
     // keeps the last g_cap insertions: entries older than the batch that
     // leave the window are removed, and batch entries that would already
@@ -608,15 +577,17 @@ struct Replayer {
         const int nv = popc(vm);
         s3_gins += (uint64_t)nv;
         if (g_cap > 0 && nv > 0) {
-            const uint32_t seq = gseq + (uint32_t)mbcnt(vm);
+            const int rk = mbcnt(vm);
+            const uint32_t seq = gseq + (uint32_t)rk;
             const uint32_t gend = gseq + (uint32_t)nv;
-            if (v && (int64_t)seq >= g_cap) {
+            const uint64_t kpre = shfl64(gpre, rk);   // gring[(seq - g_cap) & grmask], prefetched
+            if (v && (int64_t)seq >= (int64_t)g_cap) {
                 const uint32_t x = seq - (uint32_t)g_cap;
                 if (x < gseq) {
                     const uint32_t xp = x & grmask;
-                    const uint64_t kx = gring[xp];
+                    const uint64_t kx = gpre_base == gseq ? kpre : gring[xp];
                     const TH hx = thash(kx, gnbmask, rsmask);
-                    gclear_exact((hx.tag << 16) | xp, hx);
+                    tclear_exact(gtable, (hx.tag << 16) | xp, hx);
                 }
             }
             wsync();
@@ -624,14 +595,27 @@ struct Replayer {
             const TH h = thash(k, gnbmask, rsmask);
             const uint32_t val = (h.tag << 16) | (seq & grmask);
             bool ok = true;
-            uint32_t pos;
             if (v) gring[seq & grmask] = k;
-            if (ins) ok = tinsert(gtable, val, h, pos);
+            if (ins) ok = tinsert(gtable, val, h);
             const uint64_t over = ballot(ins && !ok);
             if (over) kick_lanes<false>(over, val, k);
             wsync();
+            gseq += (uint32_t)nv;
+            ghost_prefetch();
+        } else {
+            gseq += (uint32_t)nv;
         }
-        gseq += (uint32_t)nv;
+    }
+    // ghost hit for key k: remove it and report true
+    DEV bool ghost_take(uint64_t k) {
+        const TH h = thash(k, gnbmask, rsmask);
+        uint32_t e[16];
+        load_buckets(gtable, h, e);
+        int at = -1;
+        for (int i = 0; i < 16; ++i)
+            if (at < 0 && e[i] != kEmpty && (e[i] >> 16) == h.tag && gring[e[i] & grmask] == k) at = i;
+        if (at >= 0) gtable[epos(h, at)] = kEmpty;
+        return at >= 0;
     }
     DEV void evict_s3(int e) {
         const int lane = lane_id();
@@ -648,7 +632,7 @@ struct Replayer {
             const bool useS = (s_size >= s_cap && s_unp > 0) || (m_unp == 0);
             const uint32_t sp = useS ? spS : spM;
             const uint32_t lim = tail;
-            if (sp >= lim) { err = PC_EINTERNAL_CODE; break; }
+            if (sp >= lim) { err = kErrInternal; break; }
             const uint32_t pos = sp + lane;
             const bool valid = pos < lim;
             const uint32_t sl = valid ? log[pos & lmask] : 0;
@@ -660,16 +644,16 @@ struct Replayer {
             const int crk = mbcnt(candm);
             const uint32_t f = freq_of(mt);
             bool ok;
-            bool mv = false;
-            if (useS) {
-                mv = cand && (int64_t)f >= move_thr;
+            bool mv;
+            if (useS) {   // small queue: move (accessed) or evict into the ghost
+                mv = cand && (int)f >= move_thr;
                 const uint64_t mvm = ballot(mv);
                 const int mb = popc(mvm & below);
                 const int eb = popc(candm & ~mvm & below);
-                const bool useS_i = ((int64_t)(s_size - crk) >= s_cap && (s_unp - crk) > 0) || (m_unp + mb == 0);
+                const bool useS_i = (s_size - crk >= s_cap && s_unp - crk > 0) || (m_unp + mb == 0);
                 ok = cand && useS_i && eb < rem;
-            } else {
-                mv = cand && f > 0;   // reinsertion
+            } else {      // main queue: reinsert (freq > 0) or evict
+                mv = cand && f > 0;
                 const uint64_t mvm = ballot(mv);
                 const int eb = popc(candm & ~mvm & below);
                 ok = cand && eb < rem && (m_unp - eb) > 0;
@@ -681,9 +665,7 @@ struct Replayer {
             const uint64_t pmm = ballot(pmove), pem = ballot(pev);
             const int nmv = popc(pmm), nev = popc(pem);
             // live entries of this queue that stay behind the scan point
-            const uint64_t keptm = ballot(inQ && !proc && lane < stop);
-            const uint64_t stopm = bad ? (1ull << stop) : 0ull;
-            const uint64_t km = keptm | stopm;
+            const uint64_t km = ballot(inQ && !proc && lane < stop) | (bad ? (1ull << stop) : 0ull);
             if (km) {
                 const uint32_t kp = sp + (uint32_t)first_lane(km);
                 if (useS) { if (kp < keptS) keptS = kp; } else { if (kp < keptM) keptM = kp; }
@@ -713,7 +695,7 @@ struct Replayer {
             evict_lanes(pev, sl);
             rem -= nev;
             const uint32_t adv = stop < 64 ? (uint32_t)stop : ((lim - sp) < 64 ? (lim - sp) : 64u);
-            if (adv == 0) err = PC_EINTERNAL_CODE;   // a scan that cannot advance is a bug, never a hang
+            if (adv == 0) err = kErrInternal;   // a scan that cannot advance is a bug, never a hang
             if (useS) spS = sp + adv; else spM = sp + adv;
             wsync();
         }
@@ -724,17 +706,28 @@ struct Replayer {
     }
 
     // ============================================================ one request
-    DEV bool request(int64_t r, int64_t &tprev) {
+    DEV Req load_req(int64_t r) const {
+        Req q;
+        q.g = T.group[r];
+        q.c = T.contract[r];
+        q.p = T.prefix[r];
+        q.t = T.tick ? T.tick[r] : r;
+        q.ko = T.key_off[r];
+        q.nfull = T.key_off[r + 1] - q.ko;
+        return q;
+    }
+
+    // `kn` holds keys[ko + lane] of this request and bref/badm its prefix
+    // bitmap words (all prefetched); on return they hold the same for `nx`.
+    DEV bool request(int64_t r, const Req &q, int64_t &tprev, uint64_t &kn, uint32_t &bref, uint32_t &badm,
+                     const Req &nx, bool has_next) {
         PROF_T(p0);
         const int lane = lane_id();
-        const int g = T.group[r];
-        const int c = T.contract[r];
-        const uint32_t p = T.prefix[r];
-        const int64_t t = T.tick ? T.tick[r] : r;
-        const int64_t ko = T.key_off[r];
-        const int64_t nfull = T.key_off[r + 1] - ko;
-        if (g >= G || c >= K || (int64_t)p >= T.n_prefix || ko < 0 || nfull < 0 ||
-            ko + nfull > T.n_keys || nfull > T.max_req_blocks || t < 0 || t < tprev)
+        const int g = q.g, c = q.c;
+        const uint32_t p = q.p;
+        const int64_t t = q.t, ko = q.ko, nfull = q.nfull;
+        if (g >= G || c >= K || (int64_t)p >= T.n_prefix || ko < 0 || nfull < 0 || ko + nfull > T.n_keys ||
+            nfull > T.max_req_blocks || t < 0 || t < tprev)
             return false;
         tprev = t;
         const int n = (int)(nfull < C ? nfull : C);
@@ -742,35 +735,37 @@ struct Replayer {
 
         // ---- OnRequest (Alg. 1): prior reference of (g,p), then record it
         const uint32_t w = p >> 5, bit = 1u << (p & 31);
-        const uint32_t refw = bits[w], admw = bits[I.n_prefix_words + w];
-        const bool q1 = (refw & bit) != 0, adm = (admw & bit) != 0;
-        if (lane == 0 && !q1) bits[w] = refw | bit;
+        const bool q1 = (bref & bit) != 0, adm = (badm & bit) != 0;
+        if (lane == 0 && !q1) bits[w] = bref | bit;
         if (me) { c_req += 1; c_probe += (uint64_t)n; c_trunc += (uint64_t)(nfull - n); }
         const bool proven = q1 && adm;
         int64_t dg = 0;
         if (policy == kPS) dg = bcast64(me ? raw_debt(t) : 0, g);   // before this request's charge
         const bool gate_open = dg <= eps || (flags & kFlagNoGate);
 
-        // ---- lookup, duplicates, pin + OnTouch, orphans, new slots
+        // ---- lookup, duplicates, pin + OnTouch, orphans (new blocks wait)
         PROF_T(p1);
         PROF_ADD(0, p0, p1);
         for (uint32_t i = lane; i <= rsmask; i += 64) rset[i] = kEmpty;
         wsync();
         int hend = n, nhit = 0, nnew = 0, ndup = 0, norph = 0;
         int npromo = 0, ngated = 0;
+        uint64_t kcur = kn;
         for (int base = 0; base < n; base += 64) {
             const int j = base + lane;
             const bool act = j < n;
-            const uint64_t k = act ? T.keys[ko + j] : 0ull;
+            const uint64_t k = kcur;
+            if (base + 64 < n) kcur = (j + 64 < n) ? T.keys[ko + j + 64] : 0ull;   // next chunk in flight
             const TH h = thash(k, nbmask, rsmask);
             const uint32_t mine = (h.tag << 16) | (uint32_t)j;
             uint32_t rpos = 0;
             if (act) {   // first occurrence in the request keeps the smallest position
+                rkeys[j] = k;
                 uint32_t idx = h.rhome;
                 for (;;) {
                     const uint32_t old = atomicCAS(&rset[idx], kEmpty, mine);
                     if (old == kEmpty) { rpos = idx; break; }
-                    if ((old >> 16) == h.tag && T.keys[ko + (old & 0xFFFFu)] == k) {
+                    if ((old >> 16) == h.tag && rkeys[old & 0xFFFFu] == k) {
                         atomicMin(&rset[idx], mine);
                         rpos = idx;
                         break;
@@ -781,16 +776,14 @@ struct Replayer {
             wsync();
             const bool dup = act && rset[rpos] != mine;
             const bool nd = act && !dup;
-            uint32_t tp = 0;
-            const int fs = nd ? tfind(k, h, tp) : -1;
+            const int fs = nd ? tfind(k, h) : -1;
             const bool found = fs >= 0;
             const uint64_t missm = ballot(nd && !found);
             if (hend == n && missm) hend = base + first_lane(missm);
             const bool isHit = found && j < hend;
             const bool isOrph = found && j >= hend;
-            const bool isNew = nd && !found;
             const uint32_t slot = (uint32_t)fs;
-            uint32_t mt = (found) ? meta[slot] : 0u;
+            const uint32_t mt = found ? meta[slot] : 0u;
             // Eq. 4: proven reuse of a block matching (g, c, p), not yet REUSE
             bool elig = false;
             if (policy == kPS && isHit && proven && (int)owner_of(mt) == g && (int)contract_of(mt) == c &&
@@ -800,8 +793,7 @@ struct Replayer {
                 const int ne = popc(ballot(elig));
                 if (gate_open) npromo += ne; else ngated += ne;
             }
-            // hits: pin, touch
-            if (isHit) {
+            if (isHit) {   // pin; touch
                 uint32_t m2 = mt | kPin;
                 if (policy == kS3) {
                     const uint32_t f = freq_of(mt);
@@ -814,45 +806,40 @@ struct Replayer {
                     }
                 }
                 meta[slot] = m2;
-                posslot[j] = (uint16_t)slot;
             }
             if (policy == kS3) {
                 const bool inM = (mt & kQMain) != 0;
-                s_unp -= popc(ballot(isHit && !inM));
-                m_unp -= popc(ballot(isHit && inM));
-                s_unp -= popc(ballot(isOrph && !inM));
-                m_unp -= popc(ballot(isOrph && inM));
-                s_size -= popc(ballot(isOrph && !inM));
+                const int hs = popc(ballot(isHit && !inM)), hm = popc(ballot(isHit && inM));
+                const int os = popc(ballot(isOrph && !inM)), om = popc(ballot(isOrph && inM));
+                s_unp -= hs + os;
+                m_unp -= hm + om;
+                s_size -= os;
             }
-            // orphans: the old block leaves, its slot is reused for the new one
+            // orphans: the old block leaves; its slot and table entry are
+            // reused by the new block of the same key
             if (isOrph) {
                 const uint32_t o = owner_of(mt);
                 atomicSub(&res[o], 1u);
                 if (policy == kPS) atomicSub(&cnt[3 * o + (nseg == 1 ? 0u : cls_of(mt))], 1u);
                 meta[slot] = kPin;
-                posslot[j] = (uint16_t)slot;
             }
+            if (act) posslot[j] = dup ? kNoSlot : (found ? (uint16_t)slot : kNewMark);
             const int no = popc(ballot(isOrph));
             norph += no;
             resident -= no;
-            // brand-new keys: a free slot and a table entry
-            const uint32_t ns = free_pop(isNew);
-            uint32_t tpn = 0;
-            bool ok = true;
-            if (isNew) {
-                key[ns] = k;
-                meta[ns] = kPin;
-                posslot[j] = (uint16_t)ns;
-                ok = tinsert(table, (h.tag << 16) | ns, h, tpn);
-                if (ok) tpos[ns] = (uint16_t)tpn;
-            }
-            const uint64_t over = ballot(isNew && !ok);
-            if (over) kick_lanes<true>(over, (h.tag << 16) | ns, k);
-            if (act && dup) posslot[j] = kNoSlot;
             nhit += popc(ballot(isHit));
-            nnew += popc(ballot(isNew)) + no;
-            ndup += popc(ballot(act && dup));
+            nnew += popc(ballot(nd && !isHit));
+            ndup += popc(ballot(dup));
             wsync();
+        }
+        // the next request's first 64 keys and prefix bits go in flight now
+        uint64_t knext = 0;
+        uint32_t nref = 0, nadm = 0;
+        if (has_next) {
+            knext = (lane < nx.nfull) ? T.keys[nx.ko + lane] : 0ull;
+            const uint32_t nwd = nx.p >> 5;
+            nref = bits[nwd];
+            nadm = bits[I.n_prefix_words + nwd];
         }
         const int h = nhit, m = nnew;
         if (me) {
@@ -867,6 +854,7 @@ struct Replayer {
         // ---- reclamation (Alg. 2): truly free blocks first
         PROF_T(p2);
         PROF_ADD(1, p1, p2);
+        nvict = 0;
         int e = m - (C - resident);
         if (e < 0) e = 0;
         if (e > 0) {
@@ -880,6 +868,7 @@ struct Replayer {
         PROF_T(p3);
         PROF_ADD(2, p2, p3);
         uint32_t cls_new = kNormal;
+        bool adm_now = adm;
         if (m > 0) {
             uint32_t cl = 0;
             if (me) {
@@ -894,30 +883,52 @@ struct Replayer {
                 c_charged += (uint64_t)m;
             }
             cls_new = bcast32(cl, g);
-            if (lane == 0 && !adm) bits[I.n_prefix_words + w] = admw | bit;
+            if (lane == 0 && !adm) bits[I.n_prefix_words + w] = badm | bit;
+            adm_now = true;
         }
 
-        // ---- insert the new blocks (deepest first in queue order)
+        // ---- insert the new blocks: never-used slots first, then the
+        //      victims' slots; queue order is deepest first
         PROF_T(p4);
         PROF_ADD(3, p3, p4);
         if (policy == kS3 && m > 0) ensure_room((uint32_t)m);
         const uint32_t mbase = ((uint32_t)g) | ((uint32_t)c << kContractShift) | (cls_new << kClsShift) | kRes | kPin;
-        int before = 0;
+        const int nfresh = C - hwm;
+        int before = 0, nalloc = 0;
         int n_ins_S = 0, n_ins_M = 0;
         for (int base = hend; base < n; base += 64) {
             const int j = base + lane;
             const bool act = j < n;
-            const uint32_t slot = act ? posslot[j] : kNoSlot;
+            uint32_t slot = act ? posslot[j] : kNoSlot;
+            const bool isN = slot == kNewMark;
+            const uint64_t am = ballot(isN);
+            uint64_t kk = 0;
+            if (isN) {
+                const int i = nalloc + mbcnt(am);
+                slot = i < nfresh ? (uint32_t)(hwm + i) : vlist[i - nfresh];
+                kk = rkeys[j];
+                key[slot] = kk;
+                posslot[j] = (uint16_t)slot;
+            }
+            nalloc += popc(am);
             const bool nw = act && slot != kNoSlot;
             const uint64_t nm = ballot(nw);
             if (nw) {
                 meta[slot] = mbase;
                 if (policy == kPS) pfx[slot] = p;
             }
+            bool ok = true;
+            uint32_t val = 0;
+            if (isN) {
+                const TH hh = thash(kk, nbmask, rsmask);
+                val = (hh.tag << 16) | slot;
+                ok = tinsert(table, val, hh);
+            }
+            const uint64_t over = ballot(isN && !ok);
+            if (over) kick_lanes<true>(over, val, kk);
             if (policy == kS3) {
                 bool gh = false;
-                const uint64_t kk = nw ? key[slot] : 0ull;
-                if (nw && g_cap > 0) gh = gfind_clear(kk, thash(kk, gnbmask, rsmask));
+                if (nw && g_cap > 0) gh = ghost_take(isN ? kk : key[slot]);
                 const uint32_t rank = (uint32_t)(m - 1 - (before + mbcnt(nm)));
                 if (nw) {
                     const uint32_t np = tail + rank;
@@ -932,6 +943,7 @@ struct Replayer {
             before += popc(nm);
             wsync();
         }
+        hwm += nalloc < nfresh ? nalloc : nfresh;
         if (m > 0) {
             if (lane == 0) atomicAdd(&res[g], (uint32_t)m);
             resident += m;
@@ -955,7 +967,7 @@ struct Replayer {
             const uint32_t slot = act ? posslot[j] : kNoSlot;
             const bool rl = act && slot != kNoSlot;
             const uint64_t rm = ballot(rl);
-            uint32_t mt = rl ? meta[slot] : 0u;
+            const uint32_t mt = rl ? meta[slot] : 0u;
             if (policy == kS3) {
                 const bool inM = (mt & kQMain) != 0;
                 if (rl) meta[slot] = mt & ~kPin;
@@ -985,41 +997,54 @@ struct Replayer {
         }
         if (resident > rmax) rmax = resident;
         last_h = h; last_m = m; last_e = e; last_o = norph;
+        // prefix bits of the next request, with this request's updates
+        if (has_next && (nx.p >> 5) == w) {
+            nref |= bit;
+            if (adm_now) nadm |= bit;
+        }
+        kn = knext;
+        bref = nref;
+        badm = nadm;
         PROF_T(p7);
         PROF_ADD(6, p6, p7);
         return true;
     }
-    int last_h, last_m, last_e, last_o;
 
     // ============================================================ run
     DEV void init() {
         const int lane = lane_id();
         const uint32_t nte = 8u * (nbmask + 1u);
         for (uint32_t i = lane; i < nte; i += 64) table[i] = kEmpty;
-        for (int i = lane; i < pool; i += 64) {
-            meta[i] = 0;
-            fstack[i] = (uint16_t)(pool - 1 - i);
-        }
+        for (int i = lane; i < C; i += 64) meta[i] = 0;
         for (int i = lane; i < 64; i += 64) { evown[i] = 0ull; res[i] = 0u; }
-        for (int i = lane; i < 196; i += 64) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
+        if (policy == kPS)
+            for (int i = lane; i < 196; i += 64) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
         for (int i = lane; i < 2 * I.n_prefix_words; i += 64) bits[i] = 0u;
-        if (policy == kS3) {
+        if (policy == kS3 && g_cap > 0) {
             const uint32_t nge = 8u * (gnbmask + 1u);
             for (uint32_t i = lane; i < nge; i += 64) gtable[i] = kEmpty;
         }
         head = tail = 0;
-        top = pool;
+        hwm = 0;
+        nvict = 0;
         resident = 0;
         s_size = s_unp = m_unp = 0;
         gseq = curS = curM = 0;
+        gpre = 0;
+        gpre_base = 0xFFFFFFFFu;
         rmax = 0;
-        ev_total = s3_moves = s3_reins = s3_ghits = s3_gins = 0;
         err = 0;
+        ev_total = in_vgpr((uint64_t)0);
+        s3_moves = in_vgpr((uint64_t)0);
+        s3_reins = in_vgpr((uint64_t)0);
+        s3_ghits = in_vgpr((uint64_t)0);
+        s3_gins = in_vgpr((uint64_t)0);
 #pragma unroll
         for (int cc = 0; cc < 4; ++cc) { bal[cc] = cc < K ? beta[cc] : 0; last[cc] = 0; }
         c_req = c_probe = c_hit = c_miss = c_charged = c_evc = c_promo = c_gated = c_orph = c_dup = c_trunc = 0;
         d_max = d_sum = 0;
         r_max = 0;
+        last_h = last_m = last_e = last_o = 0;
 #ifdef PC_PROFILE
         for (int i = 0; i < 8; ++i) prof[i] = 0;
 #endif
@@ -1032,14 +1057,32 @@ struct Replayer {
         int32_t status = 0;
         int64_t tprev = 0, tlast = 0;
         const int64_t nreq = T.n_req;
+        Req q = {};
+        uint64_t kn = 0;
+        uint32_t bref = 0, badm = 0;
+        if (nreq > 0) {
+            q = load_req(0);
+            kn = (q.nfull > lane && q.ko >= 0 && q.ko + q.nfull <= T.n_keys) ? T.keys[q.ko + lane] : 0ull;
+            if ((int64_t)q.p < T.n_prefix) {
+                bref = bits[q.p >> 5];
+                badm = bits[I.n_prefix_words + (q.p >> 5)];
+            }
+        }
         for (int64_t r = 0; r < nreq; ++r) {
-            if (!request(r, tprev)) { status = -1; break; }
+            const bool has_next = r + 1 < nreq;
+            Req nx = {};
+            if (has_next) nx = load_req(r + 1);
+            // a malformed next request must not be prefetched from
+            const bool nx_ok = has_next && nx.ko >= 0 && nx.nfull >= 0 && nx.ko + nx.nfull <= T.n_keys &&
+                               (int64_t)nx.p < T.n_prefix;
+            if (!request(r, q, tprev, kn, bref, badm, nx, nx_ok)) { status = -1; break; }
             if (err) { status = err; break; }
             tlast = tprev;
             if (per_req && I.per_req_off >= 0 && lane == 0) {
                 int32_t *o = per_req + I.per_req_off + 4 * r;
                 o[0] = last_h; o[1] = last_m; o[2] = last_e; o[3] = last_o;
             }
+            q = nx;
         }
         wsync();
         // stats record: 64 groups x 17 int64, then the instance block
@@ -1049,22 +1092,22 @@ struct Replayer {
         const int64_t dend = (grp && ok && nreq > 0) ? raw_debt(tlast) : 0;
         const uint64_t ev_own = grp ? evown[lane] : 0ull;
         const uint32_t rr = grp ? res[lane] : 0u;
-        int64_t v[kGroupFields] = {(int64_t)c_req, (int64_t)c_probe, (int64_t)c_hit, (int64_t)c_miss,
-                                   (int64_t)c_charged, (int64_t)ev_own, (int64_t)c_evc, (int64_t)c_promo,
-                                   (int64_t)c_gated, (int64_t)c_orph, (int64_t)c_dup, (int64_t)c_trunc,
-                                   dend, d_max, d_sum, (int64_t)rr, (int64_t)r_max};
+        const int64_t v[kGroupFields] = {(int64_t)c_req, (int64_t)c_probe, (int64_t)c_hit, (int64_t)c_miss,
+                                         (int64_t)c_charged, (int64_t)ev_own, (int64_t)c_evc, (int64_t)c_promo,
+                                         (int64_t)c_gated, (int64_t)c_orph, (int64_t)c_dup, (int64_t)c_trunc,
+                                         dend, d_max, d_sum, (int64_t)rr, (int64_t)r_max};
 #pragma unroll
         for (int f = 0; f < kGroupFields; ++f) o[f] = (ok && grp) ? v[f] : 0;
         if (lane == 0) {
-            int64_t *q = st + kInstOffset;
-            q[0] = ok ? (int64_t)ev_total : 0;
-            q[1] = ok ? (int64_t)s3_moves : 0;
-            q[2] = ok ? (int64_t)s3_reins : 0;
-            q[3] = ok ? (int64_t)s3_ghits : 0;
-            q[4] = ok ? (int64_t)s3_gins : 0;
-            q[5] = ok ? (int64_t)resident : 0;
-            q[6] = ok ? (int64_t)rmax : 0;
-            q[7] = (int64_t)(uint32_t)status;   // status in the low 32 bits
+            int64_t *qq = st + kInstOffset;
+            qq[0] = ok ? (int64_t)ev_total : 0;
+            qq[1] = ok ? (int64_t)s3_moves : 0;
+            qq[2] = ok ? (int64_t)s3_reins : 0;
+            qq[3] = ok ? (int64_t)s3_ghits : 0;
+            qq[4] = ok ? (int64_t)s3_gins : 0;
+            qq[5] = ok ? (int64_t)resident : 0;
+            qq[6] = ok ? (int64_t)rmax : 0;
+            qq[7] = (int64_t)(uint32_t)status;   // status in the low 32 bits
         }
 #ifdef PC_PROFILE
         if (lane < 8) st[63 * kGroupFields + lane] = (int64_t)prof[lane];

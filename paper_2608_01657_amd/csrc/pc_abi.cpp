@@ -46,7 +46,7 @@ int64_t lds_limit() {
     static std::mutex mu;
     static int64_t cache[64] = {0};
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 65536;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 65536 - pcr::replay_static_lds_bytes() - 256;
     std::lock_guard<std::mutex> lk(mu);
     if (cache[dev] == 0) {
         int v = 0;
@@ -54,7 +54,8 @@ int64_t lds_limit() {
             v = 65536;
         cache[dev] = v;
     }
-    return cache[dev];
+    // the replay kernel's static exchange area shares the same LDS
+    return cache[dev] - pcr::replay_static_lds_bytes() - 256;
 }
 
 struct Plan {

@@ -79,6 +79,7 @@ hipError_t launch_hash(const int32_t *tokens, int64_t n_tokens, const int64_t *t
                        const int32_t *len, const int32_t *ns, const int64_t *key_off,
                        int64_t n_req, uint64_t *keys, int64_t n_keys, int32_t *status,
                        hipStream_t s);
+int32_t replay_static_lds_bytes();
 hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order,
                          int32_t n_launch, int32_t lds_bytes, bool in_lds, uint8_t *ws,
                          int64_t *stats, int32_t *per_req, hipStream_t s);

@@ -1,5 +1,5 @@
 // pc_replay.hip -- batched replay of multi-tenant prefix-cache instances on
-// gfx950, one 64-lane wavefront per instance.
+// gfx950: one workgroup of 4 wavefronts (one per SIMD) per instance.
 //
 // Per request (Alg. 1 hooks and Alg. 2 reclamation of the paper):
 //   OnRequest           prior-reference bit of (g,p), recorded
@@ -16,6 +16,14 @@
 //                       the request returns to the free queue deepest first
 //   accounting          raw debt D_g (Eq. 3) and occupancy of every group
 //
+// Work split: per-block work (keys, log entries, new blocks) is spread over
+// the 256 threads; everything that is one value per instance (queue
+// pointers, counters) or one value per accounting group (balances, debts,
+// the argmax of Eq. 7: lane x = group x) is computed redundantly by all four
+// wavefronts from the same inputs, so it never has to be exchanged.  The only
+// exchange is a block-wide ballot (each wave's 64-bit ballot through LDS and
+// one barrier), which gives every thread block-wide counts and ranks.
+//
 // State of one instance (capacity C, largest request n_max):
 //   key[C] u64, stamp[C] u32, meta[C] u32     -- one slot per cached block
 //   table[8*NB] u32  2-choice bucketized hash, entry = tag16 | slot16
@@ -30,12 +38,12 @@
 // (keys of S3-FIFO's ghost entries) and the prefix bitmaps stay in HBM.
 //
 // Victims of one request are chosen in bulk: LRU takes the first e live log
-// entries with one ballot per 64 entries; PrefixShield turns the per-victim
-// argmax of Eq. 7 into runs (the winner keeps winning while its projected
-// debt stays above every other candidate's) and drains each run from the
-// group's per-segment cursor; S3-FIFO processes queue heads 64 at a time and
-// cuts each batch where the one-at-a-time rule would switch queues.  Each
-// shortcut reproduces the one-victim-at-a-time definition exactly.
+// entries, 256 per step; PrefixShield turns the per-victim argmax of Eq. 7
+// into runs (the winner keeps winning while its projected debt stays above
+// every other candidate's) and drains each run from the group's per-segment
+// cursor; S3-FIFO processes queue heads 256 at a time and cuts each batch
+// where the one-at-a-time rule would switch queues.  Each shortcut
+// reproduces the one-victim-at-a-time definition exactly.
 #include "pc_internal.h"
 
 namespace pcr {
@@ -43,33 +51,25 @@ namespace {
 
 #define DEV __device__ __forceinline__
 
+constexpr int kW = 4;              // wavefronts per instance
+constexpr int kB = 64 * kW;        // threads per instance
 constexpr int64_t kScale = 65536;
 constexpr uint16_t kNewMark = 0xFFFE;      // posslot: new block, slot not yet assigned
 constexpr int32_t kErrInternal = -5;
 
-DEV int lane_id() { return (int)__lane_id(); }
 DEV uint64_t ballot(bool p) { return __ballot(p); }
 DEV int popc(uint64_t m) { return __popcll(m); }
 DEV int mbcnt(uint64_t m) {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
-DEV int first_lane(uint64_t m) { return __ffsll((unsigned long long)m) - 1; }   // m != 0
-DEV int last_lane(uint64_t m) { return 63 - __clzll((unsigned long long)m); }  // m != 0
-// Lanes of one wavefront exchange data through LDS/global memory.  A wave's
-// memory instructions execute in program order, so a wavefront-scope fence
-// (no instruction, no wait) is enough to keep the compiler from reordering
-// one lane's store after another lane's later load.
-DEV void wsync() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
+DEV int first_bit(uint64_t m) { return __ffsll((unsigned long long)m) - 1; }   // m != 0
+DEV uint32_t rfl(uint32_t v) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)v); }
+DEV uint64_t rfl64(uint64_t v) { return ((uint64_t)rfl((uint32_t)(v >> 32)) << 32) | rfl((uint32_t)v); }
 DEV uint32_t bcast32(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
 DEV int64_t bcast64(int64_t v, int l) {
     uint32_t lo = bcast32((uint32_t)(uint64_t)v, l);
     uint32_t hi = bcast32((uint32_t)((uint64_t)v >> 32), l);
     return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-DEV uint64_t shfl64(uint64_t v, int src) {
-    uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src);
-    uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src);
-    return ((uint64_t)hi << 32) | lo;
 }
 DEV int64_t xor64(int64_t v, int m) {
     uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)(uint64_t)v, m);
@@ -88,16 +88,117 @@ DEV uint32_t wave_sum32(uint32_t v) {
     for (int m = 32; m; m >>= 1) v += (uint32_t)__shfl_xor((int)v, m);
     return bcast32(v, 0);
 }
-// Keep a wave-uniform value in a VGPR (it is only used in per-lane arithmetic)
-// so it does not occupy scalar registers.
+// position of the k-th (0-based) set bit of m (k < popc(m))
+DEV int nth_bit(uint64_t m, int k) {
+    int pos = 0;
+    for (int w = 32; w; w >>= 1) {
+        const uint64_t lowmask = (w == 64) ? ~0ull : ((1ull << w) - 1);
+        const int c = popc(m & lowmask);
+        if (k >= c) { k -= c; m >>= w; pos += w; }
+        else m &= lowmask;
+    }
+    return pos;
+}
+// Keep a wave-uniform value in a VGPR (it is only used in per-lane
+// arithmetic) so it does not occupy scalar registers.
 template <typename T>
 DEV T in_vgpr(T x) {
     asm volatile("" : "+v"(x));
     return x;
 }
 
-// Key -> two buckets, 16-bit tag, duplicate-set home.  Keys are usually hash
-// outputs already, but the ABI accepts any uint64, so mix with 32-bit ops.
+// Global-memory pointers.  Trace arrays reach the kernel through a
+// descriptor, so without the address space the compiler would use flat loads,
+// which also count against the LDS wait counter: every LDS wait would then
+// wait for the in-flight HBM prefetches.
+#define GLOBAL __attribute__((address_space(1)))
+template <typename T>
+DEV const GLOBAL T *gptr(const T *p) { return (const GLOBAL T *)p; }
+template <typename T>
+DEV GLOBAL T *gptr_rw(T *p) { return (GLOBAL T *)p; }
+
+// Block-wide ballot result: one 64-bit mask per wavefront.
+struct BMask {
+    uint64_t w[kW];
+    DEV int count() const {
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) c += popc(w[i]);
+        return c;
+    }
+    // set bits before thread (wid, lane)
+    DEV int rank(int wid) const {
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) c += i < wid ? popc(w[i]) : 0;
+        uint64_t mine = 0;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) mine = i == wid ? w[i] : mine;
+        return c + mbcnt(mine);
+    }
+    DEV bool any() const {
+        uint64_t a = 0;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) a |= w[i];
+        return a != 0;
+    }
+    // thread index (wid*64+lane) of the first set bit, or kB
+    DEV int first() const {
+#pragma unroll
+        for (int i = 0; i < kW; ++i)
+            if (w[i]) return 64 * i + first_bit(w[i]);
+        return kB;
+    }
+    // thread index of the k-th set bit (k < count())
+    DEV int nth(int k) const {
+#pragma unroll
+        for (int i = 0; i < kW; ++i) {
+            const int c = popc(w[i]);
+            if (k < c) return 64 * i + nth_bit(w[i], k);
+            k -= c;
+        }
+        return kB;
+    }
+    // keep only bits of threads below index t
+    DEV BMask below(int t) const {
+        BMask r;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) {
+            const int lo = t - 64 * i;
+            r.w[i] = lo >= 64 ? w[i] : (lo <= 0 ? 0ull : (w[i] & ((1ull << lo) - 1)));
+        }
+        return r;
+    }
+    DEV BMask andnot(const BMask &o) const {
+        BMask r;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) r.w[i] = w[i] & ~o.w[i];
+        return r;
+    }
+    DEV BMask operator|(const BMask &o) const {
+        BMask r;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) r.w[i] = w[i] | o.w[i];
+        return r;
+    }
+};
+
+// Per-workgroup exchange area (static LDS, both variants).
+struct Coll {
+    unsigned long long m[2][8][kW];   // block ballots, double-buffered
+    uint32_t novf;                    // pending cuckoo displacements
+    uint32_t qf;                      // prior-reference / admitted bits of the request
+    uint32_t nghost;                  // ghost hits among the request's new blocks
+    int32_t kerr;                     // displacement failure
+    uint32_t pad;
+    uint64_t kkey[kB];                // displacement scratch: keys
+    uint32_t kval[kB];                // displacement scratch: entries
+    uint32_t kmain[kB];               // 1 = main table, 0 = ghost table
+};
+
+// Key -> two buckets, 16-bit tag (never 0xFFFF, so empty entries never match
+// a tag), duplicate-set home.  Keys are usually hash outputs already, but the
+// ABI accepts any uint64, so mix with 32-bit ops.
 struct TH {
     uint32_t b1, b2, tag, rhome;
 };
@@ -115,7 +216,8 @@ DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rsmask) {
     h.b1 = x & nbmask;
     h.b2 = y & nbmask;
     if (h.b2 == h.b1) h.b2 = h.b1 ^ 1u;
-    h.tag = y >> 16;
+    const uint32_t t = y >> 16;
+    h.tag = t == 0xFFFFu ? 0xFFFEu : t;
     h.rhome = (x >> 11) & rsmask;
     return h;
 }
@@ -144,10 +246,13 @@ struct Req {
 
 template <bool kLds>
 struct Replayer {
-    // ---------------- configuration (wave-uniform)
+    Coll &X;
+    const int tid, wid, lane;
+    int cb;                   // ballot buffer in use
+    // ---------------- configuration (uniform)
     const DevInst &I;
     const DevTrace &T;
-    int policy, C, flags, G, K, nseg, maxn;
+    int policy, C, flags, G, K, nseg;
     int64_t eps;
     uint32_t nbmask, rsmask, lmask, R, gnbmask, grmask;
     int32_t s_cap, g_cap, move_thr;
@@ -157,9 +262,13 @@ struct Replayer {
     uint32_t *stamp, *meta, *table, *rset, *cnt, *cur, *res, *pfx, *gtable;
     uint16_t *log, *posslot, *vlist;
     unsigned long long *evown;
-    uint32_t *bits;
-    uint64_t *gring;
-    // ---------------- uniform state
+    GLOBAL uint32_t *bits;
+    GLOBAL uint64_t *gring;
+    const GLOBAL uint64_t *tkeys;
+    const GLOBAL int64_t *tkoff, *ttick;
+    const GLOBAL uint8_t *tgroup, *tcontract;
+    const GLOBAL uint32_t *tprefix;
+    // ---------------- uniform state (identical in every wavefront)
     uint32_t head, tail;      // live log window [head, tail)
     int32_t hwm;              // slots [hwm, C) have never been used
     int32_t nvict;            // victims of the current request
@@ -168,10 +277,7 @@ struct Replayer {
     uint32_t gseq, curS, curM;
     int32_t rmax;
     int32_t err;
-    // ghost ring keys prefetched for the next expiry batch
-    uint64_t gpre;
-    uint32_t gpre_base;
-    // ---------------- statistics and group state (VGPRs; lane x = group x)
+    // ---------------- statistics and group state (lane x = group x, VGPRs)
     uint64_t ev_total, s3_moves, s3_reins, s3_ghits, s3_gins;
     int64_t bal[4], last[4];
     uint64_t c_req, c_probe, c_hit, c_miss, c_charged, c_evc, c_promo, c_gated, c_orph, c_dup, c_trunc;
@@ -182,13 +288,14 @@ struct Replayer {
     uint64_t prof[8];
 #endif
 
-    DEV Replayer(const DevInst &inst, const DevTrace &tr, uint8_t *sbase, uint8_t *ws) : I(inst), T(tr) {
+    DEV Replayer(Coll &coll, const DevInst &inst, const DevTrace &tr, uint8_t *sbase, uint8_t *ws)
+        : X(coll), tid((int)threadIdx.x), wid((int)rfl(threadIdx.x >> 6)), lane((int)__lane_id()), cb(0),
+          I(inst), T(tr) {
         policy = I.policy;
         C = I.capacity;
         flags = I.flags;
         G = T.n_groups;
         K = I.n_contracts;
-        maxn = I.maxn;
         nseg = (policy == kPS && !(flags & kFlagNoSeg)) ? 3 : 1;
         eps = I.eps;
         nbmask = (1u << I.nb_log2) - 1u;
@@ -221,8 +328,52 @@ struct Replayer {
         posslot = reinterpret_cast<uint16_t *>(sbase + I.o_posslot);
         vlist = reinterpret_cast<uint16_t *>(sbase + I.o_vlist);
         evown = reinterpret_cast<unsigned long long *>(sbase + I.o_evown);
-        bits = reinterpret_cast<uint32_t *>(ws + I.ws_bits);
-        gring = reinterpret_cast<uint64_t *>(ws + I.ws_gring);
+        bits = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_bits));
+        gring = gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_gring));
+        tkeys = gptr(T.keys);
+        tkoff = gptr(T.key_off);
+        ttick = gptr(T.tick);
+        tgroup = gptr(T.group);
+        tcontract = gptr(T.contract);
+        tprefix = gptr(T.prefix);
+    }
+
+    // ============================================================ sync
+    // Barrier making state-memory writes visible to the workgroup.  With the
+    // state in LDS, only LDS is fenced, so global prefetches stay in flight.
+    DEV void bsync() {
+        if constexpr (kLds) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        } else {
+            __syncthreads();
+        }
+    }
+    // Barrier for global memory too (ghost ring, prefix bitmaps).
+    DEV void gsync() { __syncthreads(); }
+
+    template <int M>
+    DEV void bballot(const bool (&p)[M], BMask (&out)[M]) {
+        uint64_t b[M];
+#pragma unroll
+        for (int i = 0; i < M; ++i) b[i] = ballot(p[i]);
+        if (lane == 0) {
+#pragma unroll
+            for (int i = 0; i < M; ++i) X.m[cb][i][wid] = b[i];
+        }
+        bsync();
+#pragma unroll
+        for (int i = 0; i < M; ++i)
+#pragma unroll
+            for (int ww = 0; ww < kW; ++ww) out[i].w[ww] = rfl64(X.m[cb][i][ww]);
+        cb ^= 1;
+    }
+    DEV BMask bballot1(bool p) {
+        bool a[1] = {p};
+        BMask o[1];
+        bballot<1>(a, o);
+        return o[0];
     }
 
     // ============================================================ debt (lane x)
@@ -236,6 +387,7 @@ struct Replayer {
         return bal[c] + (int64_t)lo;
     }
     DEV int64_t raw_debt(int64_t t) const {   // Eq. 3
+        if (K == 1) { const int64_t b = eff(0, t); return b < 0 ? -b : 0; }
         int64_t d = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c)
@@ -243,6 +395,7 @@ struct Replayer {
         return d;
     }
     DEV int64_t norm_debt(int64_t t) const {  // Eq. 5, 1/w_c in Q16
+        if (K == 1) { const int64_t b = eff(0, t); return b < 0 ? -b : 0; }   // w = 1
         int64_t d = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c)
@@ -257,6 +410,7 @@ struct Replayer {
         return d;
     }
     DEV int64_t decrement(int64_t t) const {  // Eq. 8: 1/W_g
+        if (K == 1) return eff(0, t) < 0 ? kScale : 0;
         int64_t m = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c)
@@ -265,7 +419,6 @@ struct Replayer {
     }
 
     // ============================================================ tables
-    // Both buckets of a key: 16 entries.
     DEV void load_buckets(const uint32_t *tb, const TH &h, uint32_t e[16]) const {
         const uint4 *t4 = reinterpret_cast<const uint4 *>(tb);
         const uint4 a0 = t4[2 * h.b1], a1 = t4[2 * h.b1 + 1], c0 = t4[2 * h.b2], c1 = t4[2 * h.b2 + 1];
@@ -273,15 +426,29 @@ struct Replayer {
         e[8] = c0.x; e[9] = c0.y; e[10] = c0.z; e[11] = c0.w; e[12] = c1.x; e[13] = c1.y; e[14] = c1.z; e[15] = c1.w;
     }
     DEV uint32_t epos(const TH &h, int i) const { return i < 8 ? 8 * h.b1 + i : 8 * h.b2 + (i - 8); }
-    // slot of key k in the main table, or -1
-    DEV int tfind(uint64_t k, const TH &h) const {
+    // Probe both buckets of k.  Returns the number of tag matches; `cand` is
+    // the slot of the last one.  With one match the caller confirms the key
+    // (together with its other loads); with several, tfind_slow decides.
+    DEV int tprobe(const TH &h, uint32_t &cand) const {
         uint32_t e[16];
         load_buckets(table, h, e);
-        int s = -1;
+        int nm = 0;
+        uint32_t cv = 0;
 #pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const bool mt = (e[i] >> 16) == h.tag;
+            nm += mt;
+            cv = mt ? e[i] : cv;
+        }
+        cand = cv & 0xFFFFu;
+        return nm;
+    }
+    DEV int tfind_slow(uint64_t k, const TH &h) const {
+        uint32_t e[16];
+        load_buckets(table, h, e);
         for (int i = 0; i < 16; ++i)
-            if (s < 0 && e[i] != kEmpty && (e[i] >> 16) == h.tag && key[e[i] & 0xFFFFu] == k) s = (int)(e[i] & 0xFFFFu);
-        return s;
+            if ((e[i] >> 16) == h.tag && key[e[i] & 0xFFFFu] == k) return (int)(e[i] & 0xFFFFu);
+        return -1;
     }
     // clear the entry holding exactly `val` (if present)
     DEV void tclear_exact(uint32_t *tb, uint32_t val, const TH &h) {
@@ -289,8 +456,7 @@ struct Replayer {
         load_buckets(tb, h, e);
         int at = -1;
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-            if (at < 0 && e[i] == val) at = i;
+        for (int i = 0; i < 16; ++i) at = (at < 0 && e[i] == val) ? i : at;
         if (at >= 0) tb[epos(h, at)] = kEmpty;
     }
     // Parallel insert of a new entry; false when both buckets are full.
@@ -310,11 +476,16 @@ struct Replayer {
         }
         return false;
     }
-    // Serial cuckoo displacement for an entry that found both buckets full.
-    template <bool kMain>
-    DEV bool kick(uint32_t val, uint64_t k) {
-        uint32_t *tb = kMain ? table : gtable;
-        const uint32_t msk = kMain ? nbmask : gnbmask;
+    // Record an entry that found both buckets full; kick_pending() places it.
+    DEV void defer_kick(uint32_t val, uint64_t k, bool main) {
+        const uint32_t i = atomicAdd(&X.novf, 1u);
+        X.kval[i] = val;
+        X.kkey[i] = k;
+        X.kmain[i] = main ? 1u : 0u;
+    }
+    // Serial cuckoo displacement, one thread.
+    DEV bool kick(uint32_t *tb, bool main, uint32_t val, uint64_t k) {
+        const uint32_t msk = main ? nbmask : gnbmask;
         uint32_t cv = val;
         uint64_t ck = k;
         uint32_t from = 0xFFFFFFFFu;
@@ -330,41 +501,40 @@ struct Replayer {
             const uint32_t victim = tb[8 * b + w];
             tb[8 * b + w] = cv;
             cv = victim;
-            ck = kMain ? key[victim & 0xFFFFu] : gring[victim & grmask];
+            ck = main ? key[victim & 0xFFFFu] : gring[victim & grmask];
             from = b;
         }
         return false;
     }
-    template <bool kMain>
-    DEV void kick_lanes(uint64_t over, uint32_t val, uint64_t k) {
-        wsync();
-        while (over) {
-            const int l = first_lane(over);
-            over &= over - 1;
-            const uint32_t v = bcast32(val, l);
-            const uint64_t kk = (uint64_t)bcast64((int64_t)k, l);
-            bool ok = true;
-            if (lane_id() == 0) ok = kick<kMain>(v, kk);
-            if (!bcast32(ok ? 1u : 0u, 0)) err = kErrInternal;
-            wsync();
+    // Called by all threads after a barrier that follows defer_kick calls.
+    DEV void kick_pending() {
+        const uint32_t nk = rfl(X.novf);
+        if (nk == 0) return;
+        if (tid == 0) {
+            for (uint32_t i = 0; i < nk; ++i) {
+                const bool main = X.kmain[i] != 0;
+                if (!kick(main ? table : gtable, main, X.kval[i], X.kkey[i])) X.kerr = kErrInternal;
+            }
+            X.novf = 0;
         }
+        gsync();
+        if (rfl((uint32_t)X.kerr)) err = kErrInternal;
     }
 
     // ============================================================ eviction core
-    DEV void evict_lanes(bool v, uint32_t s) {
-        const uint64_t vm = ballot(v);
-        if (v) {
-            const uint32_t mt = meta[s];
-            const uint32_t o = owner_of(mt);
-            atomicAdd(&evown[o], 1ull);
-            atomicSub(&res[o], 1u);
-            const uint64_t k = key[s];
-            const TH h = thash(k, nbmask, rsmask);
-            tclear_exact(table, (h.tag << 16) | s, h);
-            meta[s] = 0;
-            vlist[nvict + mbcnt(vm)] = (uint16_t)s;
-        }
-        const int nv = popc(vm);
+    // Thread holding victim slot s (vrank = its rank among this step's victims).
+    DEV void evict_elem(uint32_t s, int vrank) {
+        const uint32_t mt = meta[s];
+        const uint32_t o = owner_of(mt);
+        atomicAdd(&evown[o], 1ull);
+        atomicSub(&res[o], 1u);
+        const uint64_t k = key[s];
+        const TH h = thash(k, nbmask, rsmask);
+        tclear_exact(table, (h.tag << 16) | s, h);
+        meta[s] = 0;
+        vlist[nvict + vrank] = (uint16_t)s;
+    }
+    DEV void evicted(int nv) {
         nvict += nv;
         resident -= nv;
         ev_total += (uint64_t)nv;
@@ -373,35 +543,33 @@ struct Replayer {
     // Compaction of the free-queue log: live entries keep their order and
     // are renumbered from `head`; all cursors restart at `head`.
     DEV void compact() {
-        wsync();
-        const int lane = lane_id();
+        bsync();
         uint32_t nw = head;
-        for (uint32_t p0 = head; p0 < tail; p0 += 64) {
-            const uint32_t pos = p0 + lane;
+        for (uint32_t p0 = head; p0 < tail; p0 += kB) {
+            const uint32_t pos = p0 + tid;
             const bool valid = pos < tail;
             const uint32_t s = valid ? log[pos & lmask] : 0;
             const bool live = valid && (meta[s] & kInLog) && stamp[s] == pos;
-            const uint64_t lm = ballot(live);
-            wsync();
+            const BMask lm = bballot1(live);   // every read of this step is done
             if (live) {
-                const uint32_t np = nw + (uint32_t)mbcnt(lm);
+                const uint32_t np = nw + (uint32_t)lm.rank(wid);
                 log[np & lmask] = (uint16_t)s;
                 stamp[s] = np;
             }
-            nw += (uint32_t)popc(lm);
-            wsync();
+            nw += (uint32_t)lm.count();
+            bsync();
         }
         tail = nw;
         if (policy == kPS)
-            for (int i = lane; i < 196; i += 64) cur[i] = head;
+            for (int i = tid; i < 196; i += kB) cur[i] = head;
         curS = curM = head;
-        wsync();
+        bsync();
     }
     DEV void ensure_room(uint32_t k) {
         if (tail + k - head <= R) return;
         if (policy == kPS) {   // lowest cursor of a non-empty queue bounds every live entry
             uint32_t m = tail;
-            for (int i = lane_id(); i < 192; i += 64)
+            for (int i = lane; i < 192; i += 64)
                 if (cnt[i] > 0 && cur[i] < m) m = cur[i];
             m = wave_min32(m);
             if (m > head) head = m;
@@ -414,24 +582,23 @@ struct Replayer {
 
     // ---------------------------------------------------------------- LRU
     DEV void evict_lru(int e) {
-        const int lane = lane_id();
         int rem = e;
         while (rem > 0 && err == 0) {
-            const uint32_t pos = head + lane;
+            const uint32_t pos = head + tid;
             const bool valid = pos < tail;
             const uint32_t s = valid ? log[pos & lmask] : 0;
             const bool live = valid && (meta[s] & kInLog) && stamp[s] == pos;
-            const uint64_t lm = ballot(live);
-            const bool v = live && mbcnt(lm) < rem;
-            const uint64_t vm = ballot(v);
-            const int nv = popc(vm);
-            wsync();
-            evict_lanes(v, s);
-            if (nv == rem) head = head + (uint32_t)last_lane(vm) + 1;
-            else head = (head + 64 < tail) ? head + 64 : tail;
+            const BMask lm = bballot1(live);
+            const int rk = lm.rank(wid);
+            const int tot = lm.count();
+            const int nv = tot < rem ? tot : rem;
+            if (live && rk < rem) evict_elem(s, rk);
+            evicted(nv);
+            if (nv == rem) head = head + (uint32_t)lm.nth(rem - 1) + 1;
+            else head = (head + kB < tail) ? head + kB : tail;
             rem -= nv;
             if (nv == 0 && head >= tail) err = kErrInternal;
-            wsync();
+            bsync();
         }
     }
 
@@ -439,56 +606,55 @@ struct Replayer {
     // Take k victims from queue ci in free-queue order.  x < 0: any owner;
     // s < 0: any class (no segmentation).
     DEV void ps_take(int x, int s, int ci, int k) {
-        const int lane = lane_id();
-        uint32_t c = cur[ci];
+        uint32_t c = rfl(cur[ci]);
         int rem = k;
         while (rem > 0 && err == 0) {
-            const uint32_t pos = c + lane;
+            const uint32_t pos = c + tid;
             const bool valid = pos < tail;
             const uint32_t sl = valid ? log[pos & lmask] : 0;
             const uint32_t mt = valid ? meta[sl] : 0;
             const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
             const bool match = live && (x < 0 || (int)owner_of(mt) == x) && (s < 0 || (int)cls_of(mt) == s);
-            const uint64_t mm = ballot(match);
-            const bool v = match && mbcnt(mm) < rem;
-            const uint64_t vm = ballot(v);
-            const int nv = popc(vm);
-            wsync();
-            if (v) atomicSub(&cnt[3 * owner_of(mt) + (s < 0 ? 0u : (uint32_t)s)], 1u);
-            evict_lanes(v, sl);
-            if (nv == rem) c = c + (uint32_t)last_lane(vm) + 1;
-            else c = (c + 64 < tail) ? c + 64 : tail;
+            const BMask mm = bballot1(match);
+            const int rk = mm.rank(wid);
+            const int tot = mm.count();
+            const int nv = tot < rem ? tot : rem;
+            if (match && rk < rem) {
+                atomicSub(&cnt[3 * owner_of(mt) + (s < 0 ? 0u : (uint32_t)s)], 1u);
+                evict_elem(sl, rk);
+            }
+            evicted(nv);
+            if (nv == rem) c = c + (uint32_t)mm.nth(rem - 1) + 1;
+            else c = (c + kB < tail) ? c + kB : tail;
             rem -= nv;
             if (nv == 0 && c >= tail) err = kErrInternal;
-            wsync();
+            bsync();
         }
-        if (lane == 0) cur[ci] = c;
-        wsync();
+        if (tid == 0) cur[ci] = c;
+        bsync();
     }
     // Oldest live entry of queue (x, s); advances that queue's cursor to it.
     DEV uint32_t ps_headpos(int x, int s) {
-        const int lane = lane_id();
         const int ci = 3 * x + (s < 0 ? 0 : s);
-        uint32_t c = cur[ci];
+        uint32_t c = rfl(cur[ci]);
         uint32_t found = 0xFFFFFFFFu;
         while (c < tail) {
-            const uint32_t pos = c + lane;
+            const uint32_t pos = c + tid;
             const bool valid = pos < tail;
             const uint32_t sl = valid ? log[pos & lmask] : 0;
             const uint32_t mt = valid ? meta[sl] : 0;
             const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
             const bool match = live && (int)owner_of(mt) == x && (s < 0 || (int)cls_of(mt) == s);
-            const uint64_t mm = ballot(match);
-            if (mm) { found = c + (uint32_t)first_lane(mm); c = found; break; }
-            c = (c + 64 < tail) ? c + 64 : tail;
+            const BMask mm = bballot1(match);
+            if (mm.any()) { found = c + (uint32_t)mm.first(); c = found; break; }
+            c = (c + kB < tail) ? c + kB : tail;
         }
-        wsync();
-        if (lane == 0) cur[ci] = c;
-        wsync();
+        bsync();
+        if (tid == 0) cur[ci] = c;
+        bsync();
         return found;
     }
     DEV void evict_ps(int e, int64_t t) {
-        const int lane = lane_id();
         const bool grp = lane < G;
         int64_t P = 0, D = 0;
         uint32_t avail = 0;
@@ -504,7 +670,7 @@ struct Replayer {
             if (!Em) break;
             const int64_t pm = wave_max64(inE ? P : -1);       // Eq. 7
             uint64_t tied = ballot(inE && P == pm);
-            int gs = first_lane(tied);
+            int gs = first_bit(tied);
             if (popc(tied) > 1) {   // ties: lowest non-empty segment, then oldest head entry
                 uint32_t seg = 3;
                 if (grp)
@@ -512,11 +678,11 @@ struct Replayer {
                         if (cnt[3 * lane + s] > 0) seg = (uint32_t)s;
                 const int mseg = (int)wave_min32(((tied >> lane) & 1) ? seg : 3u);
                 tied &= ballot(seg == (uint32_t)mseg);
-                gs = first_lane(tied);
+                gs = first_bit(tied);
                 if (popc(tied) > 1) {
                     uint32_t best = 0xFFFFFFFFu;
                     for (uint64_t tm = tied; tm; tm &= tm - 1) {
-                        const int x = first_lane(tm);
+                        const int x = first_bit(tm);
                         const uint32_t hp = ps_headpos(x, nseg == 1 ? -1 : mseg);
                         if (hp < best) { best = hp; gs = x; }
                     }
@@ -536,7 +702,7 @@ struct Replayer {
             } else {
                 int kk = (int)k;
                 for (int s = 0; s < 3 && kk > 0; ++s) {
-                    const int cs = (int)cnt[3 * gs + s];
+                    const int cs = (int)rfl(cnt[3 * gs + s]);
                     const int tk = cs < kk ? cs : kk;
                     if (tk > 0) ps_take(gs, s, 3 * gs + s, tk);
                     kk -= tk;
@@ -562,49 +728,37 @@ struct Replayer {
     }
 
     // ---------------------------------------------------------------- S3-FIFO
-    DEV void ghost_prefetch() {
-        if (g_cap > 0) {
-            gpre_base = gseq;
-            gpre = gring[(gseq - (uint32_t)g_cap + (uint32_t)lane_id()) & grmask];
-        }
-    }
-    // Ghost insertion of the keys of lanes `v`, in lane order.  The ghost
-    // keeps the last g_cap insertions: entries older than the batch that
-    // leave the window are removed, and batch entries that would already
-    // have left it by the batch's end are never inserted.
-    DEV void ghost_insert(bool v, uint64_t k) {
-        const uint64_t vm = ballot(v);
-        const int nv = popc(vm);
+    // Ghost insertion for the threads with v (rk = rank among them, nv =
+    // count).  The ghost keeps the last g_cap insertions: entries older than
+    // the batch that leave the window are removed, and batch entries that
+    // would already have left it by the batch's end are never inserted.
+    DEV void ghost_insert(bool v, uint64_t k, int rk, int nv) {
         s3_gins += (uint64_t)nv;
         if (g_cap > 0 && nv > 0) {
-            const int rk = mbcnt(vm);
+            gsync();   // ring writes of earlier steps are visible
             const uint32_t seq = gseq + (uint32_t)rk;
             const uint32_t gend = gseq + (uint32_t)nv;
-            const uint64_t kpre = shfl64(gpre, rk);   // gring[(seq - g_cap) & grmask], prefetched
             if (v && (int64_t)seq >= (int64_t)g_cap) {
                 const uint32_t x = seq - (uint32_t)g_cap;
                 if (x < gseq) {
                     const uint32_t xp = x & grmask;
-                    const uint64_t kx = gpre_base == gseq ? kpre : gring[xp];
+                    const uint64_t kx = gring[xp];
                     const TH hx = thash(kx, gnbmask, rsmask);
                     tclear_exact(gtable, (hx.tag << 16) | xp, hx);
                 }
             }
-            wsync();
+            bsync();
             const bool ins = v && (int64_t)seq + g_cap >= (int64_t)gend;
-            const TH h = thash(k, gnbmask, rsmask);
-            const uint32_t val = (h.tag << 16) | (seq & grmask);
-            bool ok = true;
             if (v) gring[seq & grmask] = k;
-            if (ins) ok = tinsert(gtable, val, h);
-            const uint64_t over = ballot(ins && !ok);
-            if (over) kick_lanes<false>(over, val, k);
-            wsync();
-            gseq += (uint32_t)nv;
-            ghost_prefetch();
-        } else {
-            gseq += (uint32_t)nv;
+            if (ins) {
+                const TH h = thash(k, gnbmask, rsmask);
+                const uint32_t val = (h.tag << 16) | (seq & grmask);
+                if (!tinsert(gtable, val, h)) defer_kick(val, k, false);
+            }
+            gsync();
+            kick_pending();
         }
+        gseq += (uint32_t)nv;
     }
     // ghost hit for key k: remove it and report true
     DEV bool ghost_take(uint64_t k) {
@@ -613,19 +767,17 @@ struct Replayer {
         load_buckets(gtable, h, e);
         int at = -1;
         for (int i = 0; i < 16; ++i)
-            if (at < 0 && e[i] != kEmpty && (e[i] >> 16) == h.tag && gring[e[i] & grmask] == k) at = i;
+            if (at < 0 && (e[i] >> 16) == h.tag && gring[e[i] & grmask] == k) at = i;
         if (at >= 0) gtable[epos(h, at)] = kEmpty;
         return at >= 0;
     }
     DEV void evict_s3(int e) {
-        const int lane = lane_id();
-        const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
         int rem = e;
         uint32_t spS = curS, spM = curM;
         uint32_t keptS = 0xFFFFFFFFu, keptM = 0xFFFFFFFFu;
         while (rem > 0 && err == 0) {
-            if (tail + 64 - head > R) {
-                ensure_room(64);
+            if (tail + kB - head > R) {
+                ensure_room(kB);
                 spS = curS; spM = curM;
                 keptS = keptM = 0xFFFFFFFFu;
             }
@@ -633,47 +785,45 @@ struct Replayer {
             const uint32_t sp = useS ? spS : spM;
             const uint32_t lim = tail;
             if (sp >= lim) { err = kErrInternal; break; }
-            const uint32_t pos = sp + lane;
+            const uint32_t pos = sp + tid;
             const bool valid = pos < lim;
             const uint32_t sl = valid ? log[pos & lmask] : 0;
             const uint32_t mt = valid ? meta[sl] : 0;
             const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
             const bool inQ = live && (useS ? !(mt & kQMain) : (mt & kQMain) != 0);
             const bool cand = inQ && !(mt & kPin);
-            const uint64_t candm = ballot(cand);
-            const int crk = mbcnt(candm);
             const uint32_t f = freq_of(mt);
+            // small queue: move (accessed) or evict into the ghost;
+            // main queue: reinsert (freq > 0) or evict
+            const bool mv = cand && (useS ? (int)f >= move_thr : f > 0);
+            bool p3[3] = {cand, mv, inQ};
+            BMask m3[3];
+            bballot<3>(p3, m3);
+            const BMask &candm = m3[0], &mvm = m3[1], &inQm = m3[2];
+            const BMask evm = candm.andnot(mvm);
+            const int crk = candm.rank(wid);
+            const int mb = mvm.rank(wid);
+            const int eb = evm.rank(wid);
             bool ok;
-            bool mv;
-            if (useS) {   // small queue: move (accessed) or evict into the ghost
-                mv = cand && (int)f >= move_thr;
-                const uint64_t mvm = ballot(mv);
-                const int mb = popc(mvm & below);
-                const int eb = popc(candm & ~mvm & below);
-                const bool useS_i = (s_size - crk >= s_cap && s_unp - crk > 0) || (m_unp + mb == 0);
-                ok = cand && useS_i && eb < rem;
-            } else {      // main queue: reinsert (freq > 0) or evict
-                mv = cand && f > 0;
-                const uint64_t mvm = ballot(mv);
-                const int eb = popc(candm & ~mvm & below);
-                ok = cand && eb < rem && (m_unp - eb) > 0;
-            }
-            const uint64_t bad = candm & ~ballot(ok);
-            const int stop = bad ? first_lane(bad) : 64;
-            const bool proc = cand && lane < stop;
-            const bool pmove = proc && mv, pev = proc && !mv;
-            const uint64_t pmm = ballot(pmove), pem = ballot(pev);
-            const int nmv = popc(pmm), nev = popc(pem);
+            if (useS) ok = cand && ((s_size - crk >= s_cap && s_unp - crk > 0) || (m_unp + mb == 0)) && eb < rem;
+            else ok = cand && eb < rem && (m_unp - eb) > 0;
+            const BMask okm = bballot1(ok);
+            const BMask bad = candm.andnot(okm);
+            const int stop = bad.first();   // kB if none
+            const bool proc = cand && tid < stop;
+            const BMask pmm = mvm.below(stop), pem = evm.below(stop);
+            const int nmv = pmm.count(), nev = pem.count();
             // live entries of this queue that stay behind the scan point
-            const uint64_t km = ballot(inQ && !proc && lane < stop) | (bad ? (1ull << stop) : 0ull);
-            if (km) {
-                const uint32_t kp = sp + (uint32_t)first_lane(km);
+            const BMask kept = inQm.andnot(candm).below(stop);
+            const int kf = stop < kB ? (kept.any() ? (kept.first() < stop ? kept.first() : stop) : stop)
+                                     : (kept.any() ? kept.first() : -1);
+            if (kf >= 0) {
+                const uint32_t kp = sp + (uint32_t)kf;
                 if (useS) { if (kp < keptS) keptS = kp; } else { if (kp < keptM) keptM = kp; }
             }
-            wsync();
             // moves / reinsertions: append to the log tail in queue order
-            if (pmove) {
-                const uint32_t np = tail + (uint32_t)mbcnt(pmm);
+            if (proc && mv) {
+                const uint32_t np = tail + (uint32_t)pmm.rank(wid);
                 log[np & lmask] = (uint16_t)sl;
                 stamp[sl] = np;
                 uint32_t m2 = mt & ~(3u << kFreqShift);
@@ -682,8 +832,10 @@ struct Replayer {
                 meta[sl] = m2;
             }
             tail += (uint32_t)nmv;
+            const bool pev = proc && !mv;
+            const int erk = pem.rank(wid);
             if (useS) {
-                ghost_insert(pev, key[sl]);
+                ghost_insert(pev, pev ? key[sl] : 0ull, erk, nev);
                 s_size -= nmv + nev;
                 s_unp -= nmv + nev;
                 m_unp += nmv;
@@ -692,12 +844,13 @@ struct Replayer {
                 m_unp -= nev;
                 s3_reins += (uint64_t)nmv;
             }
-            evict_lanes(pev, sl);
+            if (pev) evict_elem(sl, erk);
+            evicted(nev);
             rem -= nev;
-            const uint32_t adv = stop < 64 ? (uint32_t)stop : ((lim - sp) < 64 ? (lim - sp) : 64u);
+            const uint32_t adv = stop < kB ? (uint32_t)stop : ((lim - sp) < (uint32_t)kB ? (lim - sp) : (uint32_t)kB);
             if (adv == 0) err = kErrInternal;   // a scan that cannot advance is a bug, never a hang
             if (useS) spS = sp + adv; else spM = sp + adv;
-            wsync();
+            bsync();
         }
         curS = keptS < spS ? keptS : spS;
         curM = keptM < spM ? keptM : spM;
@@ -708,21 +861,20 @@ struct Replayer {
     // ============================================================ one request
     DEV Req load_req(int64_t r) const {
         Req q;
-        q.g = T.group[r];
-        q.c = T.contract[r];
-        q.p = T.prefix[r];
-        q.t = T.tick ? T.tick[r] : r;
-        q.ko = T.key_off[r];
-        q.nfull = T.key_off[r + 1] - q.ko;
+        q.g = tgroup[r];
+        q.c = tcontract[r];
+        q.p = tprefix[r];
+        q.t = T.tick ? ttick[r] : r;
+        q.ko = tkoff[r];
+        q.nfull = tkoff[r + 1] - q.ko;
         return q;
     }
 
-    // `kn` holds keys[ko + lane] of this request and bref/badm its prefix
+    // `kn` holds keys[ko + tid] of this request and bref/badm its prefix
     // bitmap words (all prefetched); on return they hold the same for `nx`.
     DEV bool request(int64_t r, const Req &q, int64_t &tprev, uint64_t &kn, uint32_t &bref, uint32_t &badm,
                      const Req &nx, bool has_next) {
         PROF_T(p0);
-        const int lane = lane_id();
         const int g = q.g, c = q.c;
         const uint32_t p = q.p;
         const int64_t t = q.t, ko = q.ko, nfull = q.nfull;
@@ -733,10 +885,13 @@ struct Replayer {
         const int n = (int)(nfull < C ? nfull : C);
         const bool me = lane == g;
 
-        // ---- OnRequest (Alg. 1): prior reference of (g,p), then record it
+        // ---- OnRequest (Alg. 1): prior reference of (g,p), then record it.
+        // Thread 0 owns the prefix bitmaps and publishes this request's two
+        // bits through LDS (X.qf, written before the last barrier).
         const uint32_t w = p >> 5, bit = 1u << (p & 31);
-        const bool q1 = (bref & bit) != 0, adm = (badm & bit) != 0;
-        if (lane == 0 && !q1) bits[w] = bref | bit;
+        const uint32_t qf = rfl(X.qf);
+        const bool q1 = (qf & 1u) != 0, adm = (qf & 2u) != 0;
+        if (tid == 0 && !q1) bits[w] = bref | bit;
         if (me) { c_req += 1; c_probe += (uint64_t)n; c_trunc += (uint64_t)(nfull - n); }
         const bool proven = q1 && adm;
         int64_t dg = 0;
@@ -746,21 +901,22 @@ struct Replayer {
         // ---- lookup, duplicates, pin + OnTouch, orphans (new blocks wait)
         PROF_T(p1);
         PROF_ADD(0, p0, p1);
-        for (uint32_t i = lane; i <= rsmask; i += 64) rset[i] = kEmpty;
-        wsync();
         int hend = n, nhit = 0, nnew = 0, ndup = 0, norph = 0;
         int npromo = 0, ngated = 0;
         uint64_t kcur = kn;
-        for (int base = 0; base < n; base += 64) {
-            const int j = base + lane;
+        for (int base = 0; base < n; base += kB) {
+            const int j = base + tid;
             const bool act = j < n;
             const uint64_t k = kcur;
-            if (base + 64 < n) kcur = (j + 64 < n) ? T.keys[ko + j + 64] : 0ull;   // next chunk in flight
+            if (base + kB < n) kcur = (j + kB < n) ? tkeys[ko + j + kB] : 0ull;   // next step in flight
             const TH h = thash(k, nbmask, rsmask);
             const uint32_t mine = (h.tag << 16) | (uint32_t)j;
             uint32_t rpos = 0;
+            if (act) rkeys[j] = k;
+            // the key must be in LDS before the set entry that names it
+            if constexpr (kLds) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+            else __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
             if (act) {   // first occurrence in the request keeps the smallest position
-                rkeys[j] = k;
                 uint32_t idx = h.rhome;
                 for (;;) {
                     const uint32_t old = atomicCAS(&rset[idx], kEmpty, mine);
@@ -773,26 +929,39 @@ struct Replayer {
                     idx = (idx + 1) & rsmask;
                 }
             }
-            wsync();
+            // resident lookup of every key (also of duplicates: harmless)
+            uint32_t cand = 0;
+            const int ntag = act ? tprobe(h, cand) : 0;
+            bsync();
             const bool dup = act && rset[rpos] != mine;
             const bool nd = act && !dup;
-            const int fs = nd ? tfind(k, h) : -1;
-            const bool found = fs >= 0;
-            const uint64_t missm = ballot(nd && !found);
-            if (hend == n && missm) hend = base + first_lane(missm);
-            const bool isHit = found && j < hend;
-            const bool isOrph = found && j >= hend;
-            const uint32_t slot = (uint32_t)fs;
-            const uint32_t mt = found ? meta[slot] : 0u;
-            // Eq. 4: proven reuse of a block matching (g, c, p), not yet REUSE
-            bool elig = false;
-            if (policy == kPS && isHit && proven && (int)owner_of(mt) == g && (int)contract_of(mt) == c &&
-                cls_of(mt) != (uint32_t)kReuse)
-                elig = pfx[slot] == p;
-            if (policy == kPS) {
-                const int ne = popc(ballot(elig));
-                if (gate_open) npromo += ne; else ngated += ne;
+            // key, metadata and prefix id of the candidate in one round trip
+            const uint64_t ck = ntag == 1 ? key[cand] : 0ull;
+            uint32_t mt = ntag == 1 ? meta[cand] : 0u;
+            const uint32_t cp = (policy == kPS && ntag == 1) ? pfx[cand] : 0u;
+            int fs = (ntag == 1 && ck == k) ? (int)cand : -1;
+            if (ntag > 1) {
+                fs = tfind_slow(k, h);
+                if (fs >= 0) mt = meta[fs];
             }
+            const bool found = nd && fs >= 0;
+            const uint32_t slot = (uint32_t)fs;
+            uint32_t cpx = cp;
+            if (policy == kPS && ntag > 1 && fs >= 0) cpx = pfx[slot];
+            // Eq. 4: proven reuse of a block matching (g, c, p), not yet REUSE
+            const bool eligc = policy == kPS && found && proven && (int)owner_of(mt) == g &&
+                               (int)contract_of(mt) == c && cls_of(mt) != (uint32_t)kReuse && cpx == p;
+            const bool inS = found && !(mt & kQMain);
+            bool pa[5] = {nd && !found, found, dup, eligc, inS};
+            BMask ma[5];
+            bballot<5>(pa, ma);
+            // a one-step request leaves the set empty entry by entry
+            if (n <= kB && act) rset[rpos] = kEmpty;
+            if (hend == n && ma[0].any()) hend = base + ma[0].first();
+            const int lim = hend - base;   // threads below lim are in the leading run
+            const bool isHit = found && tid < lim;
+            const bool isOrph = found && tid >= lim;
+            const bool elig = eligc && tid < lim;
             if (isHit) {   // pin; touch
                 uint32_t m2 = mt | kPin;
                 if (policy == kS3) {
@@ -807,14 +976,6 @@ struct Replayer {
                 }
                 meta[slot] = m2;
             }
-            if (policy == kS3) {
-                const bool inM = (mt & kQMain) != 0;
-                const int hs = popc(ballot(isHit && !inM)), hm = popc(ballot(isHit && inM));
-                const int os = popc(ballot(isOrph && !inM)), om = popc(ballot(isOrph && inM));
-                s_unp -= hs + os;
-                m_unp -= hm + om;
-                s_size -= os;
-            }
             // orphans: the old block leaves; its slot and table entry are
             // reused by the new block of the same key
             if (isOrph) {
@@ -824,22 +985,34 @@ struct Replayer {
                 meta[slot] = kPin;
             }
             if (act) posslot[j] = dup ? kNoSlot : (found ? (uint16_t)slot : kNewMark);
-            const int no = popc(ballot(isOrph));
+            const BMask hitm = ma[1].below(lim);
+            const int nh = hitm.count(), nf = ma[1].count(), no = nf - nh;
+            const int ne = ma[3].below(lim).count();
+            const int hs = ma[4].below(lim).count(), os = ma[4].count() - hs;
+            nhit += nh;
             norph += no;
+            nnew += (nf - nh) + ma[0].count();
+            ndup += ma[2].count();
+            if (gate_open) npromo += ne; else ngated += ne;
             resident -= no;
-            nhit += popc(ballot(isHit));
-            nnew += popc(ballot(nd && !isHit));
-            ndup += popc(ballot(dup));
-            wsync();
+            if (policy == kS3) {
+                s_unp -= hs + os;
+                m_unp -= (nh - hs) + (no - os);
+                s_size -= os;
+            }
         }
-        // the next request's first 64 keys and prefix bits go in flight now
+        if (n > kB)   // longer requests clear the whole set (read by all steps)
+            for (uint32_t i = tid; i <= rsmask; i += kB) rset[i] = kEmpty;
+        // the next request's first keys and prefix bits go in flight now
         uint64_t knext = 0;
         uint32_t nref = 0, nadm = 0;
         if (has_next) {
-            knext = (lane < nx.nfull) ? T.keys[nx.ko + lane] : 0ull;
-            const uint32_t nwd = nx.p >> 5;
-            nref = bits[nwd];
-            nadm = bits[I.n_prefix_words + nwd];
+            knext = (tid < nx.nfull) ? tkeys[nx.ko + tid] : 0ull;
+            if (tid == 0) {
+                const uint32_t nwd = nx.p >> 5;
+                nref = bits[nwd];
+                nadm = bits[I.n_prefix_words + nwd];
+            }
         }
         const int h = nhit, m = nnew;
         if (me) {
@@ -883,107 +1056,99 @@ struct Replayer {
                 c_charged += (uint64_t)m;
             }
             cls_new = bcast32(cl, g);
-            if (lane == 0 && !adm) bits[I.n_prefix_words + w] = badm | bit;
+            if (tid == 0 && !adm) bits[I.n_prefix_words + w] = badm | bit;
             adm_now = true;
         }
 
-        // ---- insert the new blocks: never-used slots first, then the
-        //      victims' slots; queue order is deepest first
+        // ---- insert the new blocks (never-used slots first, then the
+        //      victims' slots) and release every block of the request to the
+        //      free queue, deepest first -- one pass over the positions
         PROF_T(p4);
         PROF_ADD(3, p3, p4);
-        if (policy == kS3 && m > 0) ensure_room((uint32_t)m);
-        const uint32_t mbase = ((uint32_t)g) | ((uint32_t)c << kContractShift) | (cls_new << kClsShift) | kRes | kPin;
+        const int nrel = n - ndup;
+        if (policy == kS3) { if (m > 0) ensure_room((uint32_t)m); }
+        else if (nrel > 0) ensure_room((uint32_t)nrel);
+        const uint32_t mbase = ((uint32_t)g) | ((uint32_t)c << kContractShift) | (cls_new << kClsShift) | kRes;
         const int nfresh = C - hwm;
-        int before = 0, nalloc = 0;
-        int n_ins_S = 0, n_ins_M = 0;
-        for (int base = hend; base < n; base += 64) {
-            const int j = base + lane;
+        int nalloc = 0, seen = 0, seen_new = 0;
+        if (tid == 0) X.nghost = 0;
+        for (int base = 0; base < n; base += kB) {
+            const int j = base + tid;
             const bool act = j < n;
             uint32_t slot = act ? posslot[j] : kNoSlot;
-            const bool isN = slot == kNewMark;
-            const uint64_t am = ballot(isN);
+            const bool rl = act && slot != kNoSlot;       // every non-duplicate position
+            const bool isNew = rl && j >= hend;           // new block (orphans included)
+            const bool isN = slot == kNewMark;            // new block without a slot yet
+            uint32_t mt = (rl && !isNew) ? meta[slot] : 0u;
+            bool pa[4] = {isN, rl, isNew, rl && !isNew && (mt & kQMain) != 0};
+            BMask ma[4];
+            bballot<4>(pa, ma);
             uint64_t kk = 0;
             if (isN) {
-                const int i = nalloc + mbcnt(am);
+                const int i = nalloc + ma[0].rank(wid);
                 slot = i < nfresh ? (uint32_t)(hwm + i) : vlist[i - nfresh];
                 kk = rkeys[j];
                 key[slot] = kk;
-                posslot[j] = (uint16_t)slot;
+                const TH hh = thash(kk, nbmask, rsmask);
+                const uint32_t val = (hh.tag << 16) | slot;
+                if (!tinsert(table, val, hh)) defer_kick(val, kk, true);
             }
-            nalloc += popc(am);
-            const bool nw = act && slot != kNoSlot;
-            const uint64_t nm = ballot(nw);
-            if (nw) {
-                meta[slot] = mbase;
+            nalloc += ma[0].count();
+            if (isNew) {
+                mt = mbase;
                 if (policy == kPS) pfx[slot] = p;
             }
-            bool ok = true;
-            uint32_t val = 0;
-            if (isN) {
-                const TH hh = thash(kk, nbmask, rsmask);
-                val = (hh.tag << 16) | slot;
-                ok = tinsert(table, val, hh);
-            }
-            const uint64_t over = ballot(isN && !ok);
-            if (over) kick_lanes<true>(over, val, kk);
             if (policy == kS3) {
+                // new blocks enter the ghost-selected queue in deepest-first
+                // order; hits stay where they are; everything is unpinned
                 bool gh = false;
-                if (nw && g_cap > 0) gh = ghost_take(isN ? kk : key[slot]);
-                const uint32_t rank = (uint32_t)(m - 1 - (before + mbcnt(nm)));
-                if (nw) {
-                    const uint32_t np = tail + rank;
+                if (isNew && g_cap > 0) gh = ghost_take(isN ? kk : key[slot]);
+                if (gh) atomicAdd(&X.nghost, 1u);
+                if (isNew) {
+                    const uint32_t np = tail + (uint32_t)(m - 1 - (seen_new + ma[2].rank(wid)));
                     log[np & lmask] = (uint16_t)slot;
                     stamp[slot] = np;
-                    meta[slot] = mbase | kInLog | (gh ? kQMain : 0u);
+                    meta[slot] = mt | kInLog | (gh ? kQMain : 0u);
+                } else if (rl) {
+                    meta[slot] = mt & ~kPin;
                 }
-                const int ng = popc(ballot(nw && gh));
-                n_ins_M += ng;
-                n_ins_S += popc(nm) - ng;
-            }
-            before += popc(nm);
-            wsync();
-        }
-        hwm += nalloc < nfresh ? nalloc : nfresh;
-        if (m > 0) {
-            if (lane == 0) atomicAdd(&res[g], (uint32_t)m);
-            resident += m;
-            if (policy == kS3) {
-                tail += (uint32_t)m;
-                s_size += n_ins_S;
-                s3_ghits += (uint64_t)n_ins_M;
-            }
-        }
-        wsync();
-
-        // ---- release: back to the free queue, deepest first
-        PROF_T(p5);
-        PROF_ADD(4, p4, p5);
-        const int nrel = n - ndup;
-        if (policy != kS3 && nrel > 0) ensure_room((uint32_t)nrel);
-        int seen = 0;
-        for (int base = 0; base < n; base += 64) {
-            const int j = base + lane;
-            const bool act = j < n;
-            const uint32_t slot = act ? posslot[j] : kNoSlot;
-            const bool rl = act && slot != kNoSlot;
-            const uint64_t rm = ballot(rl);
-            const uint32_t mt = rl ? meta[slot] : 0u;
-            if (policy == kS3) {
-                const bool inM = (mt & kQMain) != 0;
-                if (rl) meta[slot] = mt & ~kPin;
-                s_unp += popc(ballot(rl && !inM));
-                m_unp += popc(ballot(rl && inM));
+                const int hm = ma[3].count();
+                s_unp += ma[1].count() - ma[2].count() - hm;   // hits in the small queue
+                m_unp += hm;
             } else if (rl) {
-                const uint32_t np = tail + (uint32_t)(nrel - 1 - (seen + mbcnt(rm)));
+                const uint32_t np = tail + (uint32_t)(nrel - 1 - (seen + ma[1].rank(wid)));
                 log[np & lmask] = (uint16_t)slot;
                 stamp[slot] = np;
                 meta[slot] = (mt & ~kPin) | kInLog | kRes;
                 if (policy == kPS) atomicAdd(&cnt[3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt))], 1u);
             }
-            seen += popc(rm);
+            seen += ma[1].count();
+            seen_new += ma[2].count();
+            if (base + kB < n) {   // another step follows: place displaced entries first
+                bsync();
+                kick_pending();
+            }
         }
-        if (policy != kS3) tail += (uint32_t)nrel;
-        wsync();
+        if (policy == kS3) gsync();   // ghost-ring writes of this request are visible
+        else bsync();
+        kick_pending();
+        hwm += nalloc < nfresh ? nalloc : nfresh;
+        if (m > 0) {
+            if (tid == 0) atomicAdd(&res[g], (uint32_t)m);
+            resident += m;
+        }
+        // (one unconditional update of the log tail keeps every member of
+        // the uniform state in registers)
+        tail += (uint32_t)(policy == kS3 ? m : nrel);
+        if (policy == kS3) {
+            const int ng = (int)rfl(X.nghost);
+            s_size += m - ng;
+            s3_ghits += (uint64_t)ng;
+            s_unp += m - ng;   // new blocks are unpinned right away
+            m_unp += ng;
+        }
+        PROF_T(p5);
+        PROF_ADD(4, p4, p5);
 
         // ---- accounting for every group
         PROF_T(p6);
@@ -1005,6 +1170,11 @@ struct Replayer {
         kn = knext;
         bref = nref;
         badm = nadm;
+        if (tid == 0 && has_next) {
+            const uint32_t nb = 1u << (nx.p & 31);
+            X.qf = ((nref & nb) ? 1u : 0u) | ((nadm & nb) ? 2u : 0u);
+        }
+        bsync();   // X.qf and all state of this request are visible
         PROF_T(p7);
         PROF_ADD(6, p6, p7);
         return true;
@@ -1012,26 +1182,25 @@ struct Replayer {
 
     // ============================================================ run
     DEV void init() {
-        const int lane = lane_id();
         const uint32_t nte = 8u * (nbmask + 1u);
-        for (uint32_t i = lane; i < nte; i += 64) table[i] = kEmpty;
-        for (int i = lane; i < C; i += 64) meta[i] = 0;
-        for (int i = lane; i < 64; i += 64) { evown[i] = 0ull; res[i] = 0u; }
+        for (uint32_t i = tid; i < nte; i += kB) table[i] = kEmpty;
+        for (int i = tid; i < C; i += kB) meta[i] = 0;
+        for (int i = tid; i < 64; i += kB) { evown[i] = 0ull; res[i] = 0u; }
         if (policy == kPS)
-            for (int i = lane; i < 196; i += 64) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
-        for (int i = lane; i < 2 * I.n_prefix_words; i += 64) bits[i] = 0u;
+            for (int i = tid; i < 196; i += kB) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
+        for (int i = tid; i < 2 * I.n_prefix_words; i += kB) bits[i] = 0u;
         if (policy == kS3 && g_cap > 0) {
             const uint32_t nge = 8u * (gnbmask + 1u);
-            for (uint32_t i = lane; i < nge; i += 64) gtable[i] = kEmpty;
+            for (uint32_t i = tid; i < nge; i += kB) gtable[i] = kEmpty;
         }
+        if (tid == 0) { X.novf = 0; X.nghost = 0; X.kerr = 0; X.qf = 0; }
+        for (uint32_t i = tid; i <= rsmask; i += kB) rset[i] = kEmpty;
         head = tail = 0;
         hwm = 0;
         nvict = 0;
         resident = 0;
         s_size = s_unp = m_unp = 0;
         gseq = curS = curM = 0;
-        gpre = 0;
-        gpre_base = 0xFFFFFFFFu;
         rmax = 0;
         err = 0;
         ev_total = in_vgpr((uint64_t)0);
@@ -1048,12 +1217,11 @@ struct Replayer {
 #ifdef PC_PROFILE
         for (int i = 0; i < 8; ++i) prof[i] = 0;
 #endif
-        wsync();
+        gsync();
     }
 
     DEV void run(int64_t *st, int32_t *per_req) {
         init();
-        const int lane = lane_id();
         int32_t status = 0;
         int64_t tprev = 0, tlast = 0;
         const int64_t nreq = T.n_req;
@@ -1062,12 +1230,15 @@ struct Replayer {
         uint32_t bref = 0, badm = 0;
         if (nreq > 0) {
             q = load_req(0);
-            kn = (q.nfull > lane && q.ko >= 0 && q.ko + q.nfull <= T.n_keys) ? T.keys[q.ko + lane] : 0ull;
-            if ((int64_t)q.p < T.n_prefix) {
+            kn = (q.nfull > tid && q.ko >= 0 && q.ko + q.nfull <= T.n_keys) ? tkeys[q.ko + tid] : 0ull;
+            if ((int64_t)q.p < T.n_prefix && tid == 0) {
                 bref = bits[q.p >> 5];
                 badm = bits[I.n_prefix_words + (q.p >> 5)];
+                const uint32_t nb = 1u << (q.p & 31);
+                X.qf = ((bref & nb) ? 1u : 0u) | ((badm & nb) ? 2u : 0u);
             }
         }
+        bsync();
         for (int64_t r = 0; r < nreq; ++r) {
             const bool has_next = r + 1 < nreq;
             Req nx = {};
@@ -1078,13 +1249,14 @@ struct Replayer {
             if (!request(r, q, tprev, kn, bref, badm, nx, nx_ok)) { status = -1; break; }
             if (err) { status = err; break; }
             tlast = tprev;
-            if (per_req && I.per_req_off >= 0 && lane == 0) {
+            if (per_req && I.per_req_off >= 0 && tid == 0) {
                 int32_t *o = per_req + I.per_req_off + 4 * r;
                 o[0] = last_h; o[1] = last_m; o[2] = last_e; o[3] = last_o;
             }
             q = nx;
         }
-        wsync();
+        gsync();
+        if (wid != 0) return;
         // stats record: 64 groups x 17 int64, then the instance block
         const bool ok = status == 0;
         const bool grp = lane < G;
@@ -1116,22 +1288,25 @@ struct Replayer {
 };
 
 template <bool kLds>
-__global__ __launch_bounds__(64) void replay_kernel(const DevInst *__restrict__ insts,
+__global__ __launch_bounds__(kB) void replay_kernel(const DevInst *__restrict__ insts,
                                                     const DevTrace *__restrict__ traces,
                                                     const int32_t *__restrict__ order, uint8_t *ws,
                                                     int64_t *stats, int32_t *per_req) {
     extern __shared__ __align__(16) uint8_t smem[];
+    __shared__ Coll coll;
     const int id = order[blockIdx.x];
     const DevInst &I = insts[id];
     const DevTrace &T = traces[I.trace];
     uint8_t *sbase;
     if constexpr (kLds) sbase = smem;
     else sbase = ws + I.ws_state;
-    Replayer<kLds> rp(I, T, sbase, ws);
+    Replayer<kLds> rp(coll, I, T, sbase, ws);
     rp.run(stats + (int64_t)id * kRecordWords, per_req);
 }
 
 }  // namespace
+
+int32_t replay_static_lds_bytes() { return (int32_t)sizeof(Coll); }
 
 hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order, int32_t n_launch,
                          int32_t lds_bytes, bool in_lds, uint8_t *ws, int64_t *stats, int32_t *per_req,
@@ -1141,10 +1316,10 @@ hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const 
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel<true>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(replay_kernel<true>, dim3((unsigned)n_launch), dim3(64), (size_t)lds_bytes, s, d_inst,
+        hipLaunchKernelGGL(replay_kernel<true>, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s, d_inst,
                            d_traces, d_order, ws, stats, per_req);
     } else {
-        hipLaunchKernelGGL(replay_kernel<false>, dim3((unsigned)n_launch), dim3(64), 0, s, d_inst, d_traces,
+        hipLaunchKernelGGL(replay_kernel<false>, dim3((unsigned)n_launch), dim3(kB), 0, s, d_inst, d_traces,
                            d_order, ws, stats, per_req);
     }
     return hipGetLastError();

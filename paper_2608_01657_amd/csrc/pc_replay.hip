@@ -194,6 +194,10 @@ struct Coll {
     uint64_t kkey[kB];                // displacement scratch: keys
     uint32_t kval[kB];                // displacement scratch: entries
     uint32_t kmain[kB];               // 1 = main table, 0 = ghost table
+#ifdef PC_PROFILE
+    uint64_t prof[16];                // cycle counters (thread 0)
+    uint64_t prof_last;
+#endif
 };
 
 // Key -> two buckets, 16-bit tag (never 0xFFFF, so empty entries never match
@@ -229,19 +233,28 @@ DEV uint32_t freq_of(uint32_t mt) { return (mt >> kFreqShift) & 3u; }
 
 // Optional per-phase cycle accounting (build with -DPC_PROFILE); the totals
 // land in the stats slot of group 63.  Nothing is skipped either way.
+// PROF_MARK(i) adds the cycles since the previous mark to counter i.
 #ifdef PC_PROFILE
-#define PROF_T(var) const uint64_t var = __builtin_amdgcn_s_memtime()
-#define PROF_ADD(i, a, b) prof[i] += (b) - (a)
+#define PROF_MARK(i)                                              \
+    do {                                                          \
+        const uint64_t prof_now = __builtin_amdgcn_s_memtime();   \
+        if (tid == 0) {                                           \
+            X.prof[i] += prof_now - X.prof_last;                  \
+            X.prof_last = prof_now;                               \
+        }                                                         \
+    } while (0)
 #else
-#define PROF_T(var)
-#define PROF_ADD(i, a, b)
+#define PROF_MARK(i) do { } while (0)
 #endif
 
 // Descriptor of one request (loaded one request ahead).
+// Fields are kept as loaded (no arithmetic on them until the request runs,
+// so that issuing the loads never waits for them).
 struct Req {
-    int32_t g, c;
+    uint8_t g, c;
     uint32_t p;
-    int64_t t, ko, nfull;
+    int64_t t, ko, kend;
+    DEV int64_t nfull() const { return kend - ko; }
 };
 
 template <bool kLds>
@@ -268,6 +281,10 @@ struct Replayer {
     const GLOBAL int64_t *tkoff, *ttick;
     const GLOBAL uint8_t *tgroup, *tcontract;
     const GLOBAL uint32_t *tprefix;
+    int64_t n_req, n_keys, n_prefix;   // trace sizes, read once
+    int64_t max_rb;
+    int32_t npw;              // prefix bitmap words
+    bool has_tick;
     // ---------------- uniform state (identical in every wavefront)
     uint32_t head, tail;      // live log window [head, tail)
     int32_t hwm;              // slots [hwm, C) have never been used
@@ -275,6 +292,8 @@ struct Replayer {
     int32_t resident;         // resident blocks (excludes blocks being created)
     int32_t s_size, s_unp, m_unp;
     uint32_t gseq, curS, curM;
+    uint32_t gseq0;           // gseq when this request's reclamation began
+    uint64_t gx;              // prefetched expiring ghost key (per thread)
     int32_t rmax;
     int32_t err;
     // ---------------- statistics and group state (lane x = group x, VGPRs)
@@ -284,9 +303,8 @@ struct Replayer {
     int64_t d_max, d_sum;
     int32_t r_max;
     int last_h, last_m, last_e, last_o;
-#ifdef PC_PROFILE
-    uint64_t prof[8];
-#endif
+    int32_t *preq;            // per-request quadruples of this instance, or null
+    int64_t pr_next;          // first request whose quadruple is not written yet
 
     DEV Replayer(Coll &coll, const DevInst &inst, const DevTrace &tr, uint8_t *sbase, uint8_t *ws)
         : X(coll), tid((int)threadIdx.x), wid((int)rfl(threadIdx.x >> 6)), lane((int)__lane_id()), cb(0),
@@ -330,6 +348,12 @@ struct Replayer {
         evown = reinterpret_cast<unsigned long long *>(sbase + I.o_evown);
         bits = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_bits));
         gring = gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_gring));
+        n_req = T.n_req;
+        n_keys = T.n_keys;
+        n_prefix = T.n_prefix;
+        max_rb = T.max_req_blocks;
+        has_tick = T.tick != nullptr;
+        npw = I.n_prefix_words;
         tkeys = gptr(T.keys);
         tkoff = gptr(T.key_off);
         ttick = gptr(T.tick);
@@ -588,12 +612,15 @@ struct Replayer {
             const bool valid = pos < tail;
             const uint32_t s = valid ? log[pos & lmask] : 0;
             const bool live = valid && (meta[s] & kInLog) && stamp[s] == pos;
+            PROF_MARK(5);
             const BMask lm = bballot1(live);
+            PROF_MARK(14);
             const int rk = lm.rank(wid);
             const int tot = lm.count();
             const int nv = tot < rem ? tot : rem;
             if (live && rk < rem) evict_elem(s, rk);
             evicted(nv);
+            PROF_MARK(15);
             if (nv == rem) head = head + (uint32_t)lm.nth(rem - 1) + 1;
             else head = (head + kB < tail) ? head + kB : tail;
             rem -= nv;
@@ -732,22 +759,38 @@ struct Replayer {
     // count).  The ghost keeps the last g_cap insertions: entries older than
     // the batch that leave the window are removed, and batch entries that
     // would already have left it by the batch's end are never inserted.
+    //
+    // The keys that leave the window are read ahead: ghost_prefetch() (start
+    // of a request's reclamation) gives thread i the key of ring sequence
+    // gseq - g_cap + i.  A batch whose expiring entries all predate the
+    // request and fall in that window uses them; any other batch reads the
+    // ring after a full barrier.
+    DEV void ghost_prefetch() {
+        gseq0 = gseq;
+        const int64_t x = (int64_t)gseq - g_cap + tid;
+        gx = (g_cap > 0 && x >= 0) ? gring[(uint32_t)x & grmask] : 0ull;
+    }
+    DEV void ghost_expire(uint64_t kx, uint32_t x) {
+        const uint32_t xp = x & grmask;
+        const TH hx = thash(kx, gnbmask, rsmask);
+        tclear_exact(gtable, (hx.tag << 16) | xp, hx);
+    }
     DEV void ghost_insert(bool v, uint64_t k, int rk, int nv) {
         s3_gins += (uint64_t)nv;
         if (g_cap > 0 && nv > 0) {
-            gsync();   // ring writes of earlier steps are visible
+            const uint32_t off = gseq - gseq0;   // ring writes of this request so far
+            const int64_t xlo = (int64_t)gseq - g_cap;   // first expiring sequence
+            if (off + (uint32_t)nv <= (uint32_t)kB && (int64_t)off + nv <= (int64_t)g_cap) {
+                const int i = tid - (int)off;
+                if (i >= 0 && i < nv && xlo + i >= 0) ghost_expire(gx, (uint32_t)(xlo + i));
+            } else {
+                if (off > 0) gsync();   // this request's ring writes are complete
+                const int64_t x = xlo + tid;
+                if (tid < nv && tid < g_cap && x >= 0) ghost_expire(gring[(uint32_t)x & grmask], (uint32_t)x);
+            }
+            bsync();   // expiries read the ring before it is rewritten
             const uint32_t seq = gseq + (uint32_t)rk;
             const uint32_t gend = gseq + (uint32_t)nv;
-            if (v && (int64_t)seq >= (int64_t)g_cap) {
-                const uint32_t x = seq - (uint32_t)g_cap;
-                if (x < gseq) {
-                    const uint32_t xp = x & grmask;
-                    const uint64_t kx = gring[xp];
-                    const TH hx = thash(kx, gnbmask, rsmask);
-                    tclear_exact(gtable, (hx.tag << 16) | xp, hx);
-                }
-            }
-            bsync();
             const bool ins = v && (int64_t)seq + g_cap >= (int64_t)gend;
             if (v) gring[seq & grmask] = k;
             if (ins) {
@@ -755,23 +798,34 @@ struct Replayer {
                 const uint32_t val = (h.tag << 16) | (seq & grmask);
                 if (!tinsert(gtable, val, h)) defer_kick(val, k, false);
             }
-            gsync();
-            kick_pending();
+            bsync();
+            if (rfl(X.novf)) {   // displacement reads ring keys written just now
+                gsync();
+                kick_pending();
+            }
         }
         gseq += (uint32_t)nv;
     }
-    // ghost hit for key k: remove it and report true
+    // ghost hit for key k: remove it and report true.  Entries written by
+    // this request's own reclamation hold its victims' keys, never the key
+    // of one of its new blocks, and are skipped without reading the ring.
     DEV bool ghost_take(uint64_t k) {
         const TH h = thash(k, gnbmask, rsmask);
         uint32_t e[16];
         load_buckets(gtable, h, e);
+        const uint32_t nown = gseq - gseq0;
         int at = -1;
-        for (int i = 0; i < 16; ++i)
-            if (at < 0 && (e[i] >> 16) == h.tag && gring[e[i] & grmask] == k) at = i;
+        for (int i = 0; i < 16; ++i) {
+            const uint32_t pos = e[i] & 0xFFFFu;
+            if (at < 0 && (e[i] >> 16) == h.tag && ((gseq - 1u - pos) & grmask) >= nown &&
+                gring[pos & grmask] == k)
+                at = i;
+        }
         if (at >= 0) gtable[epos(h, at)] = kEmpty;
         return at >= 0;
     }
     DEV void evict_s3(int e) {
+        ghost_prefetch();
         int rem = e;
         uint32_t spS = curS, spM = curM;
         uint32_t keptS = 0xFFFFFFFFu, keptM = 0xFFFFFFFFu;
@@ -859,27 +913,33 @@ struct Replayer {
     }
 
     // ============================================================ one request
+    DEV void put_per_request(int64_t i) {
+        int32_t *o = preq + 4 * i;
+        o[0] = last_h; o[1] = last_m; o[2] = last_e; o[3] = last_o;
+        pr_next = i + 1;
+    }
     DEV Req load_req(int64_t r) const {
         Req q;
         q.g = tgroup[r];
         q.c = tcontract[r];
         q.p = tprefix[r];
-        q.t = T.tick ? ttick[r] : r;
+        q.t = has_tick ? ttick[r] : r;
         q.ko = tkoff[r];
-        q.nfull = tkoff[r + 1] - q.ko;
+        q.kend = tkoff[r + 1];
         return q;
     }
 
     // `kn` holds keys[ko + tid] of this request and bref/badm its prefix
     // bitmap words (all prefetched); on return they hold the same for `nx`.
+    // `nn` receives the descriptor of request r + 2 (loaded here, used two
+    // requests later, so that no descriptor load is waited for).
     DEV bool request(int64_t r, const Req &q, int64_t &tprev, uint64_t &kn, uint32_t &bref, uint32_t &badm,
-                     const Req &nx, bool has_next) {
-        PROF_T(p0);
+                     const Req &nx, bool has_next, Req &nn) {
         const int g = q.g, c = q.c;
         const uint32_t p = q.p;
-        const int64_t t = q.t, ko = q.ko, nfull = q.nfull;
-        if (g >= G || c >= K || (int64_t)p >= T.n_prefix || ko < 0 || nfull < 0 || ko + nfull > T.n_keys ||
-            nfull > T.max_req_blocks || t < 0 || t < tprev)
+        const int64_t t = q.t, ko = q.ko, nfull = q.nfull();
+        if (g >= G || c >= K || (int64_t)p >= n_prefix || ko < 0 || nfull < 0 || ko + nfull > n_keys ||
+            nfull > max_rb || t < 0 || t < tprev)
             return false;
         tprev = t;
         const int n = (int)(nfull < C ? nfull : C);
@@ -891,7 +951,6 @@ struct Replayer {
         const uint32_t w = p >> 5, bit = 1u << (p & 31);
         const uint32_t qf = rfl(X.qf);
         const bool q1 = (qf & 1u) != 0, adm = (qf & 2u) != 0;
-        if (tid == 0 && !q1) bits[w] = bref | bit;
         if (me) { c_req += 1; c_probe += (uint64_t)n; c_trunc += (uint64_t)(nfull - n); }
         const bool proven = q1 && adm;
         int64_t dg = 0;
@@ -899,8 +958,7 @@ struct Replayer {
         const bool gate_open = dg <= eps || (flags & kFlagNoGate);
 
         // ---- lookup, duplicates, pin + OnTouch, orphans (new blocks wait)
-        PROF_T(p1);
-        PROF_ADD(0, p0, p1);
+        PROF_MARK(0);
         int hend = n, nhit = 0, nnew = 0, ndup = 0, norph = 0;
         int npromo = 0, ngated = 0;
         uint64_t kcur = kn;
@@ -929,10 +987,12 @@ struct Replayer {
                     idx = (idx + 1) & rsmask;
                 }
             }
+            PROF_MARK(1);
             // resident lookup of every key (also of duplicates: harmless)
             uint32_t cand = 0;
             const int ntag = act ? tprobe(h, cand) : 0;
             bsync();
+            PROF_MARK(2);
             const bool dup = act && rset[rpos] != mine;
             const bool nd = act && !dup;
             // key, metadata and prefix id of the candidate in one round trip
@@ -954,7 +1014,9 @@ struct Replayer {
             const bool inS = found && !(mt & kQMain);
             bool pa[5] = {nd && !found, found, dup, eligc, inS};
             BMask ma[5];
+            PROF_MARK(3);
             bballot<5>(pa, ma);
+            PROF_MARK(4);
             // a one-step request leaves the set empty entry by entry
             if (n <= kB && act) rset[rpos] = kEmpty;
             if (hend == n && ma[0].any()) hend = base + ma[0].first();
@@ -1003,16 +1065,23 @@ struct Replayer {
         }
         if (n > kB)   // longer requests clear the whole set (read by all steps)
             for (uint32_t i = tid; i <= rsmask; i += kB) rset[i] = kEmpty;
-        // the next request's first keys and prefix bits go in flight now
+        // the next request's first keys and prefix bits, and the descriptor
+        // after it, go in flight now; stores follow the loads so that waiting
+        // for the loads never waits for a store
         uint64_t knext = 0;
         uint32_t nref = 0, nadm = 0;
         if (has_next) {
-            knext = (tid < nx.nfull) ? tkeys[nx.ko + tid] : 0ull;
+            knext = (tid < nx.nfull()) ? tkeys[nx.ko + tid] : 0ull;
             if (tid == 0) {
                 const uint32_t nwd = nx.p >> 5;
                 nref = bits[nwd];
-                nadm = bits[I.n_prefix_words + nwd];
+                nadm = bits[npw + nwd];
             }
+        }
+        if (r + 2 < n_req) nn = load_req(r + 2);
+        if (tid == 0) {
+            if (!q1) bits[w] = bref | bit;   // OnRequest: (g, p) referenced
+            if (preq && r > 0) put_per_request(r - 1);
         }
         const int h = nhit, m = nnew;
         if (me) {
@@ -1025,9 +1094,9 @@ struct Replayer {
         }
 
         // ---- reclamation (Alg. 2): truly free blocks first
-        PROF_T(p2);
-        PROF_ADD(1, p1, p2);
+        PROF_MARK(5);
         nvict = 0;
+        gseq0 = gseq;
         int e = m - (C - resident);
         if (e < 0) e = 0;
         if (e > 0) {
@@ -1038,8 +1107,7 @@ struct Replayer {
         if (me) c_evc += (uint64_t)e;
 
         // ---- OnCacheFullBlocks: charge n_r = m (Eq. 2), class, admission
-        PROF_T(p3);
-        PROF_ADD(2, p2, p3);
+        PROF_MARK(6);
         uint32_t cls_new = kNormal;
         bool adm_now = adm;
         if (m > 0) {
@@ -1056,18 +1124,18 @@ struct Replayer {
                 c_charged += (uint64_t)m;
             }
             cls_new = bcast32(cl, g);
-            if (tid == 0 && !adm) bits[I.n_prefix_words + w] = badm | bit;
+            if (tid == 0 && !adm) bits[npw + w] = badm | bit;
             adm_now = true;
         }
 
         // ---- insert the new blocks (never-used slots first, then the
         //      victims' slots) and release every block of the request to the
         //      free queue, deepest first -- one pass over the positions
-        PROF_T(p4);
-        PROF_ADD(3, p3, p4);
+        PROF_MARK(7);
         const int nrel = n - ndup;
         if (policy == kS3) { if (m > 0) ensure_room((uint32_t)m); }
         else if (nrel > 0) ensure_room((uint32_t)nrel);
+        PROF_MARK(8);
         const uint32_t mbase = ((uint32_t)g) | ((uint32_t)c << kContractShift) | (cls_new << kClsShift) | kRes;
         const int nfresh = C - hwm;
         int nalloc = 0, seen = 0, seen_new = 0;
@@ -1083,6 +1151,7 @@ struct Replayer {
             bool pa[4] = {isN, rl, isNew, rl && !isNew && (mt & kQMain) != 0};
             BMask ma[4];
             bballot<4>(pa, ma);
+            PROF_MARK(9);
             uint64_t kk = 0;
             if (isN) {
                 const int i = nalloc + ma[0].rank(wid);
@@ -1094,6 +1163,7 @@ struct Replayer {
                 if (!tinsert(table, val, hh)) defer_kick(val, kk, true);
             }
             nalloc += ma[0].count();
+            PROF_MARK(10);
             if (isNew) {
                 mt = mbase;
                 if (policy == kPS) pfx[slot] = p;
@@ -1124,6 +1194,7 @@ struct Replayer {
             }
             seen += ma[1].count();
             seen_new += ma[2].count();
+            PROF_MARK(11);
             if (base + kB < n) {   // another step follows: place displaced entries first
                 bsync();
                 kick_pending();
@@ -1147,12 +1218,9 @@ struct Replayer {
             s_unp += m - ng;   // new blocks are unpinned right away
             m_unp += ng;
         }
-        PROF_T(p5);
-        PROF_ADD(4, p4, p5);
+        PROF_MARK(12);
 
         // ---- accounting for every group
-        PROF_T(p6);
-        PROF_ADD(5, p5, p6);
         if (lane < G) {
             const int64_t d = raw_debt(t);
             d_sum = (int64_t)((uint64_t)d_sum + (uint64_t)d);
@@ -1175,8 +1243,7 @@ struct Replayer {
             X.qf = ((nref & nb) ? 1u : 0u) | ((nadm & nb) ? 2u : 0u);
         }
         bsync();   // X.qf and all state of this request are visible
-        PROF_T(p7);
-        PROF_ADD(6, p6, p7);
+        PROF_MARK(13);
         return true;
     }
 
@@ -1201,6 +1268,8 @@ struct Replayer {
         resident = 0;
         s_size = s_unp = m_unp = 0;
         gseq = curS = curM = 0;
+        gseq0 = 0;
+        gx = 0;
         rmax = 0;
         err = 0;
         ev_total = in_vgpr((uint64_t)0);
@@ -1215,25 +1284,30 @@ struct Replayer {
         r_max = 0;
         last_h = last_m = last_e = last_o = 0;
 #ifdef PC_PROFILE
-        for (int i = 0; i < 8; ++i) prof[i] = 0;
+        if (tid < 16) X.prof[tid] = 0;
+        if (tid == 0) X.prof_last = __builtin_amdgcn_s_memtime();
 #endif
         gsync();
     }
 
     DEV void run(int64_t *st, int32_t *per_req) {
+        preq = (per_req && I.per_req_off >= 0) ? per_req + I.per_req_off : nullptr;
+        pr_next = 0;
         init();
         int32_t status = 0;
         int64_t tprev = 0, tlast = 0;
-        const int64_t nreq = T.n_req;
-        Req q = {};
+        const int64_t nreq = n_req;
+        Req q = {}, nx = {};
+        int64_t done = 0;
         uint64_t kn = 0;
         uint32_t bref = 0, badm = 0;
         if (nreq > 0) {
             q = load_req(0);
-            kn = (q.nfull > tid && q.ko >= 0 && q.ko + q.nfull <= T.n_keys) ? tkeys[q.ko + tid] : 0ull;
-            if ((int64_t)q.p < T.n_prefix && tid == 0) {
+            if (nreq > 1) nx = load_req(1);
+            kn = (q.nfull() > tid && q.ko >= 0 && q.kend <= n_keys) ? tkeys[q.ko + tid] : 0ull;
+            if ((int64_t)q.p < n_prefix && tid == 0) {
                 bref = bits[q.p >> 5];
-                badm = bits[I.n_prefix_words + (q.p >> 5)];
+                badm = bits[npw + (q.p >> 5)];
                 const uint32_t nb = 1u << (q.p & 31);
                 X.qf = ((bref & nb) ? 1u : 0u) | ((badm & nb) ? 2u : 0u);
             }
@@ -1241,20 +1315,20 @@ struct Replayer {
         bsync();
         for (int64_t r = 0; r < nreq; ++r) {
             const bool has_next = r + 1 < nreq;
-            Req nx = {};
-            if (has_next) nx = load_req(r + 1);
             // a malformed next request must not be prefetched from
-            const bool nx_ok = has_next && nx.ko >= 0 && nx.nfull >= 0 && nx.ko + nx.nfull <= T.n_keys &&
-                               (int64_t)nx.p < T.n_prefix;
-            if (!request(r, q, tprev, kn, bref, badm, nx, nx_ok)) { status = -1; break; }
+            const bool nx_ok = has_next && nx.ko >= 0 && nx.nfull() >= 0 && nx.kend <= n_keys &&
+                               (int64_t)nx.p < n_prefix;
+            Req nn = {};
+            if (!request(r, q, tprev, kn, bref, badm, nx, nx_ok, nn)) { status = -1; break; }
+            ++done;
             if (err) { status = err; break; }
             tlast = tprev;
-            if (per_req && I.per_req_off >= 0 && tid == 0) {
-                int32_t *o = per_req + I.per_req_off + 4 * r;
-                o[0] = last_h; o[1] = last_m; o[2] = last_e; o[3] = last_o;
-            }
             q = nx;
+            nx = nn;
         }
+        // the last completed request's quadruple (the others were written
+        // while the request after them ran)
+        if (preq && tid == 0 && done > pr_next) put_per_request(done - 1);
         gsync();
         if (wid != 0) return;
         // stats record: 64 groups x 17 int64, then the instance block
@@ -1282,7 +1356,7 @@ struct Replayer {
             qq[7] = (int64_t)(uint32_t)status;   // status in the low 32 bits
         }
 #ifdef PC_PROFILE
-        if (lane < 8) st[63 * kGroupFields + lane] = (int64_t)prof[lane];
+        if (lane < 16) st[63 * kGroupFields + lane] = (int64_t)X.prof[lane];
 #endif
     }
 };

@@ -38,9 +38,23 @@ def parse():
     ap.add_argument("--requests", type=int, default=None, help="requests per trace (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-requests", type=int, default=25000)
-    ap.add_argument("--parity-check", action="store_true",
-                    help="compare one instance per policy against the oracle (slow; off by default)")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (3 times) and exit: the "
+                         "known-size kernel that HBM byte counters are scaled against")
     return ap.parse_args()
+
+
+def calibrate_copy(mib):
+    import torch
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n,
+                      "launches": 3}))
 
 
 def main():
@@ -50,6 +64,9 @@ def main():
               "would shard across GPUs with no collective, but no multi-GPU run is part of it.",
               file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy_mib:
+        calibrate_copy(args.calibrate_copy_mib)
+        return
     import torch
     from paper_2608_01657_amd import device as dv
     from paper_2608_01657_amd import tracegen as tg

@@ -155,11 +155,13 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         // main table: 8-entry buckets, load <= 2/3
         d.nb_log2 = std::max(1, ceil_log2((int64_t)s.capacity * 3 / 16 + 1));
         d.log_log2 = ceil_log2(s.capacity + maxn + 128);
-        d.rs_log2 = std::max(6, ceil_log2(2 * maxn));
         if (s.policy == PC_S3FIFO && d.g_cap > 0) {
             d.gnb_log2 = std::max(1, ceil_log2((int64_t)d.g_cap * 3 / 16 + 1));
             d.gr_log2 = ceil_log2((int64_t)d.g_cap + 64);
         }
+        // request duplicate set: 8-entry buckets, at most half full; between
+        // lookups it also holds the per-bucket claim counters of both tables
+        d.rs_log2 = std::max({6, ceil_log2(2 * maxn), d.nb_log2, d.gnb_log2});
         d.n_prefix_words = (int32_t)((t.n_prefix + 31) / 32);
         // state region (identical layout in LDS or in the workspace)
         int64_t so = 0;
@@ -175,7 +177,7 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         d.o_rset = take(4LL << d.rs_log2);
         d.o_posslot = take(2 * mx);
         d.o_vlist = take(2 * mx);
-        d.o_evown = take(8LL * 64);
+        d.o_rcnt = take(4LL << (d.rs_log2 - 3));
         d.o_res = take(4LL * 64);
         if (s.policy == PC_PREFIXSHIELD) {
             d.o_pfx = take(4 * C);

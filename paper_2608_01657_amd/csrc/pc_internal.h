@@ -53,7 +53,7 @@ struct DevInst {
     int32_t n_prefix_words;
     // state-region offsets (bytes)
     int32_t o_key, o_stamp, o_meta, o_table, o_log, o_posslot, o_rset, o_rkeys, o_vlist;
-    int32_t o_pfx, o_gtable, o_evown, o_res, o_cnt, o_cur;
+    int32_t o_pfx, o_gtable, o_rcnt, o_res, o_cnt, o_cur;
     // workspace offsets (bytes from workspace base)
     int64_t ws_state;      // state region when !in_lds
     int64_t ws_bits;       // uint32 [2 * n_prefix_words]: referenced, admitted

@@ -200,13 +200,13 @@ struct Coll {
 #endif
 };
 
-// Key -> two buckets, 16-bit tag (never 0xFFFF, so empty entries never match
-// a tag), duplicate-set home.  Keys are usually hash outputs already, but the
-// ABI accepts any uint64, so mix with 32-bit ops.
+// Key -> two table buckets, 16-bit tag (never 0xFFFF, so empty entries never
+// match a tag), two duplicate-set buckets.  Keys are usually hash outputs
+// already, but the ABI accepts any uint64, so mix with 32-bit ops.
 struct TH {
-    uint32_t b1, b2, tag, rhome;
+    uint32_t b1, b2, tag, r1, r2;
 };
-DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rsmask) {
+DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rbmask) {
     const uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
     uint32_t x = lo * 0x85EBCA6Bu ^ hi;
     x ^= x >> 15;
@@ -222,7 +222,9 @@ DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rsmask) {
     if (h.b2 == h.b1) h.b2 = h.b1 ^ 1u;
     const uint32_t t = y >> 16;
     h.tag = t == 0xFFFFu ? 0xFFFEu : t;
-    h.rhome = (x >> 11) & rsmask;
+    h.r1 = (x >> 11) & rbmask;
+    h.r2 = (y >> 3) & rbmask;
+    if (h.r2 == h.r1) h.r2 = h.r1 ^ 1u;
     return h;
 }
 
@@ -267,14 +269,13 @@ struct Replayer {
     const DevTrace &T;
     int policy, C, flags, G, K, nseg;
     int64_t eps;
-    uint32_t nbmask, rsmask, lmask, R, gnbmask, grmask;
+    uint32_t nbmask, rsmask, rbmask, lmask, R, gnbmask, grmask;
     int32_t s_cap, g_cap, move_thr;
     int64_t rho[4], beta[4], invw[4];   // kept in VGPRs
     // ---------------- arrays
     uint64_t *key, *rkeys;
-    uint32_t *stamp, *meta, *table, *rset, *cnt, *cur, *res, *pfx, *gtable;
+    uint32_t *stamp, *meta, *table, *rset, *rcnt, *cnt, *cur, *res, *pfx, *gtable;
     uint16_t *log, *posslot, *vlist;
-    unsigned long long *evown;
     GLOBAL uint32_t *bits;
     GLOBAL uint64_t *gring;
     const GLOBAL uint64_t *tkeys;
@@ -298,6 +299,7 @@ struct Replayer {
     int32_t err;
     // ---------------- statistics and group state (lane x = group x, VGPRs)
     uint64_t ev_total, s3_moves, s3_reins, s3_ghits, s3_gins;
+    uint64_t evw;             // evictions of group `lane` seen by this wavefront
     int64_t bal[4], last[4];
     uint64_t c_req, c_probe, c_hit, c_miss, c_charged, c_evc, c_promo, c_gated, c_orph, c_dup, c_trunc;
     int64_t d_max, d_sum;
@@ -318,6 +320,7 @@ struct Replayer {
         eps = I.eps;
         nbmask = (1u << I.nb_log2) - 1u;
         rsmask = (1u << I.rs_log2) - 1u;
+        rbmask = rsmask >> 3;
         R = 1u << I.log_log2;
         lmask = R - 1u;
         gnbmask = (1u << I.gnb_log2) - 1u;
@@ -345,7 +348,7 @@ struct Replayer {
         log = reinterpret_cast<uint16_t *>(sbase + I.o_log);
         posslot = reinterpret_cast<uint16_t *>(sbase + I.o_posslot);
         vlist = reinterpret_cast<uint16_t *>(sbase + I.o_vlist);
-        evown = reinterpret_cast<unsigned long long *>(sbase + I.o_evown);
+        rcnt = reinterpret_cast<uint32_t *>(sbase + I.o_rcnt);
         bits = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_bits));
         gring = gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_gring));
         n_req = T.n_req;
@@ -483,22 +486,40 @@ struct Replayer {
         for (int i = 0; i < 16; ++i) at = (at < 0 && e[i] == val) ? i : at;
         if (at >= 0) tb[epos(h, at)] = kEmpty;
     }
-    // Parallel insert of a new entry; false when both buckets are full.
-    DEV bool tinsert(uint32_t *tb, uint32_t val, const TH &h) {
-        uint32_t e[16];
-        load_buckets(tb, h, e);
-        int n1 = 0, n2 = 0;
+    // Parallel insert without compare-and-swap.  Every inserter of a step
+    // reads its two buckets (e, the snapshot) before a barrier that no table
+    // write crosses; after it, a claim counter per bucket (ctr[b], kEmpty
+    // meaning zero) hands out distinct ranks, and rank r takes the r-th empty
+    // entry of the snapshot -- the emptier bucket first.  `touched` records
+    // the counters used, which tclaim_reset puts back to kEmpty after the
+    // next barrier.  False when both buckets are full.
+    DEV bool tclaim(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, const uint32_t (&e)[16],
+                    uint32_t &touched) {
+        uint32_t m1 = 0, m2 = 0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) { n1 += e[i] == kEmpty; n2 += e[8 + i] == kEmpty; }
-        const int first = n2 > n1 ? 8 : 0;
+        for (int i = 0; i < 8; ++i) {
+            m1 |= (e[i] == kEmpty ? 1u : 0u) << i;
+            m2 |= (e[8 + i] == kEmpty ? 1u : 0u) << i;
+        }
+        const bool sec = __builtin_popcount(m2) > __builtin_popcount(m1);
+        touched = 0;
         for (int pass = 0; pass < 2; ++pass) {
-            const int base = pass == 0 ? first : 8 - first;
-            for (int w = 0; w < 8; ++w) {
-                if (e[base + w] != kEmpty) continue;
-                if (atomicCAS(&tb[epos(h, base + w)], kEmpty, val) == kEmpty) return true;
+            const bool use2 = (pass == 0) == sec;
+            const uint32_t b = use2 ? h.b2 : h.b1;
+            uint32_t msk = use2 ? m2 : m1;
+            touched |= use2 ? 2u : 1u;
+            uint32_t r = atomicAdd(&ctr[b], 1u) + 1u;
+            if (r < (uint32_t)__builtin_popcount(msk)) {
+                while (r--) msk &= msk - 1u;
+                tb[8 * b + (uint32_t)__builtin_ctz(msk)] = val;
+                return true;
             }
         }
         return false;
+    }
+    DEV void tclaim_reset(uint32_t *ctr, const TH &h, uint32_t touched) {
+        if (touched & 1u) ctr[h.b1] = kEmpty;
+        if (touched & 2u) ctr[h.b2] = kEmpty;
     }
     // Record an entry that found both buckets full; kick_pending() places it.
     DEV void defer_kick(uint32_t val, uint64_t k, bool main) {
@@ -514,7 +535,7 @@ struct Replayer {
         uint64_t ck = k;
         uint32_t from = 0xFFFFFFFFu;
         for (int it = 0; it < 512; ++it) {
-            const TH h = thash(ck, msk, rsmask);
+            const TH h = thash(ck, msk, rbmask);
             for (int i = 0; i < 16; ++i) {
                 const uint32_t p = epos(h, i);
                 if (tb[p] == kEmpty) { tb[p] = cv; return true; }
@@ -545,18 +566,45 @@ struct Replayer {
         if (rfl((uint32_t)X.kerr)) err = kErrInternal;
     }
 
+    // ============================================================ per-group counters
+    // LDS atomics on a few shared counters serialize lane by lane, so the
+    // lanes of a wavefront are grouped by index first: one atomic per
+    // distinct index.  Called by every lane of the wavefront.
+    DEV void wave_add(uint32_t *arr, uint32_t idx, bool active, int d) {
+        uint64_t act = ballot(active);
+        while (act) {
+            const int l = first_bit(act);
+            const uint32_t x = __builtin_amdgcn_readlane(idx, l);
+            const uint64_t m = ballot(active && idx == x);
+            if (lane == l) atomicAdd(&arr[x], (uint32_t)(d * popc(m)));
+            act &= ~m;
+        }
+    }
+    // evictions by owner, counted in lane `owner` of this wavefront
+    DEV void wave_count_evicted(uint32_t o, bool active) {
+        uint64_t act = ballot(active);
+        while (act) {
+            const uint32_t x = __builtin_amdgcn_readlane(o, first_bit(act));
+            const uint64_t m = ballot(active && o == x);
+            if ((uint32_t)lane == x) evw += (uint64_t)popc(m);
+            act &= ~m;
+        }
+    }
+
     // ============================================================ eviction core
-    // Thread holding victim slot s (vrank = its rank among this step's victims).
-    DEV void evict_elem(uint32_t s, int vrank) {
-        const uint32_t mt = meta[s];
+    // Victims of one step: thread with v holds victim slot s with metadata mt
+    // (vrank = its rank among the step's victims).  Every thread calls this.
+    DEV void evict_elems(bool v, uint32_t s, uint32_t mt, int vrank) {
         const uint32_t o = owner_of(mt);
-        atomicAdd(&evown[o], 1ull);
-        atomicSub(&res[o], 1u);
-        const uint64_t k = key[s];
-        const TH h = thash(k, nbmask, rsmask);
-        tclear_exact(table, (h.tag << 16) | s, h);
-        meta[s] = 0;
-        vlist[nvict + vrank] = (uint16_t)s;
+        wave_count_evicted(o, v);
+        wave_add(res, o, v, -1);
+        if (v) {
+            const uint64_t k = key[s];
+            const TH h = thash(k, nbmask, rbmask);
+            tclear_exact(table, (h.tag << 16) | s, h);
+            meta[s] = 0;
+            vlist[nvict + vrank] = (uint16_t)s;
+        }
     }
     DEV void evicted(int nv) {
         nvict += nv;
@@ -611,16 +659,14 @@ struct Replayer {
             const uint32_t pos = head + tid;
             const bool valid = pos < tail;
             const uint32_t s = valid ? log[pos & lmask] : 0;
-            const bool live = valid && (meta[s] & kInLog) && stamp[s] == pos;
-            PROF_MARK(5);
+            const uint32_t mt = valid ? meta[s] : 0u;
+            const bool live = valid && (mt & kInLog) && stamp[s] == pos;
             const BMask lm = bballot1(live);
-            PROF_MARK(14);
             const int rk = lm.rank(wid);
             const int tot = lm.count();
             const int nv = tot < rem ? tot : rem;
-            if (live && rk < rem) evict_elem(s, rk);
+            evict_elems(live && rk < rem, s, mt, rk);
             evicted(nv);
-            PROF_MARK(15);
             if (nv == rem) head = head + (uint32_t)lm.nth(rem - 1) + 1;
             else head = (head + kB < tail) ? head + kB : tail;
             rem -= nv;
@@ -646,10 +692,9 @@ struct Replayer {
             const int rk = mm.rank(wid);
             const int tot = mm.count();
             const int nv = tot < rem ? tot : rem;
-            if (match && rk < rem) {
-                atomicSub(&cnt[3 * owner_of(mt) + (s < 0 ? 0u : (uint32_t)s)], 1u);
-                evict_elem(sl, rk);
-            }
+            const bool vic = match && rk < rem;
+            wave_add(cnt, 3 * owner_of(mt) + (s < 0 ? 0u : (uint32_t)s), vic, -1);
+            evict_elems(vic, sl, mt, rk);
             evicted(nv);
             if (nv == rem) c = c + (uint32_t)mm.nth(rem - 1) + 1;
             else c = (c + kB < tail) ? c + kB : tail;
@@ -772,7 +817,7 @@ struct Replayer {
     }
     DEV void ghost_expire(uint64_t kx, uint32_t x) {
         const uint32_t xp = x & grmask;
-        const TH hx = thash(kx, gnbmask, rsmask);
+        const TH hx = thash(kx, gnbmask, rbmask);
         tclear_exact(gtable, (hx.tag << 16) | xp, hx);
     }
     DEV void ghost_insert(bool v, uint64_t k, int rk, int nv) {
@@ -793,12 +838,20 @@ struct Replayer {
             const uint32_t gend = gseq + (uint32_t)nv;
             const bool ins = v && (int64_t)seq + g_cap >= (int64_t)gend;
             if (v) gring[seq & grmask] = k;
+            TH h = {};
+            uint32_t e[16];
             if (ins) {
-                const TH h = thash(k, gnbmask, rsmask);
+                h = thash(k, gnbmask, rbmask);
+                load_buckets(gtable, h, e);
+            }
+            bsync();   // snapshots are taken before any claim writes
+            uint32_t touched = 0;
+            if (ins) {
                 const uint32_t val = (h.tag << 16) | (seq & grmask);
-                if (!tinsert(gtable, val, h)) defer_kick(val, k, false);
+                if (!tclaim(gtable, rset, val, h, e, touched)) defer_kick(val, k, false);
             }
             bsync();
+            tclaim_reset(rset, h, touched);
             if (rfl(X.novf)) {   // displacement reads ring keys written just now
                 gsync();
                 kick_pending();
@@ -810,7 +863,7 @@ struct Replayer {
     // this request's own reclamation hold its victims' keys, never the key
     // of one of its new blocks, and are skipped without reading the ring.
     DEV bool ghost_take(uint64_t k) {
-        const TH h = thash(k, gnbmask, rsmask);
+        const TH h = thash(k, gnbmask, rbmask);
         uint32_t e[16];
         load_buckets(gtable, h, e);
         const uint32_t nown = gseq - gseq0;
@@ -898,7 +951,7 @@ struct Replayer {
                 m_unp -= nev;
                 s3_reins += (uint64_t)nmv;
             }
-            if (pev) evict_elem(sl, erk);
+            evict_elems(pev, sl, mt, erk);
             evicted(nev);
             rem -= nev;
             const uint32_t adv = stop < kB ? (uint32_t)stop : ((lim - sp) < (uint32_t)kB ? (lim - sp) : (uint32_t)kB);
@@ -967,24 +1020,22 @@ struct Replayer {
             const bool act = j < n;
             const uint64_t k = kcur;
             if (base + kB < n) kcur = (j + kB < n) ? tkeys[ko + j + kB] : 0ull;   // next step in flight
-            const TH h = thash(k, nbmask, rsmask);
-            const uint32_t mine = (h.tag << 16) | (uint32_t)j;
-            uint32_t rpos = 0;
-            if (act) rkeys[j] = k;
-            // the key must be in LDS before the set entry that names it
-            if constexpr (kLds) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-            else __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-            if (act) {   // first occurrence in the request keeps the smallest position
-                uint32_t idx = h.rhome;
+            const TH h = thash(k, nbmask, rbmask);
+            // file (tag, position) in the request's duplicate set: the first
+            // bucket with room along r1, r2, r2+1, ... (a claim counter each)
+            uint32_t rpos = 0, nhop = 0;
+            if (act) {
+                rkeys[j] = k;
+                uint32_t b = h.r1;
                 for (;;) {
-                    const uint32_t old = atomicCAS(&rset[idx], kEmpty, mine);
-                    if (old == kEmpty) { rpos = idx; break; }
-                    if ((old >> 16) == h.tag && rkeys[old & 0xFFFFu] == k) {
-                        atomicMin(&rset[idx], mine);
-                        rpos = idx;
+                    const uint32_t r = atomicAdd(&rcnt[b], 1u);
+                    if (r < 8u) {
+                        rpos = 8u * b + r;
+                        rset[rpos] = (h.tag << 16) | (uint32_t)j;
                         break;
                     }
-                    idx = (idx + 1) & rsmask;
+                    b = nhop == 0 ? h.r2 : ((b + 1u) & rbmask);
+                    ++nhop;
                 }
             }
             PROF_MARK(1);
@@ -993,7 +1044,25 @@ struct Replayer {
             const int ntag = act ? tprobe(h, cand) : 0;
             bsync();
             PROF_MARK(2);
-            const bool dup = act && rset[rpos] != mine;
+            // duplicate: an earlier position holds the same key.  It was filed
+            // along the same bucket sequence, no later than the first bucket
+            // whose counter never passed 8 (no claim ever left that bucket).
+            bool dup = false;
+            if (act) {
+                uint32_t b = h.r1;
+                for (int hop = 0;; ++hop) {
+                    const uint32_t cn = rcnt[b];
+                    const uint4 *q4 = reinterpret_cast<const uint4 *>(rset + 8u * b);
+                    const uint4 a0 = q4[0], a1 = q4[1];
+                    const uint32_t ev[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+                    for (int i = 0; i < 8; ++i)
+                        if ((ev[i] >> 16) == h.tag && (ev[i] & 0xFFFFu) < (uint32_t)j)
+                            dup = dup || rkeys[ev[i] & 0xFFFFu] == k;
+                    if (dup || cn <= 8u) break;
+                    b = hop == 0 ? h.r2 : ((b + 1u) & rbmask);
+                }
+            }
             const bool nd = act && !dup;
             // key, metadata and prefix id of the candidate in one round trip
             const uint64_t ck = ntag == 1 ? key[cand] : 0ull;
@@ -1018,12 +1087,24 @@ struct Replayer {
             bballot<5>(pa, ma);
             PROF_MARK(4);
             // a one-step request leaves the set empty entry by entry
-            if (n <= kB && act) rset[rpos] = kEmpty;
+            if (n <= kB && act) {
+                rset[rpos] = kEmpty;
+                uint32_t b = h.r1;
+                rcnt[b] = 0u;
+                for (uint32_t hop = 0; hop < nhop; ++hop) {
+                    b = hop == 0 ? h.r2 : ((b + 1u) & rbmask);
+                    rcnt[b] = 0u;
+                }
+            }
             if (hend == n && ma[0].any()) hend = base + ma[0].first();
             const int lim = hend - base;   // threads below lim are in the leading run
             const bool isHit = found && tid < lim;
             const bool isOrph = found && tid >= lim;
             const bool elig = eligc && tid < lim;
+            // hits and orphans leave their free queue; orphans also leave
+            // their owner's resident count
+            if (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), found, -1);
+            wave_add(res, owner_of(mt), isOrph, -1);
             if (isHit) {   // pin; touch
                 uint32_t m2 = mt | kPin;
                 if (policy == kS3) {
@@ -1031,21 +1112,14 @@ struct Replayer {
                     m2 = (m2 & ~(3u << kFreqShift)) | ((f < 3 ? f + 1 : 3u) << kFreqShift);
                 } else {
                     m2 &= ~kInLog;
-                    if (policy == kPS) {
-                        atomicSub(&cnt[3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt))], 1u);
-                        if (elig && gate_open) m2 = (m2 & ~(3u << kClsShift)) | ((uint32_t)kReuse << kClsShift);
-                    }
+                    if (policy == kPS && elig && gate_open)
+                        m2 = (m2 & ~(3u << kClsShift)) | ((uint32_t)kReuse << kClsShift);
                 }
                 meta[slot] = m2;
             }
             // orphans: the old block leaves; its slot and table entry are
             // reused by the new block of the same key
-            if (isOrph) {
-                const uint32_t o = owner_of(mt);
-                atomicSub(&res[o], 1u);
-                if (policy == kPS) atomicSub(&cnt[3 * o + (nseg == 1 ? 0u : cls_of(mt))], 1u);
-                meta[slot] = kPin;
-            }
+            if (isOrph) meta[slot] = kPin;
             if (act) posslot[j] = dup ? kNoSlot : (found ? (uint16_t)slot : kNewMark);
             const BMask hitm = ma[1].below(lim);
             const int nh = hitm.count(), nf = ma[1].count(), no = nf - nh;
@@ -1063,8 +1137,10 @@ struct Replayer {
                 s_size -= os;
             }
         }
-        if (n > kB)   // longer requests clear the whole set (read by all steps)
+        if (n > kB) {   // longer requests clear the whole set (read by all steps)
             for (uint32_t i = tid; i <= rsmask; i += kB) rset[i] = kEmpty;
+            for (uint32_t i = tid; i <= rbmask; i += kB) rcnt[i] = 0u;
+        }
         // the next request's first keys and prefix bits, and the descriptor
         // after it, go in flight now; stores follow the loads so that waiting
         // for the loads never waits for a store
@@ -1140,6 +1216,8 @@ struct Replayer {
         const int nfresh = C - hwm;
         int nalloc = 0, seen = 0, seen_new = 0;
         if (tid == 0) X.nghost = 0;
+        TH hh = {};
+        uint32_t touched = 0;
         for (int base = 0; base < n; base += kB) {
             const int j = base + tid;
             const bool act = j < n;
@@ -1148,19 +1226,25 @@ struct Replayer {
             const bool isNew = rl && j >= hend;           // new block (orphans included)
             const bool isN = slot == kNewMark;            // new block without a slot yet
             uint32_t mt = (rl && !isNew) ? meta[slot] : 0u;
+            // a new key reads its buckets before the barrier of the ballot
+            uint64_t kk = 0;
+            uint32_t e[16];
+            if (isN) {
+                kk = rkeys[j];
+                hh = thash(kk, nbmask, rbmask);
+                load_buckets(table, hh, e);
+            }
             bool pa[4] = {isN, rl, isNew, rl && !isNew && (mt & kQMain) != 0};
             BMask ma[4];
             bballot<4>(pa, ma);
             PROF_MARK(9);
-            uint64_t kk = 0;
+            touched = 0;
             if (isN) {
                 const int i = nalloc + ma[0].rank(wid);
                 slot = i < nfresh ? (uint32_t)(hwm + i) : vlist[i - nfresh];
-                kk = rkeys[j];
                 key[slot] = kk;
-                const TH hh = thash(kk, nbmask, rsmask);
                 const uint32_t val = (hh.tag << 16) | slot;
-                if (!tinsert(table, val, hh)) defer_kick(val, kk, true);
+                if (!tclaim(table, rset, val, hh, e, touched)) defer_kick(val, kk, true);
             }
             nalloc += ma[0].count();
             PROF_MARK(10);
@@ -1168,12 +1252,16 @@ struct Replayer {
                 mt = mbase;
                 if (policy == kPS) pfx[slot] = p;
             }
+            PROF_MARK(14);
             if (policy == kS3) {
                 // new blocks enter the ghost-selected queue in deepest-first
                 // order; hits stay where they are; everything is unpinned
                 bool gh = false;
                 if (isNew && g_cap > 0) gh = ghost_take(isN ? kk : key[slot]);
-                if (gh) atomicAdd(&X.nghost, 1u);
+                {
+                    const uint64_t gm = ballot(gh);
+                    if (lane == 0 && gm) atomicAdd(&X.nghost, (uint32_t)popc(gm));
+                }
                 if (isNew) {
                     const uint32_t np = tail + (uint32_t)(m - 1 - (seen_new + ma[2].rank(wid)));
                     log[np & lmask] = (uint16_t)slot;
@@ -1190,18 +1278,21 @@ struct Replayer {
                 log[np & lmask] = (uint16_t)slot;
                 stamp[slot] = np;
                 meta[slot] = (mt & ~kPin) | kInLog | kRes;
-                if (policy == kPS) atomicAdd(&cnt[3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt))], 1u);
             }
+            if (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), rl, 1);
+            PROF_MARK(15);
             seen += ma[1].count();
             seen_new += ma[2].count();
             PROF_MARK(11);
             if (base + kB < n) {   // another step follows: place displaced entries first
                 bsync();
+                tclaim_reset(rset, hh, touched);
                 kick_pending();
             }
         }
         if (policy == kS3) gsync();   // ghost-ring writes of this request are visible
         else bsync();
+        tclaim_reset(rset, hh, touched);
         kick_pending();
         hwm += nalloc < nfresh ? nalloc : nfresh;
         if (m > 0) {
@@ -1252,7 +1343,8 @@ struct Replayer {
         const uint32_t nte = 8u * (nbmask + 1u);
         for (uint32_t i = tid; i < nte; i += kB) table[i] = kEmpty;
         for (int i = tid; i < C; i += kB) meta[i] = 0;
-        for (int i = tid; i < 64; i += kB) { evown[i] = 0ull; res[i] = 0u; }
+        for (int i = tid; i < 64; i += kB) res[i] = 0u;
+        for (uint32_t i = tid; i <= rbmask; i += kB) rcnt[i] = 0u;
         if (policy == kPS)
             for (int i = tid; i < 196; i += kB) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
         for (int i = tid; i < 2 * I.n_prefix_words; i += kB) bits[i] = 0u;
@@ -1277,6 +1369,7 @@ struct Replayer {
         s3_reins = in_vgpr((uint64_t)0);
         s3_ghits = in_vgpr((uint64_t)0);
         s3_gins = in_vgpr((uint64_t)0);
+        evw = 0;
 #pragma unroll
         for (int cc = 0; cc < 4; ++cc) { bal[cc] = cc < K ? beta[cc] : 0; last[cc] = 0; }
         c_req = c_probe = c_hit = c_miss = c_charged = c_evc = c_promo = c_gated = c_orph = c_dup = c_trunc = 0;
@@ -1329,6 +1422,7 @@ struct Replayer {
         // the last completed request's quadruple (the others were written
         // while the request after them ran)
         if (preq && tid == 0 && done > pr_next) put_per_request(done - 1);
+        X.kkey[tid] = evw;   // per-wavefront eviction counts, summed below
         gsync();
         if (wid != 0) return;
         // stats record: 64 groups x 17 int64, then the instance block
@@ -1336,7 +1430,7 @@ struct Replayer {
         const bool grp = lane < G;
         int64_t *o = st + lane * kGroupFields;
         const int64_t dend = (grp && ok && nreq > 0) ? raw_debt(tlast) : 0;
-        const uint64_t ev_own = grp ? evown[lane] : 0ull;
+        const uint64_t ev_own = grp ? X.kkey[lane] + X.kkey[64 + lane] + X.kkey[128 + lane] + X.kkey[192 + lane] : 0ull;
         const uint32_t rr = grp ? res[lane] : 0u;
         const int64_t v[kGroupFields] = {(int64_t)c_req, (int64_t)c_probe, (int64_t)c_hit, (int64_t)c_miss,
                                          (int64_t)c_charged, (int64_t)ev_own, (int64_t)c_evc, (int64_t)c_promo,

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libpcreplay.so")
 
 PC_OK, PC_EINVAL, PC_ENOMEM, PC_EDEVICE, PC_EUNSUPPORTED, PC_EINTERNAL = 0, -1, -2, -3, -4, -5
 PC_BLOCK_TOKENS = 16
+PC_MAX_GROUPS, PC_MAX_CONTRACTS, PC_MAX_CAPACITY = 64, 4, 32767
 PC_LRU, PC_S3FIFO, PC_PREFIXSHIELD = 0, 1, 2
 PC_FLAG_NO_SEGMENTATION, PC_FLAG_NO_DEBT_GATE = 1, 2
 PC_STATS_RECORD_BYTES = 64 * 136 + 64

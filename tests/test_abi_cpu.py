@@ -1,0 +1,136 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/pc.h declares, and rejects malformed calls on the host (before any
+device work) with the documented error codes.  No compute call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_01657_amd as P
+from paper_2608_01657_amd import tracegen as tg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000   # a non-null device address; host validation never dereferences it
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "pc.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w \t\*]*?\b(pc_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ("pc_hash_blocks", "pc_replay_batch", "pc_get_stats", "pc_block_offsets",
+              "pc_replay_workspace_bytes", "pc_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(P.LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(P.EXPORTS) == sorted(_declared()), "binding and header disagree"
+
+
+def test_struct_sizes_match_header():
+    assert ctypes.sizeof(P.pc_group_stats) == 136
+    assert ctypes.sizeof(P.pc_instance_stats) == 64
+    assert P.PC_STATS_RECORD_BYTES == 64 * 136 + 64
+
+
+def _trace(**kw):
+    t = P.pc_trace_desc()
+    t.d_keys = t.d_key_off = t.d_group = t.d_contract = t.d_prefix = FAKE
+    t.n_req, t.n_keys, t.n_prefix, t.n_groups, t.max_req_blocks = 10, 100, 4, 2, 20
+    for k, v in kw.items():
+        setattr(t, k, v)
+    return t
+
+
+def _inst(**kw):
+    i = P.make_instance_desc(tg.Instance(0, tg.POLICY_PREFIXSHIELD, 64))
+    for k, v in kw.items():
+        setattr(i, k, v)
+    return i
+
+
+def _ws(t, i):
+    lib = P.lib()
+    return lib.pc_replay_workspace_bytes((P.pc_trace_desc * 1)(t), 1, (P.pc_instance_desc * 1)(i), 1)
+
+
+def test_workspace_size_of_a_valid_batch():
+    assert _ws(_trace(), _inst()) > 0
+
+
+@pytest.mark.parametrize("field,value,needle", [
+    ("capacity", 0, "capacity"),
+    ("capacity", P.PC_MAX_CAPACITY + 1, "capacity"),
+    ("policy", 3, "policy"),
+    ("flags", 4, "flags"),
+    ("n_contracts", 0, "n_contracts"),
+    ("n_contracts", 5, "n_contracts"),
+    ("reserved", 1, "reserved"),
+    ("eps_q16", -1, "eps"),
+    ("trace", 1, "trace"),
+])
+def test_instance_validation(field, value, needle):
+    assert _ws(_trace(), _inst(**{field: value})) == P.PC_EINVAL
+    assert needle in P.pc_last_error()
+
+
+def test_contract_validation():
+    i = _inst()
+    i.contract[0].rho_q16 = 0
+    assert _ws(_trace(), i) == P.PC_EINVAL and "rho" in P.pc_last_error()
+    i = _inst()
+    i.contract[0].beta_q16 = -1
+    assert _ws(_trace(), i) == P.PC_EINVAL and "beta" in P.pc_last_error()
+
+
+@pytest.mark.parametrize("field,value", [
+    ("n_groups", 0), ("n_groups", 65), ("n_req", -1), ("d_keys", 0), ("d_key_off", 0),
+])
+def test_trace_validation(field, value):
+    assert _ws(_trace(**{field: value}), _inst()) == P.PC_EINVAL
+
+
+def test_replay_rejects_small_or_misaligned_workspace():
+    lib = P.lib()
+    T = (P.pc_trace_desc * 1)(_trace())
+    I = (P.pc_instance_desc * 1)(_inst())
+    need = lib.pc_replay_workspace_bytes(T, 1, I, 1)
+    assert need > 0
+    assert lib.pc_replay_batch(T, 1, I, 1, FAKE, need - 1, FAKE, None, None) == P.PC_ENOMEM
+    assert lib.pc_replay_batch(T, 1, I, 1, FAKE + 4, need, FAKE, None, None) == P.PC_EINVAL
+    assert lib.pc_replay_batch(T, 1, I, 1, None, need, FAKE, None, None) == P.PC_EINVAL
+
+
+def test_hash_rejects_before_launch():
+    lib = P.lib()
+    st = ctypes.c_void_p(FAKE)
+    # only 16-token blocks are implemented
+    assert lib.pc_hash_blocks(FAKE, 64, FAKE, FAKE, FAKE, FAKE, 1, 32, FAKE, 4, st, None) == P.PC_EUNSUPPORTED
+    assert lib.pc_hash_blocks(FAKE, 64, FAKE, FAKE, FAKE, FAKE, 1, 16, FAKE, 4, None, None) == P.PC_EINVAL
+    assert lib.pc_hash_blocks(FAKE + 4, 64, FAKE, FAKE, FAKE, FAKE, 1, 16, FAKE, 4, st, None) == P.PC_EINVAL
+    assert lib.pc_hash_blocks(FAKE, -1, FAKE, FAKE, FAKE, FAKE, 1, 16, FAKE, 4, st, None) == P.PC_EINVAL
+    assert lib.pc_block_offsets(FAKE, 4, 8, FAKE, None) == P.PC_EUNSUPPORTED
+
+
+def test_get_stats_rejects_bad_instance_index():
+    lib = P.lib()
+    G = (P.pc_group_stats * 64)()
+    S = (P.pc_instance_stats * 1)()
+    assert lib.pc_get_stats(FAKE, 2, 5, G, 64, S, None) == P.PC_EINVAL
+    assert lib.pc_get_stats(None, 2, 0, G, 64, S, None) == P.PC_EINVAL
+
+
+def test_product_path_has_no_fallback(monkeypatch):
+    """Without the built library the binding raises; it never computes on
+    the host."""
+    monkeypatch.setattr(P, "LIB_PATH", os.path.join(ROOT, "no_such_library.so"))
+    monkeypatch.setattr(P, "_lib", None)
+    with pytest.raises(RuntimeError, match="no CPU fallback"):
+        P.pc_last_error()

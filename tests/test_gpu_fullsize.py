@@ -1,0 +1,124 @@
+"""GPU parity at the full sizes of the five workloads.
+
+Every instance is a full-length trace.  The one-touch 4096-block batch is
+replayed exactly as bench.py times it (16 traces x 3 policies = 48
+instances, 50,000 requests each, one batch) and every instance is compared
+with the oracle.  The larger batches are replayed on a sample of their seeds
+(the trace length, capacities, policies and refill sweep are the full ones);
+there the oracle checks a sample of instances and every instance is checked
+against invariants that hold at any size."""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import assert_same
+from paper_2608_01657_amd import device as dv
+from paper_2608_01657_amd import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+WORKERS = min(16, os.cpu_count() or 1)
+
+
+def _hash_all(traces, check_keys=(0,)):
+    """Hash every trace on the GPU; keys of the traces in `check_keys` are
+    compared with the oracle's.  Returns device traces and oracle keys."""
+    dts = [dv.upload(tr) for tr in traces]
+    for t in dts:
+        dv.cut_and_hash(t)
+    with ThreadPoolExecutor(WORKERS) as ex:
+        okeys = list(ex.map(oracle.hash_trace, traces))
+    for i, t in enumerate(dts):
+        assert int(t.status.item()) == 0
+        assert np.array_equal(t.key_off.cpu().numpy(), okeys[i][1]), f"trace {i}: key offsets differ"
+        if i in check_keys:
+            keys = t.keys[:t.n_keys].cpu().numpy().view(np.uint64)
+            assert np.array_equal(keys, okeys[i][0]), f"trace {i}: keys differ"
+    return dts, okeys
+
+
+def _invariants(groups, inst, spec, n_req):
+    """Properties of any replay: conservation of probes, charges and
+    residency (every block is keyed in its group's namespace, so an orphan's
+    owner is its requester)."""
+    tot = lambda f: sum(g[f] for g in groups)
+    assert tot("requests") == n_req
+    for g in groups:
+        assert g["hits"] + g["misses"] == g["probes"]
+        assert g["charged"] == g["misses"] - g["dups"]
+        assert g["resident_end"] == g["charged"] - g["evicted_owned"] - g["orphans"]
+        assert 0 <= g["resident_end"] <= g["resident_max"] <= spec.capacity
+        assert g["debt_end_q16"] <= g["debt_max_q16"]
+    assert tot("evicted_owned") == tot("evictions_caused") == inst["evictions"]
+    assert 0 <= inst["resident_end"] <= inst["resident_max"] <= spec.capacity
+    assert inst["resident_end"] == tot("resident_end")
+    if spec.policy != tg.POLICY_PREFIXSHIELD:
+        assert tot("promotions") == 0 and tot("gated") == 0
+
+
+def _replay_and_compare(traces, insts, dts, okeys, oracle_ids):
+    b = dv.ReplayBatch(dts, insts)
+    b.launch()
+    res = b.results()
+
+    def orc(k):
+        spec = insts[k]
+        return k, oracle.replay_trace(traces[spec.trace], okeys[spec.trace][0], okeys[spec.trace][1], spec)
+
+    with ThreadPoolExecutor(WORKERS) as ex:
+        outs = list(ex.map(orc, oracle_ids))
+    for k, o in outs:
+        assert_same(res[k], o, f"instance {k} ({insts[k].label}, seed trace {insts[k].trace})")
+    for k, (groups, inst, status) in enumerate(res):
+        assert status == 0
+        _invariants(groups, inst, insts[k], traces[insts[k].trace].n_req)
+    return res
+
+
+def test_onetouch4096_bench_batch_all_instances():
+    traces, insts = tg.workload("onetouch4096")
+    assert len(insts) == 48 and all(t.n_req == 50000 for t in traces)
+    dts, okeys = _hash_all(traces, check_keys=range(len(traces)))
+    _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))
+
+
+def test_twopass_full_length_sampled_seeds():
+    traces, insts = tg.workload("twopass", seeds=[0, 1, 2, 3])
+    assert all(t.n_req == 80000 for t in traces)
+    dts, okeys = _hash_all(traces)
+    _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))
+
+
+def test_delayed_full_length_refill_sweep():
+    traces, insts = tg.workload("delayed", seeds=[0, 1])
+    assert all(t.n_req == 200000 for t in traces) and len(insts) == 48
+    dts, okeys = _hash_all(traces)
+    # oracle: every policy at the lowest and highest refill rate of seed 0
+    sample = [k for k, i in enumerate(insts) if i.trace == 0 and ("_rho1" == i.label[-5:] or i.label.endswith("_rho128"))]
+    assert len(sample) == 6
+    _replay_and_compare(traces, insts, dts, okeys, sample)
+
+
+def test_chat_full_length_all_capacities():
+    """Capacities up to 16,384 blocks: the larger ones keep their state in the
+    workspace instead of LDS."""
+    traces, insts = tg.workload("chat", seeds=[0, 1])
+    assert all(t.n_req == 100000 for t in traces) and len(insts) == 30
+    dts, okeys = _hash_all(traces)
+    sample = [k for k, i in enumerate(insts) if i.trace == 0]
+    _replay_and_compare(traces, insts, dts, okeys, sample)
+
+
+def test_scale1024_sampled():
+    """1,024 concurrent 4096-block instances (16 traces x 64 policy variants);
+    the oracle checks LRU, S3-FIFO and three refill rates of one trace."""
+    traces, insts = tg.workload("scale1024")
+    assert len(insts) == 1024
+    dts, okeys = _hash_all(traces)
+    sample = [k for k, i in enumerate(insts) if i.trace == 5 and
+              (i.policy != tg.POLICY_PREFIXSHIELD or i.label.split("rho")[-1] in ("1/4", "16/4", "62/4"))]
+    assert len(sample) == 5
+    _replay_and_compare(traces, insts, dts, okeys, sample)

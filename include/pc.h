@@ -5,8 +5,8 @@
  * 2608.01657): cutting token sequences into full 16-token KV blocks with
  * chained 64-bit block keys, and replaying many independent multi-tenant
  * prefix-cache instances (LRU, S3-FIFO, PrefixShield) over those keys, one
- * GPU wavefront per instance, with admission debt metered per accounting
- * group.
+ * GPU workgroup (four wavefronts) per instance, with admission debt metered
+ * per accounting group.
  *
  * Conventions (every entry point):
  *   - Pointers named d_* are DEVICE pointers owned by the caller; they must
@@ -152,7 +152,7 @@ typedef struct {
 int64_t pc_replay_workspace_bytes(const pc_trace_desc *traces, int32_t n_traces,
                                   const pc_instance_desc *inst, int32_t n_inst);
 
-/* Replay every instance over its trace, one wavefront per instance; queued
+/* Replay every instance over its trace, one workgroup per instance; queued
  * on `stream`.
  *   d_workspace   device memory of at least pc_replay_workspace_bytes()
  *                 bytes, 256-byte aligned; its contents need not be zeroed.

@@ -259,15 +259,18 @@ struct Req {
     DEV int64_t nfull() const { return kend - ko; }
 };
 
-template <bool kLds>
+// kPol is the instance's policy: each policy gets its own specialized copy
+// of the request loop (no runtime policy tests, fewer live registers).
+template <bool kLds, int kPol>
 struct Replayer {
+    static constexpr int policy = kPol;
     Coll &X;
     const int tid, wid, lane;
     int cb;                   // ballot buffer in use
     // ---------------- configuration (uniform)
     const DevInst &I;
     const DevTrace &T;
-    int policy, C, flags, G, K, nseg;
+    int C, flags, G, K, nseg;
     int64_t eps;
     uint32_t nbmask, rsmask, rbmask, lmask, R, gnbmask, grmask;
     int32_t s_cap, g_cap, move_thr;
@@ -311,7 +314,6 @@ struct Replayer {
     DEV Replayer(Coll &coll, const DevInst &inst, const DevTrace &tr, uint8_t *sbase, uint8_t *ws)
         : X(coll), tid((int)threadIdx.x), wid((int)rfl(threadIdx.x >> 6)), lane((int)__lane_id()), cb(0),
           I(inst), T(tr) {
-        policy = I.policy;
         C = I.capacity;
         flags = I.flags;
         G = T.n_groups;
@@ -632,20 +634,20 @@ struct Replayer {
             bsync();
         }
         tail = nw;
-        if (policy == kPS)
+        if constexpr (policy == kPS)
             for (int i = tid; i < 196; i += kB) cur[i] = head;
         curS = curM = head;
         bsync();
     }
     DEV void ensure_room(uint32_t k) {
         if (tail + k - head <= R) return;
-        if (policy == kPS) {   // lowest cursor of a non-empty queue bounds every live entry
+        if constexpr (policy == kPS) {   // lowest cursor of a non-empty queue bounds every live entry
             uint32_t m = tail;
             for (int i = lane; i < 192; i += 64)
                 if (cnt[i] > 0 && cur[i] < m) m = cur[i];
             m = wave_min32(m);
             if (m > head) head = m;
-        } else if (policy == kS3) {
+        } else if constexpr (policy == kS3) {
             const uint32_t m = curS < curM ? curS : curM;
             if (m > head) head = m;
         }
@@ -1007,7 +1009,7 @@ struct Replayer {
         if (me) { c_req += 1; c_probe += (uint64_t)n; c_trunc += (uint64_t)(nfull - n); }
         const bool proven = q1 && adm;
         int64_t dg = 0;
-        if (policy == kPS) dg = bcast64(me ? raw_debt(t) : 0, g);   // before this request's charge
+        if constexpr (policy == kPS) dg = bcast64(me ? raw_debt(t) : 0, g);   // before this request's charge
         const bool gate_open = dg <= eps || (flags & kFlagNoGate);
 
         // ---- lookup, duplicates, pin + OnTouch, orphans (new blocks wait)
@@ -1103,11 +1105,11 @@ struct Replayer {
             const bool elig = eligc && tid < lim;
             // hits and orphans leave their free queue; orphans also leave
             // their owner's resident count
-            if (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), found, -1);
+            if constexpr (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), found, -1);
             wave_add(res, owner_of(mt), isOrph, -1);
             if (isHit) {   // pin; touch
                 uint32_t m2 = mt | kPin;
-                if (policy == kS3) {
+                if constexpr (policy == kS3) {
                     const uint32_t f = freq_of(mt);
                     m2 = (m2 & ~(3u << kFreqShift)) | ((f < 3 ? f + 1 : 3u) << kFreqShift);
                 } else {
@@ -1131,7 +1133,7 @@ struct Replayer {
             ndup += ma[2].count();
             if (gate_open) npromo += ne; else ngated += ne;
             resident -= no;
-            if (policy == kS3) {
+            if constexpr (policy == kS3) {
                 s_unp -= hs + os;
                 m_unp -= (nh - hs) + (no - os);
                 s_size -= os;
@@ -1176,8 +1178,8 @@ struct Replayer {
         int e = m - (C - resident);
         if (e < 0) e = 0;
         if (e > 0) {
-            if (policy == kLRU) evict_lru(e);
-            else if (policy == kPS) evict_ps(e, t);
+            if constexpr (policy == kLRU) evict_lru(e);
+            else if constexpr (policy == kPS) evict_ps(e, t);
             else evict_s3(e);
         }
         if (me) c_evc += (uint64_t)e;
@@ -1209,7 +1211,7 @@ struct Replayer {
         //      free queue, deepest first -- one pass over the positions
         PROF_MARK(7);
         const int nrel = n - ndup;
-        if (policy == kS3) { if (m > 0) ensure_room((uint32_t)m); }
+        if constexpr (policy == kS3) { if (m > 0) ensure_room((uint32_t)m); }
         else if (nrel > 0) ensure_room((uint32_t)nrel);
         PROF_MARK(8);
         const uint32_t mbase = ((uint32_t)g) | ((uint32_t)c << kContractShift) | (cls_new << kClsShift) | kRes;
@@ -1250,10 +1252,10 @@ struct Replayer {
             PROF_MARK(10);
             if (isNew) {
                 mt = mbase;
-                if (policy == kPS) pfx[slot] = p;
+                if constexpr (policy == kPS) pfx[slot] = p;
             }
             PROF_MARK(14);
-            if (policy == kS3) {
+            if constexpr (policy == kS3) {
                 // new blocks enter the ghost-selected queue in deepest-first
                 // order; hits stay where they are; everything is unpinned
                 bool gh = false;
@@ -1279,7 +1281,7 @@ struct Replayer {
                 stamp[slot] = np;
                 meta[slot] = (mt & ~kPin) | kInLog | kRes;
             }
-            if (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), rl, 1);
+            if constexpr (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), rl, 1);
             PROF_MARK(15);
             seen += ma[1].count();
             seen_new += ma[2].count();
@@ -1290,7 +1292,7 @@ struct Replayer {
                 kick_pending();
             }
         }
-        if (policy == kS3) gsync();   // ghost-ring writes of this request are visible
+        if constexpr (policy == kS3) gsync();   // ghost-ring writes of this request are visible
         else bsync();
         tclaim_reset(rset, hh, touched);
         kick_pending();
@@ -1302,7 +1304,7 @@ struct Replayer {
         // (one unconditional update of the log tail keeps every member of
         // the uniform state in registers)
         tail += (uint32_t)(policy == kS3 ? m : nrel);
-        if (policy == kS3) {
+        if constexpr (policy == kS3) {
             const int ng = (int)rfl(X.nghost);
             s_size += m - ng;
             s3_ghits += (uint64_t)ng;
@@ -1345,7 +1347,7 @@ struct Replayer {
         for (int i = tid; i < C; i += kB) meta[i] = 0;
         for (int i = tid; i < 64; i += kB) res[i] = 0u;
         for (uint32_t i = tid; i <= rbmask; i += kB) rcnt[i] = 0u;
-        if (policy == kPS)
+        if constexpr (policy == kPS)
             for (int i = tid; i < 196; i += kB) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
         for (int i = tid; i < 2 * I.n_prefix_words; i += kB) bits[i] = 0u;
         if (policy == kS3 && g_cap > 0) {
@@ -1468,8 +1470,17 @@ __global__ __launch_bounds__(kB) void replay_kernel(const DevInst *__restrict__ 
     uint8_t *sbase;
     if constexpr (kLds) sbase = smem;
     else sbase = ws + I.ws_state;
-    Replayer<kLds> rp(coll, I, T, sbase, ws);
-    rp.run(stats + (int64_t)id * kRecordWords, per_req);
+    int64_t *st = stats + (int64_t)id * kRecordWords;
+    if (I.policy == kLRU) {
+        Replayer<kLds, kLRU> rp(coll, I, T, sbase, ws);
+        rp.run(st, per_req);
+    } else if (I.policy == kS3) {
+        Replayer<kLds, kS3> rp(coll, I, T, sbase, ws);
+        rp.run(st, per_req);
+    } else {
+        Replayer<kLds, kPS> rp(coll, I, T, sbase, ws);
+        rp.run(st, per_req);
+    }
 }
 
 }  // namespace

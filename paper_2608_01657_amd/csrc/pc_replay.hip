@@ -99,6 +99,16 @@ DEV int nth_bit(uint64_t m, int k) {
     }
     return pos;
 }
+// floor(a / b) for b > 0 and a < 2^62: a double-precision estimate, then an
+// exact integer correction (the estimate is off by at most a few units).
+DEV uint64_t udiv64(uint64_t a, uint64_t b) {
+    if (a < b) return 0;
+    uint64_t q = (uint64_t)((double)a / (double)b);
+    int64_t r = (int64_t)(a - q * b);
+    while (r < 0) { --q; r += (int64_t)b; }
+    while ((uint64_t)r >= b) { ++q; r -= (int64_t)b; }
+    return q;
+}
 // Keep a wave-uniform value in a VGPR (it is only used in per-lane
 // arithmetic) so it does not occupy scalar registers.
 template <typename T>
@@ -195,8 +205,9 @@ struct Coll {
     uint32_t kval[kB];                // displacement scratch: entries
     uint32_t kmain[kB];               // 1 = main table, 0 = ghost table
 #ifdef PC_PROFILE
-    uint64_t prof[16];                // cycle counters (thread 0)
+    uint64_t prof[32];                // cycle counters (thread 0)
     uint64_t prof_last;
+    uint64_t pcnt[16];                // event counters (thread 0)
 #endif
 };
 
@@ -245,8 +256,10 @@ DEV uint32_t freq_of(uint32_t mt) { return (mt >> kFreqShift) & 3u; }
             X.prof_last = prof_now;                               \
         }                                                         \
     } while (0)
+#define PROF_COUNT(i, v) do { if (tid == 0) X.pcnt[i] += (uint64_t)(v); } while (0)
 #else
 #define PROF_MARK(i) do { } while (0)
+#define PROF_COUNT(i, v) do { } while (0)
 #endif
 
 // Descriptor of one request (loaded one request ahead).
@@ -297,7 +310,9 @@ struct Replayer {
     int32_t s_size, s_unp, m_unp;
     uint32_t gseq, curS, curM;
     uint32_t gseq0;           // gseq when this request's reclamation began
-    uint64_t gx;              // prefetched expiring ghost key (per thread)
+    uint32_t gsw;             // ghost sweep cursor
+    uint32_t gne, gspan;      // ghost table entries; sweep span (ring - g_cap - 256)
+    uint64_t gsrate;          // ceil(gne * 2^16 / gspan): entries swept per insertion, Q16
     int32_t rmax;
     int32_t err;
     // ---------------- statistics and group state (lane x = group x, VGPRs)
@@ -327,6 +342,9 @@ struct Replayer {
         lmask = R - 1u;
         gnbmask = (1u << I.gnb_log2) - 1u;
         grmask = (1u << I.gr_log2) - 1u;
+        gne = 8u << I.gnb_log2;
+        gspan = (grmask + 1u) - (uint32_t)I.g_cap - (uint32_t)kB;
+        gsrate = I.g_cap > 0 ? (((uint64_t)gne << 16) + gspan - 1) / gspan : 0;
         s_cap = I.s_cap;
         g_cap = I.g_cap;
         move_thr = I.move_thr;
@@ -495,13 +513,17 @@ struct Replayer {
     // entry of the snapshot -- the emptier bucket first.  `touched` records
     // the counters used, which tclaim_reset puts back to kEmpty after the
     // next barrier.  False when both buckets are full.
+    // For the ghost table (gref != 0) an entry that left the window counts
+    // as empty (see glive).
     DEV bool tclaim(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, const uint32_t (&e)[16],
-                    uint32_t &touched) {
+                    uint32_t &touched, bool ghost = false, uint32_t gref = 0) {
         uint32_t m1 = 0, m2 = 0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            m1 |= (e[i] == kEmpty ? 1u : 0u) << i;
-            m2 |= (e[8 + i] == kEmpty ? 1u : 0u) << i;
+            const bool f1 = ghost ? !glive(e[i], gref) : e[i] == kEmpty;
+            const bool f2 = ghost ? !glive(e[8 + i], gref) : e[8 + i] == kEmpty;
+            m1 |= (f1 ? 1u : 0u) << i;
+            m2 |= (f2 ? 1u : 0u) << i;
         }
         const bool sec = __builtin_popcount(m2) > __builtin_popcount(m1);
         touched = 0;
@@ -530,8 +552,9 @@ struct Replayer {
         X.kkey[i] = k;
         X.kmain[i] = main ? 1u : 0u;
     }
-    // Serial cuckoo displacement, one thread.
-    DEV bool kick(uint32_t *tb, bool main, uint32_t val, uint64_t k) {
+    // Serial cuckoo displacement, one thread.  gref: ghost sequence that
+    // decides which ghost entries are still live.
+    DEV bool kick(uint32_t *tb, bool main, uint32_t val, uint64_t k, uint32_t gref) {
         const uint32_t msk = main ? nbmask : gnbmask;
         uint32_t cv = val;
         uint64_t ck = k;
@@ -540,7 +563,7 @@ struct Replayer {
             const TH h = thash(ck, msk, rbmask);
             for (int i = 0; i < 16; ++i) {
                 const uint32_t p = epos(h, i);
-                if (tb[p] == kEmpty) { tb[p] = cv; return true; }
+                if (main ? tb[p] == kEmpty : !glive(tb[p], gref)) { tb[p] = cv; return true; }
             }
             uint32_t b = (h.b1 == from) ? h.b2 : h.b1;
             if (from == 0xFFFFFFFFu && (it & 1)) b = h.b2;
@@ -554,13 +577,13 @@ struct Replayer {
         return false;
     }
     // Called by all threads after a barrier that follows defer_kick calls.
-    DEV void kick_pending() {
+    DEV void kick_pending(uint32_t gref = 0) {
         const uint32_t nk = rfl(X.novf);
         if (nk == 0) return;
         if (tid == 0) {
             for (uint32_t i = 0; i < nk; ++i) {
                 const bool main = X.kmain[i] != 0;
-                if (!kick(main ? table : gtable, main, X.kval[i], X.kkey[i])) X.kerr = kErrInternal;
+                if (!kick(main ? table : gtable, main, X.kval[i], X.kkey[i], gref)) X.kerr = kErrInternal;
             }
             X.novf = 0;
         }
@@ -617,6 +640,7 @@ struct Replayer {
     // Compaction of the free-queue log: live entries keep their order and
     // are renumbered from `head`; all cursors restart at `head`.
     DEV void compact() {
+        PROF_COUNT(2, 1);
         bsync();
         uint32_t nw = head;
         for (uint32_t p0 = head; p0 < tail; p0 += kB) {
@@ -681,6 +705,7 @@ struct Replayer {
     // Take k victims from queue ci in free-queue order.  x < 0: any owner;
     // s < 0: any class (no segmentation).
     DEV void ps_take(int x, int s, int ci, int k) {
+        PROF_COUNT(3, 1);
         uint32_t c = rfl(cur[ci]);
         int rem = k;
         while (rem > 0 && err == 0) {
@@ -767,7 +792,7 @@ struct Replayer {
             const int64_t p2 = wave_max64((inE && lane != gs) ? P : -1);
             const int64_t thr = p2 > eps ? p2 : eps;
             // g* keeps winning strictly while P - i*D > max(second, eps)
-            const int64_t k1 = Pg > thr ? (Pg - thr + Dg - 1) / Dg : 0;
+            const int64_t k1 = Pg > thr ? (int64_t)udiv64((uint64_t)(Pg - thr) + (uint64_t)Dg - 1, (uint64_t)Dg) : 0;
             int64_t k = k1 > 1 ? k1 : 1;
             if (k > rem) k = rem;
             if (k > ag) k = ag;
@@ -802,61 +827,58 @@ struct Replayer {
     }
 
     // ---------------------------------------------------------------- S3-FIFO
+    // The ghost remembers the last g_cap insertions.  Entries hold (tag, ring
+    // position = sequence mod 2^gr); an entry is live while its age
+    // gref - 1 - sequence is below g_cap, so leaving the window needs no work
+    // at all.  A sweep clears dead entries before their age could wrap the
+    // ring: each batch of nv insertions (nv <= 256) sweeps
+    // ceil(nv * entries / span) entries at its start, span = 2^gr - g_cap - 256.
+    // Between two visits of an entry fewer than 256 + span insertions happen,
+    // so an entry seen live at one visit (age < g_cap) has age below
+    // g_cap + 256 + span = 2^gr when it is seen next, and is cleared then if
+    // dead.  (2^gr = min(2^16, next power of two >= 2 g_cap + 256).)
+    DEV bool glive(uint32_t e, uint32_t gref) const {
+        return e != kEmpty && ((gref - 1u - (e & 0xFFFFu)) & grmask) < (uint32_t)g_cap;
+    }
     // Ghost insertion for the threads with v (rk = rank among them, nv =
-    // count).  The ghost keeps the last g_cap insertions: entries older than
-    // the batch that leave the window are removed, and batch entries that
-    // would already have left it by the batch's end are never inserted.
-    //
-    // The keys that leave the window are read ahead: ghost_prefetch() (start
-    // of a request's reclamation) gives thread i the key of ring sequence
-    // gseq - g_cap + i.  A batch whose expiring entries all predate the
-    // request and fall in that window uses them; any other batch reads the
-    // ring after a full barrier.
-    DEV void ghost_prefetch() {
-        gseq0 = gseq;
-        const int64_t x = (int64_t)gseq - g_cap + tid;
-        gx = (g_cap > 0 && x >= 0) ? gring[(uint32_t)x & grmask] : 0ull;
-    }
-    DEV void ghost_expire(uint64_t kx, uint32_t x) {
-        const uint32_t xp = x & grmask;
-        const TH hx = thash(kx, gnbmask, rbmask);
-        tclear_exact(gtable, (hx.tag << 16) | xp, hx);
-    }
+    // count).  Batch entries that would already have left the window by the
+    // batch's end are never inserted.
     DEV void ghost_insert(bool v, uint64_t k, int rk, int nv) {
         s3_gins += (uint64_t)nv;
         if (g_cap > 0 && nv > 0) {
-            const uint32_t off = gseq - gseq0;   // ring writes of this request so far
-            const int64_t xlo = (int64_t)gseq - g_cap;   // first expiring sequence
-            if (off + (uint32_t)nv <= (uint32_t)kB && (int64_t)off + nv <= (int64_t)g_cap) {
-                const int i = tid - (int)off;
-                if (i >= 0 && i < nv && xlo + i >= 0) ghost_expire(gx, (uint32_t)(xlo + i));
-            } else {
-                if (off > 0) gsync();   // this request's ring writes are complete
-                const int64_t x = xlo + tid;
-                if (tid < nv && tid < g_cap && x >= 0) ghost_expire(gring[(uint32_t)x & grmask], (uint32_t)x);
-            }
-            bsync();   // expiries read the ring before it is rewritten
             const uint32_t seq = gseq + (uint32_t)rk;
             const uint32_t gend = gseq + (uint32_t)nv;
             const bool ins = v && (int64_t)seq + g_cap >= (int64_t)gend;
-            if (v) gring[seq & grmask] = k;
+            if (ins) gring[seq & grmask] = k;
+            uint32_t ns = (uint32_t)(((uint64_t)nv * gsrate + 0xFFFFu) >> 16);   // >= nv * gne / gspan
+            if (ns > gne) ns = gne;
+            for (uint32_t i = tid; i < ns; i += kB) {
+                const uint32_t ix = (gsw + i) & (gne - 1u);
+                const uint32_t ev = gtable[ix];
+                if (ev != kEmpty && !glive(ev, gseq)) gtable[ix] = kEmpty;
+            }
+            gsw += ns;
+            PROF_MARK(24);
             TH h = {};
             uint32_t e[16];
             if (ins) {
                 h = thash(k, gnbmask, rbmask);
                 load_buckets(gtable, h, e);
             }
-            bsync();   // snapshots are taken before any claim writes
+            bsync();   // snapshots and the sweep come before any claim writes
+            PROF_MARK(25);
             uint32_t touched = 0;
             if (ins) {
                 const uint32_t val = (h.tag << 16) | (seq & grmask);
-                if (!tclaim(gtable, rset, val, h, e, touched)) defer_kick(val, k, false);
+                if (!tclaim(gtable, rset, val, h, e, touched, true, gseq)) defer_kick(val, k, false);
             }
+            PROF_MARK(26);
             bsync();
+            PROF_MARK(27);
             tclaim_reset(rset, h, touched);
             if (rfl(X.novf)) {   // displacement reads ring keys written just now
                 gsync();
-                kick_pending();
+                kick_pending(gend);
             }
         }
         gseq += (uint32_t)nv;
@@ -872,7 +894,7 @@ struct Replayer {
         int at = -1;
         for (int i = 0; i < 16; ++i) {
             const uint32_t pos = e[i] & 0xFFFFu;
-            if (at < 0 && (e[i] >> 16) == h.tag && ((gseq - 1u - pos) & grmask) >= nown &&
+            if (at < 0 && (e[i] >> 16) == h.tag && glive(e[i], gseq) && ((gseq - 1u - pos) & grmask) >= nown &&
                 gring[pos & grmask] == k)
                 at = i;
         }
@@ -880,7 +902,6 @@ struct Replayer {
         return at >= 0;
     }
     DEV void evict_s3(int e) {
-        ghost_prefetch();
         int rem = e;
         uint32_t spS = curS, spM = curM;
         uint32_t keptS = 0xFFFFFFFFu, keptM = 0xFFFFFFFFu;
@@ -890,7 +911,10 @@ struct Replayer {
                 spS = curS; spM = curM;
                 keptS = keptM = 0xFFFFFFFFu;
             }
+            PROF_MARK(16);
             const bool useS = (s_size >= s_cap && s_unp > 0) || (m_unp == 0);
+            PROF_COUNT(0, 1);
+            PROF_COUNT(1, useS ? 1 : 0);
             const uint32_t sp = useS ? spS : spM;
             const uint32_t lim = tail;
             if (sp >= lim) { err = kErrInternal; break; }
@@ -907,7 +931,9 @@ struct Replayer {
             const bool mv = cand && (useS ? (int)f >= move_thr : f > 0);
             bool p3[3] = {cand, mv, inQ};
             BMask m3[3];
+            PROF_MARK(17);
             bballot<3>(p3, m3);
+            PROF_MARK(18);
             const BMask &candm = m3[0], &mvm = m3[1], &inQm = m3[2];
             const BMask evm = candm.andnot(mvm);
             const int crk = candm.rank(wid);
@@ -916,7 +942,9 @@ struct Replayer {
             bool ok;
             if (useS) ok = cand && ((s_size - crk >= s_cap && s_unp - crk > 0) || (m_unp + mb == 0)) && eb < rem;
             else ok = cand && eb < rem && (m_unp - eb) > 0;
+            PROF_MARK(19);
             const BMask okm = bballot1(ok);
+            PROF_MARK(20);
             const BMask bad = candm.andnot(okm);
             const int stop = bad.first();   // kB if none
             const bool proc = cand && tid < stop;
@@ -943,8 +971,10 @@ struct Replayer {
             tail += (uint32_t)nmv;
             const bool pev = proc && !mv;
             const int erk = pem.rank(wid);
+            PROF_MARK(21);
             if (useS) {
                 ghost_insert(pev, pev ? key[sl] : 0ull, erk, nev);
+                PROF_MARK(22);
                 s_size -= nmv + nev;
                 s_unp -= nmv + nev;
                 m_unp += nmv;
@@ -954,6 +984,7 @@ struct Replayer {
                 s3_reins += (uint64_t)nmv;
             }
             evict_elems(pev, sl, mt, erk);
+            PROF_MARK(23);
             evicted(nev);
             rem -= nev;
             const uint32_t adv = stop < kB ? (uint32_t)stop : ((lim - sp) < (uint32_t)kB ? (lim - sp) : (uint32_t)kB);
@@ -1363,7 +1394,7 @@ struct Replayer {
         s_size = s_unp = m_unp = 0;
         gseq = curS = curM = 0;
         gseq0 = 0;
-        gx = 0;
+        gsw = 0;
         rmax = 0;
         err = 0;
         ev_total = in_vgpr((uint64_t)0);
@@ -1379,7 +1410,8 @@ struct Replayer {
         r_max = 0;
         last_h = last_m = last_e = last_o = 0;
 #ifdef PC_PROFILE
-        if (tid < 16) X.prof[tid] = 0;
+        if (tid < 32) X.prof[tid] = 0;
+        if (tid < 16) X.pcnt[tid] = 0;
         if (tid == 0) X.prof_last = __builtin_amdgcn_s_memtime();
 #endif
         gsync();
@@ -1453,6 +1485,8 @@ struct Replayer {
         }
 #ifdef PC_PROFILE
         if (lane < 16) st[63 * kGroupFields + lane] = (int64_t)X.prof[lane];
+        if (lane < 16) st[61 * kGroupFields + lane] = (int64_t)X.prof[16 + lane];
+        if (lane < 16) st[62 * kGroupFields + lane] = (int64_t)X.pcnt[lane];
 #endif
     }
 };

@@ -22,6 +22,12 @@ from concurrent.futures import ThreadPoolExecutor
 import numpy as np
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+ROOT = os.path.dirname(os.path.abspath(__file__))
+# measured HBM bytes of the replay kernel for the default batch (rocprofv3
+# FETCH_SIZE / WRITE_SIZE, calibrated against a device copy); valid only for
+# the kernel source it was measured on
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "replay_kernel_onetouch4096_hbm_traffic.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_01657_amd", "csrc", f) for f in ("pc_replay.hip", "pc_internal.h")]
 HASH_BYTES_PER_BLOCK = 64 + 8  # 16 int32 tokens in, one uint64 key out
 HASH_BYTES_PER_REQ = 8 + 4 + 4 + 8 + 8   # tok_off, len, ns, key_off read, key_off write
 REPLAY_BYTES_PER_PROBE = 8     # the key
@@ -42,6 +48,35 @@ def parse():
                     help="only run a plain device-to-device copy of this many MiB (3 times) and exit: the "
                          "known-size kernel that HBM byte counters are scaled against")
     return ap.parse_args()
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, n_traces, n_req):
+    """HBM bytes per replay launch from the committed counter summary, or
+    None when it was taken on another kernel source or another batch."""
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_PROFILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    if kv.get("batch") != f"{workload} traces={n_traces} requests={n_req}":
+        return None
+    try:
+        return int(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def calibrate_copy(mib):
@@ -132,7 +167,7 @@ def main():
             "achieved": round(replay_gbs if dominant == "replay" else hash_gbs, 3),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round((replay_gbs if dominant == "replay" else hash_gbs) / HBM_PEAK_GBS, 6),
-            "traffic": None,
+            "traffic": measured_traffic(args.workload, len(traces), traces[0].n_req) if dominant == "replay" else None,
             "bytes_per_launch": int(replay_bytes if dominant == "replay" else hash_bytes),
             "avg_launch_ms": round(replay_ms if dominant == "replay" else hash_ms, 4)}
     roof_hash = {"kernel": "hash_kernel (+ block offsets)", "bound": "hbm", "achieved": round(hash_gbs, 2),

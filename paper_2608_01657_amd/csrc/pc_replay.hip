@@ -99,10 +99,19 @@ DEV int nth_bit(uint64_t m, int k) {
     }
     return pos;
 }
-// floor(a / b) for b > 0 and a < 2^62: a double-precision estimate, then an
-// exact integer correction (the estimate is off by at most a few units).
+// floor(a / b) for 0 < b < 2^63: below 2^53 a double-precision estimate and
+// an exact integer correction (the estimate is off by at most one or two);
+// above, plain shift-and-subtract.
 DEV uint64_t udiv64(uint64_t a, uint64_t b) {
     if (a < b) return 0;
+    if (a >> 53) {
+        uint64_t q = 0, r = 0;
+        for (int i = 63; i >= 0; --i) {
+            r = (r << 1) | ((a >> i) & 1u);
+            if (r >= b) { r -= b; q |= 1ull << i; }
+        }
+        return q;
+    }
     uint64_t q = (uint64_t)((double)a / (double)b);
     int64_t r = (int64_t)(a - q * b);
     while (r < 0) { --q; r += (int64_t)b; }

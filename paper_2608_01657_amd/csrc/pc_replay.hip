@@ -188,6 +188,16 @@ struct BMask {
         }
         return r;
     }
+    // keep only bits of threads at index t or above
+    DEV BMask from(int t) const {
+        BMask r;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) {
+            const int lo = t - 64 * i;
+            r.w[i] = lo <= 0 ? w[i] : (lo >= 64 ? 0ull : (w[i] & ~((1ull << lo) - 1)));
+        }
+        return r;
+    }
     DEV BMask andnot(const BMask &o) const {
         BMask r;
 #pragma unroll
@@ -524,16 +534,23 @@ struct Replayer {
     // next barrier.  False when both buckets are full.
     // For the ghost table (gref != 0) an entry that left the window counts
     // as empty (see glive).
+    // Free-entry masks of both buckets of a snapshot: bits 0-7 bucket b1,
+    // bits 8-15 bucket b2.
+    DEV uint32_t free_mask(const uint32_t (&e)[16], bool ghost, uint32_t gref) const {
+        uint32_t m = 0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const bool f = ghost ? !glive(e[i], gref) : e[i] == kEmpty;
+            m |= (f ? 1u : 0u) << i;
+        }
+        return m;
+    }
     DEV bool tclaim(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, const uint32_t (&e)[16],
                     uint32_t &touched, bool ghost = false, uint32_t gref = 0) {
-        uint32_t m1 = 0, m2 = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const bool f1 = ghost ? !glive(e[i], gref) : e[i] == kEmpty;
-            const bool f2 = ghost ? !glive(e[8 + i], gref) : e[8 + i] == kEmpty;
-            m1 |= (f1 ? 1u : 0u) << i;
-            m2 |= (f2 ? 1u : 0u) << i;
-        }
+        return tclaim_m(tb, ctr, val, h, free_mask(e, ghost, gref), touched);
+    }
+    DEV bool tclaim_m(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, uint32_t fm, uint32_t &touched) {
+        const uint32_t m1 = fm & 0xFFu, m2 = fm >> 8;
         const bool sec = __builtin_popcount(m2) > __builtin_popcount(m1);
         touched = 0;
         for (int pass = 0; pass < 2; ++pass) {
@@ -626,16 +643,33 @@ struct Replayer {
     }
 
     // ============================================================ eviction core
+    // Before the barrier of a scan step, every thread that may hold a victim
+    // looks up its block's key and the table entry naming its slot (the
+    // table does not change during reclamation, except for the clears of
+    // this same step, which never move an entry).  Returns the entry's
+    // index, or kEmpty.
+    DEV uint32_t victim_entry(bool maybe, uint32_t s, uint64_t &k) const {
+        k = 0;
+        if (!maybe) return kEmpty;
+        k = key[s];
+        const TH h = thash(k, nbmask, rbmask);
+        uint32_t e[16];
+        load_buckets(table, h, e);
+        const uint32_t val = (h.tag << 16) | s;
+        uint32_t loc = kEmpty;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) loc = (loc == kEmpty && e[i] == val) ? epos(h, i) : loc;
+        return loc;
+    }
     // Victims of one step: thread with v holds victim slot s with metadata mt
-    // (vrank = its rank among the step's victims).  Every thread calls this.
-    DEV void evict_elems(bool v, uint32_t s, uint32_t mt, int vrank) {
+    // (vrank = its rank among the step's victims) and its table entry loc.
+    // Every thread calls this.
+    DEV void evict_elems(bool v, uint32_t s, uint32_t mt, int vrank, uint32_t loc) {
         const uint32_t o = owner_of(mt);
         wave_count_evicted(o, v);
         wave_add(res, o, v, -1);
         if (v) {
-            const uint64_t k = key[s];
-            const TH h = thash(k, nbmask, rbmask);
-            tclear_exact(table, (h.tag << 16) | s, h);
+            if (loc != kEmpty) table[loc] = kEmpty;
             meta[s] = 0;
             vlist[nvict + vrank] = (uint16_t)s;
         }
@@ -696,11 +730,13 @@ struct Replayer {
             const uint32_t s = valid ? log[pos & lmask] : 0;
             const uint32_t mt = valid ? meta[s] : 0u;
             const bool live = valid && (mt & kInLog) && stamp[s] == pos;
+            uint64_t vk;
+            const uint32_t loc = victim_entry(live, s, vk);
             const BMask lm = bballot1(live);
             const int rk = lm.rank(wid);
             const int tot = lm.count();
             const int nv = tot < rem ? tot : rem;
-            evict_elems(live && rk < rem, s, mt, rk);
+            evict_elems(live && rk < rem, s, mt, rk, loc);
             evicted(nv);
             if (nv == rem) head = head + (uint32_t)lm.nth(rem - 1) + 1;
             else head = (head + kB < tail) ? head + kB : tail;
@@ -724,13 +760,15 @@ struct Replayer {
             const uint32_t mt = valid ? meta[sl] : 0;
             const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
             const bool match = live && (x < 0 || (int)owner_of(mt) == x) && (s < 0 || (int)cls_of(mt) == s);
+            uint64_t vk;
+            const uint32_t loc = victim_entry(match, sl, vk);
             const BMask mm = bballot1(match);
             const int rk = mm.rank(wid);
             const int tot = mm.count();
             const int nv = tot < rem ? tot : rem;
             const bool vic = match && rk < rem;
             wave_add(cnt, 3 * owner_of(mt) + (s < 0 ? 0u : (uint32_t)s), vic, -1);
-            evict_elems(vic, sl, mt, rk);
+            evict_elems(vic, sl, mt, rk, loc);
             evicted(nv);
             if (nv == rem) c = c + (uint32_t)mm.nth(rem - 1) + 1;
             else c = (c + kB < tail) ? c + kB : tail;
@@ -840,7 +878,7 @@ struct Replayer {
     // position = sequence mod 2^gr); an entry is live while its age
     // gref - 1 - sequence is below g_cap, so leaving the window needs no work
     // at all.  A sweep clears dead entries before their age could wrap the
-    // ring: each batch of nv insertions (nv <= 256) sweeps
+    // ring: each batch (nv <= 256 insertions) sweeps at least
     // ceil(nv * entries / span) entries at its start, span = 2^gr - g_cap - 256.
     // Between two visits of an entry fewer than 256 + span insertions happen,
     // so an entry seen live at one visit (age < g_cap) has age below
@@ -848,49 +886,6 @@ struct Replayer {
     // dead.  (2^gr = min(2^16, next power of two >= 2 g_cap + 256).)
     DEV bool glive(uint32_t e, uint32_t gref) const {
         return e != kEmpty && ((gref - 1u - (e & 0xFFFFu)) & grmask) < (uint32_t)g_cap;
-    }
-    // Ghost insertion for the threads with v (rk = rank among them, nv =
-    // count).  Batch entries that would already have left the window by the
-    // batch's end are never inserted.
-    DEV void ghost_insert(bool v, uint64_t k, int rk, int nv) {
-        s3_gins += (uint64_t)nv;
-        if (g_cap > 0 && nv > 0) {
-            const uint32_t seq = gseq + (uint32_t)rk;
-            const uint32_t gend = gseq + (uint32_t)nv;
-            const bool ins = v && (int64_t)seq + g_cap >= (int64_t)gend;
-            if (ins) gring[seq & grmask] = k;
-            uint32_t ns = (uint32_t)(((uint64_t)nv * gsrate + 0xFFFFu) >> 16);   // >= nv * gne / gspan
-            if (ns > gne) ns = gne;
-            for (uint32_t i = tid; i < ns; i += kB) {
-                const uint32_t ix = (gsw + i) & (gne - 1u);
-                const uint32_t ev = gtable[ix];
-                if (ev != kEmpty && !glive(ev, gseq)) gtable[ix] = kEmpty;
-            }
-            gsw += ns;
-            PROF_MARK(24);
-            TH h = {};
-            uint32_t e[16];
-            if (ins) {
-                h = thash(k, gnbmask, rbmask);
-                load_buckets(gtable, h, e);
-            }
-            bsync();   // snapshots and the sweep come before any claim writes
-            PROF_MARK(25);
-            uint32_t touched = 0;
-            if (ins) {
-                const uint32_t val = (h.tag << 16) | (seq & grmask);
-                if (!tclaim(gtable, rset, val, h, e, touched, true, gseq)) defer_kick(val, k, false);
-            }
-            PROF_MARK(26);
-            bsync();
-            PROF_MARK(27);
-            tclaim_reset(rset, h, touched);
-            if (rfl(X.novf)) {   // displacement reads ring keys written just now
-                gsync();
-                kick_pending(gend);
-            }
-        }
-        gseq += (uint32_t)nv;
     }
     // ghost hit for key k: remove it and report true.  Entries written by
     // this request's own reclamation hold its victims' keys, never the key
@@ -910,6 +905,23 @@ struct Replayer {
         if (at >= 0) gtable[epos(h, at)] = kEmpty;
         return at >= 0;
     }
+    // Sweep of the ghost table for a batch of at most kB insertions (see
+    // the ghost's description above); runs before the batch's barrier.
+    DEV void ghost_sweep() {
+        uint32_t ns = (uint32_t)(((uint64_t)kB * gsrate + 0xFFFFu) >> 16);
+        if (ns > gne) ns = gne;
+        for (uint32_t i = tid; i < ns; i += kB) {
+            const uint32_t ix = (gsw + i) & (gne - 1u);
+            const uint32_t ev = gtable[ix];
+            if (ev != kEmpty && !glive(ev, gseq)) gtable[ix] = kEmpty;
+        }
+        gsw += ns;
+    }
+    // One scan step per batch: the queue in use (S or M, Z18) is scanned from
+    // its cursor; candidates are its live unpinned entries.  Everything a
+    // victim needs that does not depend on which candidates end up as
+    // victims (its table entry, its ghost buckets, the ghost sweep) is done
+    // before the step's only ballot.
     DEV void evict_s3(int e) {
         int rem = e;
         uint32_t spS = curS, spM = curM;
@@ -938,6 +950,21 @@ struct Replayer {
             // small queue: move (accessed) or evict into the ghost;
             // main queue: reinsert (freq > 0) or evict
             const bool mv = cand && (useS ? (int)f >= move_thr : f > 0);
+            const bool maybe_ev = cand && !mv;
+            uint64_t vk;
+            const uint32_t loc = victim_entry(maybe_ev, sl, vk);
+            const bool gho = useS && g_cap > 0;
+            TH hg = {};
+            uint32_t gfree = 0;
+            if (gho) {
+                if (maybe_ev) {
+                    hg = thash(vk, gnbmask, rbmask);
+                    uint32_t eg[16];
+                    load_buckets(gtable, hg, eg);
+                    gfree = free_mask(eg, true, gseq);
+                }
+                ghost_sweep();
+            }
             bool p3[3] = {cand, mv, inQ};
             BMask m3[3];
             PROF_MARK(17);
@@ -945,17 +972,41 @@ struct Replayer {
             PROF_MARK(18);
             const BMask &candm = m3[0], &mvm = m3[1], &inQm = m3[2];
             const BMask evm = candm.andnot(mvm);
-            const int crk = candm.rank(wid);
-            const int mb = mvm.rank(wid);
-            const int eb = evm.rank(wid);
-            bool ok;
-            if (useS) ok = cand && ((s_size - crk >= s_cap && s_unp - crk > 0) || (m_unp + mb == 0)) && eb < rem;
-            else ok = cand && eb < rem && (m_unp - eb) > 0;
+            // The batch is the longest prefix of candidates that may all be
+            // processed: each condition below holds on a prefix of them, so
+            // `stop` (first candidate not processed, kB if none) is the
+            // earliest position where one of them starts to fail.
+            const int ncand = candm.count(), nevall = evm.count();
+            int stop;
+            if (useS) {
+                // |S| - (earlier candidates) >= S_cap and unpinned S left
+                const int la = min(s_size - s_cap + 1, s_unp);
+                const int pa = la <= 0 ? candm.first() : (la < ncand ? candm.nth(la) : kB);
+                // ... or M has no unpinned block and nothing moved there yet
+                int pb;
+                if (m_unp > 0) pb = candm.first();
+                else if (mvm.any()) {
+                    const BMask a = candm.from(mvm.first() + 1);
+                    pb = a.any() ? a.first() : kB;
+                } else pb = kB;
+                // fewer than `rem` evictions before it
+                int pc = kB;
+                if (rem <= nevall) {
+                    const BMask a = candm.from(evm.nth(rem - 1) + 1);
+                    pc = a.any() ? a.first() : kB;
+                }
+                stop = min(max(pa, pb), pc);
+            } else {
+                // fewer than min(rem, unpinned M) evictions before it
+                const int q = min(rem, m_unp);
+                stop = kB;
+                if (q <= 0) stop = candm.first();
+                else if (q <= nevall) {
+                    const BMask a = candm.from(evm.nth(q - 1) + 1);
+                    stop = a.any() ? a.first() : kB;
+                }
+            }
             PROF_MARK(19);
-            const BMask okm = bballot1(ok);
-            PROF_MARK(20);
-            const BMask bad = candm.andnot(okm);
-            const int stop = bad.first();   // kB if none
             const bool proc = cand && tid < stop;
             const BMask pmm = mvm.below(stop), pem = evm.below(stop);
             const int nmv = pmm.count(), nev = pem.count();
@@ -980,10 +1031,22 @@ struct Replayer {
             tail += (uint32_t)nmv;
             const bool pev = proc && !mv;
             const int erk = pem.rank(wid);
-            PROF_MARK(21);
+            PROF_MARK(20);
+            uint32_t gtouched = 0;
             if (useS) {
-                ghost_insert(pev, pev ? key[sl] : 0ull, erk, nev);
-                PROF_MARK(22);
+                // ghost insertion of the evicted blocks, in eviction order;
+                // entries that would leave the window within the batch are
+                // not inserted
+                if (gho && nev > 0) {
+                    const uint32_t seq = gseq + (uint32_t)erk;
+                    const uint32_t gend = gseq + (uint32_t)nev;
+                    if (pev && (int64_t)seq + g_cap >= (int64_t)gend) {
+                        gring[seq & grmask] = vk;
+                        const uint32_t val = (hg.tag << 16) | (seq & grmask);
+                        if (!tclaim_m(gtable, rset, val, hg, gfree, gtouched)) defer_kick(val, vk, false);
+                    }
+                }
+                s3_gins += (uint64_t)nev;
                 s_size -= nmv + nev;
                 s_unp -= nmv + nev;
                 m_unp += nmv;
@@ -992,14 +1055,26 @@ struct Replayer {
                 m_unp -= nev;
                 s3_reins += (uint64_t)nmv;
             }
-            evict_elems(pev, sl, mt, erk);
-            PROF_MARK(23);
+            PROF_MARK(21);
+            evict_elems(pev, sl, mt, erk, loc);
+            PROF_MARK(22);
             evicted(nev);
             rem -= nev;
             const uint32_t adv = stop < kB ? (uint32_t)stop : ((lim - sp) < (uint32_t)kB ? (lim - sp) : (uint32_t)kB);
             if (adv == 0) err = kErrInternal;   // a scan that cannot advance is a bug, never a hang
             if (useS) spS = sp + adv; else spM = sp + adv;
             bsync();
+            PROF_MARK(23);
+            if (useS) {
+                if (gho && nev > 0) {
+                    tclaim_reset(rset, hg, gtouched);
+                    if (rfl(X.novf)) {   // displacement reads ring keys written just now
+                        gsync();
+                        kick_pending(gseq + (uint32_t)nev);
+                    }
+                }
+                gseq += (uint32_t)nev;
+            }
         }
         curS = keptS < spS ? keptS : spS;
         curM = keptM < spM ? keptM : spM;

@@ -294,6 +294,54 @@ def delayed_replay(seed: int = 4000, n_requests: int = 200000) -> Trace:
                    8, 80 + n_unique, roles)
 
 
+# The three service tiers of the paper's setup (premium, standard, basic:
+# 64 / 40 / 16 blocks/s refill, bursts 256 / 192 / 128 blocks), converted to
+# blocks per request at its ~6 req/s load, in Q16.
+TIER_CONTRACTS = [((64 * Q16 + 3) // 6, 256 * Q16),
+                  ((40 * Q16 + 3) // 6, 192 * Q16),
+                  ((16 * Q16 + 3) // 6, 128 * Q16)]
+
+
+def tiered_contracts(seed: int = 6000, n_requests: int = 50000) -> Trace:
+    """Six tenants on three contract tiers (contract ids 0 premium, 1
+    standard, 2 basic):
+      g0 premium  victim-like hot prefixes (32, Zipf 0.9, +128 tokens)
+      g1 standard 8 private 2048-token prefixes, Zipf 1.1, +128 tokens
+      g2 basic    same shape as g1
+      g3 two contracts: its prefixes 0-3 are billed to standard, 4-7 to basic
+      g4 premium polluter (unique prompts, the one-touch length law)
+      g5 basic polluter   (same)
+    Each request picks its tenant with weights 20/15/15/15/15/20 %."""
+    rng = _rng(seed)
+    vic = _VictimSource(rng)
+    hot = {g: [rng.integers(0, VOCAB, size=2048, dtype=np.int32) for _ in range(8)] for g in (1, 2, 3)}
+    tenants = rng.choice(6, size=n_requests, p=[0.20, 0.15, 0.15, 0.15, 0.15, 0.20])
+    zv = vic.draw(n_requests)
+    zb = _zipf_choice(rng, 1.1, 8, n_requests)
+    plen = _polluter_lengths(rng, n_requests)
+    st = _Stream(rng)
+    offs, lens, groups, prefixes, contracts = [], [], [], [], []
+    n_unique = 0
+    for r in range(n_requests):
+        g = int(tenants[r])
+        if g == 0:
+            o, L, pid = vic.emit(st, zv[r]); c = 0
+        elif g in (1, 2, 3):
+            z = int(zb[r])
+            t = np.concatenate([hot[g][z], st.fresh(128)])
+            o = st.append(t); L = len(t); pid = 32 + 8 * (g - 1) + z
+            c = 1 if g == 1 else 2 if g == 2 else (1 if z < 4 else 2)
+        else:
+            L = int(plen[r]); o = st.append(st.fresh(L)); pid = 56 + n_unique; n_unique += 1
+            c = 0 if g == 4 else 2
+        offs.append(o); lens.append(L); groups.append(g); prefixes.append(pid); contracts.append(c)
+    tr = _finish(f"tiered_contracts_s{seed}", st, offs, lens, groups, prefixes, 6, 56 + n_unique,
+                 {0: "premium victim", 1: "standard", 2: "basic", 3: "two contracts",
+                  4: "premium polluter", 5: "basic polluter"})
+    tr.contract = np.asarray(contracts, np.uint8)
+    return tr
+
+
 def conversations(seed: int = 5000, n_requests: int = 100000, n_groups: int = 16,
                   active_per_group: int = 4, max_tokens: int = 16384) -> Trace:
     """Benign multi-turn chats.  Each request picks a group uniformly, then
@@ -373,6 +421,8 @@ def workload(name: str, seeds: Optional[Sequence[int]] = None,
     chat          16 groups, C in {1K..16K}, 100,000 requests, 64 seeds, 960
     scale1024     onetouch4096 traces x 64 variants (LRU, S3-FIFO and
                   PrefixShield at 62 refill rates k/4, k=1..62) = 1024
+    tiers         6 groups on 3 contract tiers, C=4096, 50,000 requests,
+                  8 seeds, 3 policies -> 24
     `seeds` selects seed indices (0-based) and `n_requests` shortens traces.
     """
     traces: List[Trace] = []
@@ -413,6 +463,13 @@ def workload(name: str, seeds: Optional[Sequence[int]] = None,
                     inst.append(Instance(len(traces) - 1, pol, 4096,
                                          contracts=[(rho * Q16, DEFAULT_BETA_Q16)],
                                          label=f"{POLICY_NAMES[pol]}_rho{rho}"))
+    elif name == "tiers":
+        idx = list(seeds) if seeds is not None else list(range(8))
+        for i in idx:
+            traces.append(tiered_contracts(6000 + i, n_requests or 50000))
+            for pol in policies:
+                inst.append(Instance(len(traces) - 1, pol, 4096, contracts=list(TIER_CONTRACTS),
+                                     label=POLICY_NAMES[pol]))
     elif name == "chat":
         idx = list(seeds) if seeds is not None else list(range(64))
         caps = list(capacities) if capacities is not None else [1024, 2048, 4096, 8192, 16384]

@@ -122,3 +122,12 @@ def test_scale1024_sampled():
               (i.policy != tg.POLICY_PREFIXSHIELD or i.label.split("rho")[-1] in ("1/4", "16/4", "62/4"))]
     assert len(sample) == 5
     _replay_and_compare(traces, insts, dts, okeys, sample)
+
+
+def test_tiers_full_length_all_instances():
+    """Three contract tiers (normalized debt, Eq. 5; a group with two
+    contracts), full length, every instance against the oracle."""
+    traces, insts = tg.workload("tiers", seeds=[0, 1])
+    assert all(t.n_req == 50000 for t in traces) and len(insts) == 6
+    dts, okeys = _hash_all(traces, check_keys=(0, 1))
+    _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))

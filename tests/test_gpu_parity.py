@@ -160,3 +160,16 @@ def test_replay_delayed_short():
 def test_replay_chat_all_capacities():
     """Includes capacities whose state does not fit in LDS (workspace path)."""
     _workload_parity("chat", [0], 4000, per_request=True)
+
+
+def test_replay_normalized_debt_tiers():
+    """The Eq. 5 / Eq. 8 pins of the oracle (fast vs slow contract at equal
+    raw debt, before and past the crossover) on the GPU."""
+    from test_oracle_replay_pins import _tier_trace
+    Q = tg.Q16
+    kts, per = [], []
+    for m, e in [(40, 20), (40, 36), (64, 47), (64, 60)]:
+        kts.append(_tier_trace(m, e))
+        per.append([tg.Instance(0, pol, 2 * m, contracts=[(4 * Q, 0), (Q, 0), (Q, 1 << 40)], flags=fl)
+                    for pol in POLICIES for fl in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0])])
+    run_key_traces(kts, per)

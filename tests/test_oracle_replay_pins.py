@@ -342,3 +342,51 @@ def test_victim_protected_under_one_touch():
     r_ps = oracle.replay_trace(tr, keys, off, tg.Instance(0, tg.POLICY_PREFIXSHIELD, 256))
     assert r_ps.groups[0]["hits"] > r_lru.groups[0]["hits"]
     assert r_ps.groups[1]["evicted_owned"] > r_lru.groups[1]["evicted_owned"]
+
+
+# ---------------------------------------------------------------- Eq. 5
+
+def _tier_trace(m, e):
+    """Groups A (fast contract 0) and B (slow contract 1) each materialize m
+    one-touch blocks at tick 0 (equal raw debt m blocks, beta = 0); then group
+    D (contract 2, a huge burst, so never indebted) needs e new blocks in a
+    cache of 2m."""
+    A = list(range(1, m + 1))
+    B = list(range(1000, 1000 + m))
+    D = list(range(5000, 5000 + e))
+    return key_trace([A, B, D], groups=[0, 1, 2], contracts=[0, 1, 2], tick=[0, 0, 0])
+
+
+@pytest.mark.parametrize("m,e", [(40, 20), (40, 30), (64, 47)])
+def test_normalized_debt_ranks_slow_contract_first(m, e):
+    """Eq. 5: with equal raw debt, the group on the faster-refilling contract
+    has the smaller normalized debt (debt / w_c, w_c = rho_c / rho_min), so
+    every victim comes from the slow contract's group while its projected
+    debt m - k stays above the fast group's m * rho_slow / rho_fast (Eqs. 7-8:
+    k < 3m/4 here).  Ranking by raw debt would instead tie and take the older
+    blocks of A first."""
+    fast, slow = 4 * Q, Q
+    inst = tg.Instance(0, tg.POLICY_PREFIXSHIELD, 2 * m,
+                       contracts=[(fast, 0), (slow, 0), (Q, 1 << 40)])
+    res = oracle.replay_key_trace(_tier_trace(m, e), inst)
+    assert e < 3 * m // 4 + 1
+    assert res.groups[1]["evicted_owned"] == e
+    assert res.groups[0]["evicted_owned"] == 0
+    assert res.groups[2]["debt_max_q16"] == 0
+
+
+def test_normalized_debt_crossover():
+    """Past the crossover both Eq. 5 and Eq. 8 show.  m = 40, e = 36:
+    P_B = 40 - k_B (decrement 1/W_B = 1 block) and P_A = 10 - k_A/4 (A's only
+    indebted contract has w = rho_fast/rho_min = 4, so 1/W_A = 1/4 block).
+    B takes the first 30 victims (40 - k_B > 10).  Then P_B = P_A = 10, and
+    the tie goes to the older head stamp, which is A's: A (9.75), B (9),
+    A (9.5), A (9.25), A (9), tie -> A (8.75).  That makes 5 victims from A
+    and 31 from B."""
+    m, e = 40, 36
+    fast, slow = 4 * Q, Q
+    inst = tg.Instance(0, tg.POLICY_PREFIXSHIELD, 2 * m,
+                       contracts=[(fast, 0), (slow, 0), (Q, 1 << 40)])
+    res = oracle.replay_key_trace(_tier_trace(m, e), inst)
+    ea, eb = res.groups[0]["evicted_owned"], res.groups[1]["evicted_owned"]
+    assert (ea, eb) == (5, 31)

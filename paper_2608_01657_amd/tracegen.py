@@ -240,6 +240,58 @@ def two_pass(seed: int = 3000, n_requests: int = 80000) -> Trace:
                    2, 32 + n_unique, {0: "victim", 1: "polluter"})
 
 
+ATTACK_KINDS = ("none", "onetouch", "lowslow", "replay")
+
+
+def attack_trace(kind: str, seed: int = 7000, n_requests: int = 4000) -> Trace:
+    """The attack traces at the scale of the paper's setup: a victim group
+    with four 1,536-token hot prefixes (96 blocks each, 384 in all; Zipf 1.0)
+    plus 64 fresh tokens, and a polluter sending 1,536-token prompts.  The
+    first tenth of the trace is victim-only (the victim's prefixes are warm
+    and its creation debt has cleared when the attack starts); then:
+      none      victim requests only (the no-attack control)
+      onetouch  victim and a fresh polluter prompt alternate
+      lowslow   one fresh polluter prompt every 8th request (the same kind of
+                pressure, spread over time)
+      replay    alternating; every polluter prompt is sent twice in a row
+                (same prefix id), so its second request finds the blocks it
+                created -- apparent reuse that the debt gate must not turn
+                into protection"""
+    if kind not in ATTACK_KINDS:
+        raise ValueError(kind)
+    rng = _rng(seed)
+    hot = rng.integers(0, VOCAB, size=(4, 1536), dtype=np.int32)
+    r_ = np.arange(n_requests)
+    if kind == "none":
+        pol = np.zeros(n_requests, bool)
+    elif kind == "lowslow":
+        pol = (r_ % 8) == 7
+    else:
+        pol = (r_ % 2) == 1
+    pol &= r_ >= n_requests // 10
+    nv = int((~pol).sum()); npol = int(pol.sum())
+    z = _zipf_choice(rng, 1.0, 4, nv)
+    n_unique = (npol + 1) // 2 if kind == "replay" else npol
+    st = _Stream(rng)
+    offs, lens, groups, prefixes = [], [], [], []
+    views = []
+    vi = pi = 0
+    for r in range(n_requests):
+        if not pol[r]:
+            t = np.concatenate([hot[z[vi]], st.fresh(64)])
+            offs.append(st.append(t)); lens.append(len(t)); groups.append(0)
+            prefixes.append(int(z[vi])); vi += 1
+        else:
+            if kind == "replay" and pi % 2 == 1:
+                k = pi // 2
+                o = views[k]; pid = 4 + k
+            else:
+                o = st.append(st.fresh(1536)); views.append(o); pid = 4 + len(views) - 1
+            offs.append(o); lens.append(1536); groups.append(1); prefixes.append(pid); pi += 1
+    return _finish(f"attack_{kind}_s{seed}", st, offs, lens, groups, prefixes,
+                   2, 4 + max(n_unique, 1), {0: "victim", 1: "polluter"})
+
+
 def delayed_replay(seed: int = 4000, n_requests: int = 200000) -> Trace:
     """8 groups: 6 benign (8 private 2048-token prefixes, Zipf 1.1, +128
     fresh tokens), a victim (as in the one-touch workload) and a polluter.
@@ -423,6 +475,13 @@ def workload(name: str, seeds: Optional[Sequence[int]] = None,
                   PrefixShield at 62 refill rates k/4, k=1..62) = 1024
     tiers         6 groups on 3 contract tiers, C=4096, 50,000 requests,
                   8 seeds, 3 policies -> 24
+    attack_<kind> the paper-scale attack traces (kind in ATTACK_KINDS),
+                  C=511, 4,000 requests, 10 seeds x {LRU, S3-FIFO,
+                  PrefixShield, PrefixShield without segmentation, without
+                  the debt gate} -> 50
+    chat_bursty   chat traces whose requests arrive in bursts of 32 per tick
+                  (the accounting clock of Eq. 1 advances 32 ticks between
+                  bursts), C=4096, 3 policies
     `seeds` selects seed indices (0-based) and `n_requests` shortens traces.
     """
     traces: List[Trace] = []
@@ -470,6 +529,27 @@ def workload(name: str, seeds: Optional[Sequence[int]] = None,
             for pol in policies:
                 inst.append(Instance(len(traces) - 1, pol, 4096, contracts=list(TIER_CONTRACTS),
                                      label=POLICY_NAMES[pol]))
+    elif name.startswith("attack_"):
+        kind = name[len("attack_"):]
+        idx = list(seeds) if seeds is not None else list(range(10))
+        for i in idx:
+            traces.append(attack_trace(kind, 7000 + i, n_requests or 4000))
+            t = len(traces) - 1
+            for pol in policies:
+                inst.append(Instance(t, pol, 511, label=POLICY_NAMES[pol]))
+            if POLICY_PREFIXSHIELD in policies:
+                inst.append(Instance(t, POLICY_PREFIXSHIELD, 511, flags=FLAG_NO_SEGMENTATION,
+                                     label="prefixshield_noseg"))
+                inst.append(Instance(t, POLICY_PREFIXSHIELD, 511, flags=FLAG_NO_DEBT_GATE,
+                                     label="prefixshield_nogate"))
+    elif name == "chat_bursty":
+        idx = list(seeds) if seeds is not None else list(range(8))
+        for i in idx:
+            tr = conversations(5000 + i, n_requests or 100000)
+            tr.tick = (np.arange(tr.n_req, dtype=np.int64) // 32) * 32
+            traces.append(tr)
+            for pol in policies:
+                inst.append(Instance(len(traces) - 1, pol, 4096, label=POLICY_NAMES[pol]))
     elif name == "chat":
         idx = list(seeds) if seeds is not None else list(range(64))
         caps = list(capacities) if capacities is not None else [1024, 2048, 4096, 8192, 16384]

@@ -131,3 +131,29 @@ def test_tiers_full_length_all_instances():
     assert all(t.n_req == 50000 for t in traces) and len(insts) == 6
     dts, okeys = _hash_all(traces, check_keys=(0, 1))
     _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))
+
+
+def test_attack_traces_all_variants_per_request():
+    """The paper-scale attack traces (C = 511), every variant including the
+    two ablations, per-request outputs too."""
+    for kind in tg.ATTACK_KINDS:
+        traces, insts = tg.workload("attack_" + kind, seeds=[0, 1])
+        assert len(insts) == 10
+        dts, okeys = _hash_all(traces, check_keys=(0, 1))
+        b = dv.ReplayBatch(dts, insts, per_request=True)
+        b.launch()
+        res = b.results()
+        pr = b.per_request_arrays()
+        for k, spec in enumerate(insts):
+            o = oracle.replay_trace(traces[spec.trace], okeys[spec.trace][0], okeys[spec.trace][1], spec,
+                                    per_request=True)
+            assert_same(res[k], o, f"{kind} {spec.label}")
+            assert np.array_equal(pr[k], o.per_request), f"{kind} {spec.label}: per-request outputs differ"
+
+
+def test_chat_bursty_ticks_full_length():
+    """Conversational traces with bursty arrival ticks (Eq. 1's clock), full length."""
+    traces, insts = tg.workload("chat_bursty", seeds=[0])
+    assert traces[0].n_req == 100000 and traces[0].tick is not None
+    dts, okeys = _hash_all(traces)
+    _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))

@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--requests", type=int, default=None, help="requests per trace (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-requests", type=int, default=25000)
+    ap.add_argument("--phase-profile", action="store_true",
+                    help="use the phase-counter library and add per-phase cycles, reclamation latency per "
+                         "evicting request and state bytes per cached block to the JSON line")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (3 times) and exit: the "
                          "known-size kernel that HBM byte counters are scaled against")
@@ -103,6 +106,9 @@ def main():
         calibrate_copy(args.calibrate_copy_mib)
         return
     import torch
+    import paper_2608_01657_amd as P
+    if args.phase_profile:
+        P.use_phase_counters()
     from paper_2608_01657_amd import device as dv
     from paper_2608_01657_amd import tracegen as tg
 
@@ -179,6 +185,8 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(traces, insts, args.cpu_sample_requests)
 
+    phases = phase_report(batch, insts, traces, replay_ms) if args.phase_profile else None
+
     value = probes / (step_ms * 1e-3)
     out = {
         "metric": "block probes/sec (batched replay, 1 GPU)",
@@ -202,7 +210,37 @@ def main():
         "roofline_hash": roof_hash,
         "cpu_baseline": cpu,
     }
+    if phases is not None:
+        out["phase_profile"] = phases
     print(json.dumps(out))
+
+
+def phase_report(batch, insts, traces, replay_ms):
+    """Per policy: mean cycles per request of each phase, the reclamation
+    cycles of a request that evicts (converted to microseconds with the clock
+    rate implied by the slowest instance, whose cycles span the launch), and
+    state bytes per cached block."""
+    import paper_2608_01657_amd as P
+    from paper_2608_01657_amd import tracegen as tg
+    pcs = batch.phase_counters()
+    totals = [sum(pc[f"cycles_{n}"] for n in P.PHASE_NAMES) for pc in pcs]
+    mhz = max(totals) / (replay_ms * 1e3)   # cycles per microsecond
+    sbytes, in_lds = P.pc_replay_state_bytes(batch.tdesc, batch.idesc)
+    rep = {"clock_cycles_per_us": round(mhz, 1)}
+    for pol in sorted({i.policy for i in insts}):
+        ks = [k for k, i in enumerate(insts) if i.policy == pol]
+        nreq = sum(traces[insts[k].trace].n_req for k in ks)
+        ev = sum(pcs[k]["evicting_requests"] for k in ks)
+        r = {n: round(sum(pcs[k][f"cycles_{n}"] for k in ks) / nreq, 1) for n in P.PHASE_NAMES}
+        r["us_per_request"] = round(sum(totals[k] for k in ks) / nreq / mhz, 3)
+        r["reclaim_us_per_evicting_request"] = round(sum(pcs[k]["cycles_reclamation"] for k in ks) / max(ev, 1) / mhz, 3)
+        r["evicting_requests"] = ev
+        r["state_bytes_per_block"] = round(float(np.mean([sbytes[k] / insts[k].capacity for k in ks])), 1)
+        r["state_in_lds"] = all(in_lds[k] for k in ks)
+        for n in P.PHASE_EVENTS[1:]:
+            r[n] = sum(pcs[k][n] for k in ks)
+        rep[tg.POLICY_NAMES[pol]] = r
+    return rep
 
 
 def cpu_baseline(traces, insts, sample_requests):

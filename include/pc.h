@@ -152,6 +152,16 @@ typedef struct {
 int64_t pc_replay_workspace_bytes(const pc_trace_desc *traces, int32_t n_traces,
                                   const pc_instance_desc *inst, int32_t n_inst);
 
+/* Per-instance replay state (the cache metadata: block keys and metadata,
+ * the free-queue log, the block and ghost tables, per-request scratch) that
+ * pc_replay_batch would use for this batch: bytes_out[i] bytes, kept in LDS
+ * (in_lds_out[i] = 1) or in the workspace (0).  Host only; validates like
+ * pc_replay_workspace_bytes.  The per-prefix bitmaps and the S3-FIFO ghost
+ * ring live in the workspace and are not counted. */
+int32_t pc_replay_state_bytes(const pc_trace_desc *traces, int32_t n_traces,
+                              const pc_instance_desc *inst, int32_t n_inst,
+                              int64_t *bytes_out, int32_t *in_lds_out);
+
 /* Replay every instance over its trace, one workgroup per instance; queued
  * on `stream`.
  *   d_workspace   device memory of at least pc_replay_workspace_bytes()

@@ -17,6 +17,10 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpcreplay.so")
+# the same library with per-request-phase cycle counters (see phase_counters)
+PHASES_LIB_PATH = os.path.join(_HERE, "libpcreplay_phases.so")
+PHASE_NAMES = ["request_start", "lookup", "reclamation", "charge", "insert_release", "accounting"]
+PHASE_EVENTS = ["evicting_requests", "log_compactions", "s3fifo_scan_batches", "prefixshield_queue_takes"]
 
 PC_OK, PC_EINVAL, PC_ENOMEM, PC_EDEVICE, PC_EUNSUPPORTED, PC_EINTERNAL = 0, -1, -2, -3, -4, -5
 PC_BLOCK_TOKENS = 16
@@ -70,9 +74,28 @@ class pc_instance_stats(ctypes.Structure):
 
 
 EXPORTS = ["pc_last_error", "pc_block_offsets", "pc_hash_blocks", "pc_replay_workspace_bytes",
-           "pc_replay_batch", "pc_get_stats"]
+           "pc_replay_state_bytes", "pc_replay_batch", "pc_get_stats"]
 
 _lib = None
+
+
+def use_phase_counters(on: bool = True):
+    """Select the phase-counter library (before the first call into the
+    library).  Its stats record of group 63 holds the counters instead of
+    group 63's own (instances must have at most 63 groups)."""
+    global LIB_PATH
+    if _lib is not None:
+        raise RuntimeError("the library is already loaded")
+    LIB_PATH = PHASES_LIB_PATH if on else os.path.join(_HERE, "libpcreplay.so")
+
+
+def phase_counters(groups) -> dict:
+    """Decode the counters from an instance's group records (phase build)."""
+    g = groups[63]
+    vals = [g[f] for f in GROUP_FIELDS]
+    out = {f"cycles_{n}": int(vals[i]) for i, n in enumerate(PHASE_NAMES)}
+    out.update({n: int(vals[8 + i]) for i, n in enumerate(PHASE_EVENTS)})
+    return out
 
 
 def lib():
@@ -93,6 +116,9 @@ def lib():
         L.pc_replay_workspace_bytes.restype = i64
         L.pc_replay_workspace_bytes.argtypes = [ctypes.POINTER(pc_trace_desc), i32,
                                                 ctypes.POINTER(pc_instance_desc), i32]
+        L.pc_replay_state_bytes.restype = i32
+        L.pc_replay_state_bytes.argtypes = [ctypes.POINTER(pc_trace_desc), i32, ctypes.POINTER(pc_instance_desc),
+                                            i32, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int32)]
         L.pc_replay_batch.restype = i32
         L.pc_replay_batch.argtypes = [ctypes.POINTER(pc_trace_desc), i32, ctypes.POINTER(pc_instance_desc),
                                       i32, P, i64, P, P, P]
@@ -154,6 +180,16 @@ def pc_replay_workspace_bytes(traces: Sequence[pc_trace_desc], instances: Sequen
     if v < 0:
         raise PCError(int(v), pc_last_error())
     return int(v)
+
+
+def pc_replay_state_bytes(traces: Sequence[pc_trace_desc], instances: Sequence[pc_instance_desc]):
+    """Per-instance state bytes and whether each instance keeps it in LDS."""
+    T, I = _descs(traces, instances)
+    n = len(instances)
+    b = (ctypes.c_int64 * max(n, 1))()
+    f = (ctypes.c_int32 * max(n, 1))()
+    _check(lib().pc_replay_state_bytes(T, len(traces), I, n, b, f))
+    return [int(b[i]) for i in range(n)], [bool(f[i]) for i in range(n)]
 
 
 def pc_replay_batch(traces, instances, workspace, stats, per_request=None, stream=None):

@@ -1,4 +1,6 @@
-"""Builds libpcreplay.so (the HIP library behind include/pc.h) for gfx950.
+"""Builds libpcreplay.so (the HIP library behind include/pc.h) for gfx950,
+and libpcreplay_phases.so, the same library with per-phase cycle counters
+(-DPC_PROFILE; the counters replace the stats record of group 63).
 
     python -m paper_2608_01657_amd.build
 """
@@ -14,6 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libpcreplay.so")
+LIB_PHASES = os.path.join(HERE, "libpcreplay_phases.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["pc_hash.hip", "pc_replay.hip", "pc_abi.cpp"]
@@ -32,14 +35,20 @@ def _hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
+    _build_one(LIB, BUILD_DIR, [], verbose)
+    _build_one(LIB_PHASES, os.path.join(BUILD_DIR, "phases"), ["-DPC_PROFILE"], verbose)
+    return LIB
+
+
+def _build_one(lib_path, build_dir, extra, verbose):
+    os.makedirs(build_dir, exist_ok=True)
     hipcc = _hipcc()
 
     def compile_one(src):
-        obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-        cmd = [hipcc, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
+        cmd = [hipcc, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
         if src.endswith(".cpp"):
-            cmd = [hipcc, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+            cmd = [hipcc, *FLAGS, *extra, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
@@ -49,13 +58,13 @@ def build(verbose: bool = False) -> str:
 
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(compile_one, SOURCES))
-    tmp = LIB + f".tmp{os.getpid()}"
+    tmp = lib_path + f".tmp{os.getpid()}"
     r = subprocess.run([hipcc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs],
                        capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":

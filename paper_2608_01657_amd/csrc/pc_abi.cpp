@@ -267,6 +267,19 @@ int64_t pc_replay_workspace_bytes(const pc_trace_desc *traces, int32_t n_traces,
     return P.ws_bytes;
 }
 
+int32_t pc_replay_state_bytes(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst,
+                              int32_t n_inst, int64_t *bytes_out, int32_t *in_lds_out) {
+    if (n_inst > 0 && (!bytes_out || !in_lds_out)) return fail(PC_EINVAL, "null output");
+    Plan P;
+    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_limit(), P);
+    if (rc != PC_OK) return rc;
+    for (int i = 0; i < n_inst; ++i) {
+        bytes_out[i] = P.di[i].state_bytes;
+        in_lds_out[i] = P.di[i].in_lds;
+    }
+    return ok();
+}
+
 int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst, int32_t n_inst,
                         void *d_workspace, int64_t workspace_bytes, void *d_stats, int32_t *d_per_request,
                         void *stream) {

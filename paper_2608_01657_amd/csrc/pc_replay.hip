@@ -224,9 +224,9 @@ struct Coll {
     uint32_t kval[kB];                // displacement scratch: entries
     uint32_t kmain[kB];               // 1 = main table, 0 = ghost table
 #ifdef PC_PROFILE
-    uint64_t prof[32];                // cycle counters (thread 0)
+    uint64_t prof[8];                 // cycles per request phase (thread 0)
     uint64_t prof_last;
-    uint64_t pcnt[16];                // event counters (thread 0)
+    uint64_t pcnt[8];                 // event counts (thread 0)
 #endif
 };
 
@@ -263,8 +263,14 @@ DEV uint32_t contract_of(uint32_t mt) { return (mt >> kContractShift) & 3u; }
 DEV uint32_t cls_of(uint32_t mt) { return (mt >> kClsShift) & 3u; }
 DEV uint32_t freq_of(uint32_t mt) { return (mt >> kFreqShift) & 3u; }
 
-// Optional per-phase cycle accounting (build with -DPC_PROFILE); the totals
-// land in the stats slot of group 63.  Nothing is skipped either way.
+// Optional per-phase cycle accounting (the phase-counter build, -DPC_PROFILE).
+// Thread 0 reads the shader clock at each phase boundary of a request:
+//   0 request start (descriptor checks, OnRequest)   1 lookup (+ prefetch)
+//   2 reclamation   3 charge   4 insert + release   5 accounting
+// and counts: 0 requests that evicted, 1 log compactions, 2 S3-FIFO scan
+// batches, 3 PrefixShield queue takes.  The totals replace the record of
+// group 63 in the stats.  The counters cost a few percent; nothing of the
+// replay itself is skipped or changed.
 // PROF_MARK(i) adds the cycles since the previous mark to counter i.
 #ifdef PC_PROFILE
 #define PROF_MARK(i)                                              \
@@ -683,7 +689,7 @@ struct Replayer {
     // Compaction of the free-queue log: live entries keep their order and
     // are renumbered from `head`; all cursors restart at `head`.
     DEV void compact() {
-        PROF_COUNT(2, 1);
+        PROF_COUNT(1, 1);
         bsync();
         uint32_t nw = head;
         for (uint32_t p0 = head; p0 < tail; p0 += kB) {
@@ -932,10 +938,8 @@ struct Replayer {
                 spS = curS; spM = curM;
                 keptS = keptM = 0xFFFFFFFFu;
             }
-            PROF_MARK(16);
             const bool useS = (s_size >= s_cap && s_unp > 0) || (m_unp == 0);
-            PROF_COUNT(0, 1);
-            PROF_COUNT(1, useS ? 1 : 0);
+            PROF_COUNT(2, 1);
             const uint32_t sp = useS ? spS : spM;
             const uint32_t lim = tail;
             if (sp >= lim) { err = kErrInternal; break; }
@@ -967,9 +971,7 @@ struct Replayer {
             }
             bool p3[3] = {cand, mv, inQ};
             BMask m3[3];
-            PROF_MARK(17);
             bballot<3>(p3, m3);
-            PROF_MARK(18);
             const BMask &candm = m3[0], &mvm = m3[1], &inQm = m3[2];
             const BMask evm = candm.andnot(mvm);
             // The batch is the longest prefix of candidates that may all be
@@ -1006,7 +1008,6 @@ struct Replayer {
                     stop = a.any() ? a.first() : kB;
                 }
             }
-            PROF_MARK(19);
             const bool proc = cand && tid < stop;
             const BMask pmm = mvm.below(stop), pem = evm.below(stop);
             const int nmv = pmm.count(), nev = pem.count();
@@ -1031,7 +1032,6 @@ struct Replayer {
             tail += (uint32_t)nmv;
             const bool pev = proc && !mv;
             const int erk = pem.rank(wid);
-            PROF_MARK(20);
             uint32_t gtouched = 0;
             if (useS) {
                 // ghost insertion of the evicted blocks, in eviction order;
@@ -1055,16 +1055,13 @@ struct Replayer {
                 m_unp -= nev;
                 s3_reins += (uint64_t)nmv;
             }
-            PROF_MARK(21);
             evict_elems(pev, sl, mt, erk, loc);
-            PROF_MARK(22);
             evicted(nev);
             rem -= nev;
             const uint32_t adv = stop < kB ? (uint32_t)stop : ((lim - sp) < (uint32_t)kB ? (lim - sp) : (uint32_t)kB);
             if (adv == 0) err = kErrInternal;   // a scan that cannot advance is a bug, never a hang
             if (useS) spS = sp + adv; else spM = sp + adv;
             bsync();
-            PROF_MARK(23);
             if (useS) {
                 if (gho && nev > 0) {
                     tclaim_reset(rset, hg, gtouched);
@@ -1155,12 +1152,10 @@ struct Replayer {
                     ++nhop;
                 }
             }
-            PROF_MARK(1);
             // resident lookup of every key (also of duplicates: harmless)
             uint32_t cand = 0;
             const int ntag = act ? tprobe(h, cand) : 0;
             bsync();
-            PROF_MARK(2);
             // duplicate: an earlier position holds the same key.  It was filed
             // along the same bucket sequence, no later than the first bucket
             // whose counter never passed 8 (no claim ever left that bucket).
@@ -1200,9 +1195,7 @@ struct Replayer {
             const bool inS = found && !(mt & kQMain);
             bool pa[5] = {nd && !found, found, dup, eligc, inS};
             BMask ma[5];
-            PROF_MARK(3);
             bballot<5>(pa, ma);
-            PROF_MARK(4);
             // a one-step request leaves the set empty entry by entry
             if (n <= kB && act) {
                 rset[rpos] = kEmpty;
@@ -1287,11 +1280,12 @@ struct Replayer {
         }
 
         // ---- reclamation (Alg. 2): truly free blocks first
-        PROF_MARK(5);
+        PROF_MARK(1);
         nvict = 0;
         gseq0 = gseq;
         int e = m - (C - resident);
         if (e < 0) e = 0;
+        PROF_COUNT(0, e > 0 ? 1 : 0);
         if (e > 0) {
             if constexpr (policy == kLRU) evict_lru(e);
             else if constexpr (policy == kPS) evict_ps(e, t);
@@ -1300,7 +1294,7 @@ struct Replayer {
         if (me) c_evc += (uint64_t)e;
 
         // ---- OnCacheFullBlocks: charge n_r = m (Eq. 2), class, admission
-        PROF_MARK(6);
+        PROF_MARK(2);
         uint32_t cls_new = kNormal;
         bool adm_now = adm;
         if (m > 0) {
@@ -1324,11 +1318,11 @@ struct Replayer {
         // ---- insert the new blocks (never-used slots first, then the
         //      victims' slots) and release every block of the request to the
         //      free queue, deepest first -- one pass over the positions
-        PROF_MARK(7);
+        PROF_MARK(3);
         const int nrel = n - ndup;
         if constexpr (policy == kS3) { if (m > 0) ensure_room((uint32_t)m); }
         else if (nrel > 0) ensure_room((uint32_t)nrel);
-        PROF_MARK(8);
+        PROF_MARK(4);
         const uint32_t mbase = ((uint32_t)g) | ((uint32_t)c << kContractShift) | (cls_new << kClsShift) | kRes;
         const int nfresh = C - hwm;
         int nalloc = 0, seen = 0, seen_new = 0;
@@ -1354,7 +1348,6 @@ struct Replayer {
             bool pa[4] = {isN, rl, isNew, rl && !isNew && (mt & kQMain) != 0};
             BMask ma[4];
             bballot<4>(pa, ma);
-            PROF_MARK(9);
             touched = 0;
             if (isN) {
                 const int i = nalloc + ma[0].rank(wid);
@@ -1364,12 +1357,10 @@ struct Replayer {
                 if (!tclaim(table, rset, val, hh, e, touched)) defer_kick(val, kk, true);
             }
             nalloc += ma[0].count();
-            PROF_MARK(10);
             if (isNew) {
                 mt = mbase;
                 if constexpr (policy == kPS) pfx[slot] = p;
             }
-            PROF_MARK(14);
             if constexpr (policy == kS3) {
                 // new blocks enter the ghost-selected queue in deepest-first
                 // order; hits stay where they are; everything is unpinned
@@ -1397,10 +1388,8 @@ struct Replayer {
                 meta[slot] = (mt & ~kPin) | kInLog | kRes;
             }
             if constexpr (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), rl, 1);
-            PROF_MARK(15);
             seen += ma[1].count();
             seen_new += ma[2].count();
-            PROF_MARK(11);
             if (base + kB < n) {   // another step follows: place displaced entries first
                 bsync();
                 tclaim_reset(rset, hh, touched);
@@ -1426,7 +1415,7 @@ struct Replayer {
             s_unp += m - ng;   // new blocks are unpinned right away
             m_unp += ng;
         }
-        PROF_MARK(12);
+        PROF_MARK(4);
 
         // ---- accounting for every group
         if (lane < G) {
@@ -1451,7 +1440,7 @@ struct Replayer {
             X.qf = ((nref & nb) ? 1u : 0u) | ((nadm & nb) ? 2u : 0u);
         }
         bsync();   // X.qf and all state of this request are visible
-        PROF_MARK(13);
+        PROF_MARK(5);
         return true;
     }
 
@@ -1494,8 +1483,7 @@ struct Replayer {
         r_max = 0;
         last_h = last_m = last_e = last_o = 0;
 #ifdef PC_PROFILE
-        if (tid < 32) X.prof[tid] = 0;
-        if (tid < 16) X.pcnt[tid] = 0;
+        if (tid < 8) { X.prof[tid] = 0; X.pcnt[tid] = 0; }
         if (tid == 0) X.prof_last = __builtin_amdgcn_s_memtime();
 #endif
         gsync();
@@ -1568,9 +1556,10 @@ struct Replayer {
             qq[7] = (int64_t)(uint32_t)status;   // status in the low 32 bits
         }
 #ifdef PC_PROFILE
-        if (lane < 16) st[63 * kGroupFields + lane] = (int64_t)X.prof[lane];
-        if (lane < 16) st[61 * kGroupFields + lane] = (int64_t)X.prof[16 + lane];
-        if (lane < 16) st[62 * kGroupFields + lane] = (int64_t)X.pcnt[lane];
+        // phase build: the record of group 63 carries the 6 phase cycle
+        // totals, then (fields 8-11) the event counts
+        if (G < 64 && lane < 6) st[63 * kGroupFields + lane] = (int64_t)X.prof[lane];
+        if (G < 64 && lane < 4) st[63 * kGroupFields + 8 + lane] = (int64_t)X.pcnt[lane];
 #endif
     }
 };

@@ -9,7 +9,7 @@ from typing import List, Optional, Sequence
 import numpy as np
 import torch
 
-from . import (make_instance_desc, make_trace_desc, pc_block_offsets, pc_get_stats, pc_hash_blocks,
+from . import (make_instance_desc, phase_counters, make_trace_desc, pc_block_offsets, pc_get_stats, pc_hash_blocks,
                pc_replay_batch, pc_replay_workspace_bytes, stats_to_dicts, PC_STATS_RECORD_BYTES)
 
 
@@ -146,6 +146,13 @@ class ReplayBatch:
         G, S = pc_get_stats(self.stats, len(self.instances), -1, 64, stream)
         ng = [self.dtraces[i.trace].n_groups for i in self.instances]
         return stats_to_dicts(G, S, ng)
+
+    def phase_counters(self, stream=None) -> List[dict]:
+        """Per-instance phase cycles and event counts (phase-counter library
+        only; see paper_2608_01657_amd.use_phase_counters)."""
+        G, S = pc_get_stats(self.stats, len(self.instances), -1, 64, stream)
+        full = stats_to_dicts(G, S, [64] * len(self.instances))
+        return [phase_counters(groups) for groups, _, _ in full]
 
     def per_request_arrays(self) -> List[np.ndarray]:
         assert self.per_request is not None

@@ -292,6 +292,25 @@ def attack_trace(kind: str, seed: int = 7000, n_requests: int = 4000) -> Trace:
                    2, 4 + max(n_unique, 1), {0: "victim", 1: "polluter"})
 
 
+def selector_trace(n_groups: int, seed: int = 8000, n_requests: int = 20000) -> Trace:
+    """Reclamation under contention from many groups: every request is a
+    fresh prompt of lognormal(6.2, 0.5) tokens clipped to [128, 2048] (about
+    31 blocks) from group g with probability proportional to g + 1, so every
+    group is in debt by a different amount and, once the cache is full,
+    every request needs a reclamation batch (the setting of the paper's
+    selector-latency measurement, Sec. V-D)."""
+    rng = _rng(seed)
+    w = np.arange(1, n_groups + 1, dtype=np.float64)
+    groups_ = rng.choice(n_groups, size=n_requests, p=w / w.sum())
+    L_ = _lognormal_len(rng, 6.2, 0.5, n_requests, lo=128, hi=2048)
+    st = _Stream(rng)
+    offs, lens, groups, prefixes = [], [], [], []
+    for r in range(n_requests):
+        L = int(L_[r])
+        offs.append(st.append(st.fresh(L))); lens.append(L); groups.append(int(groups_[r])); prefixes.append(r)
+    return _finish(f"selector_g{n_groups}_s{seed}", st, offs, lens, groups, prefixes, n_groups, n_requests, {})
+
+
 def delayed_replay(seed: int = 4000, n_requests: int = 200000) -> Trace:
     """8 groups: 6 benign (8 private 2048-token prefixes, Zipf 1.1, +128
     fresh tokens), a victim (as in the one-touch workload) and a polluter.
@@ -479,6 +498,10 @@ def workload(name: str, seeds: Optional[Sequence[int]] = None,
                   C=511, 4,000 requests, 10 seeds x {LRU, S3-FIFO,
                   PrefixShield, PrefixShield without segmentation, without
                   the debt gate} -> 50
+    selector512x8, selector4096x32
+                  one-touch contention from 8 / 32 groups at C = 512 / 4096
+                  (the paper's selector measurement sizes), 20,000
+                  requests, 4 seeds, 3 policies
     chat_bursty   chat traces whose requests arrive in bursts of 32 per tick
                   (the accounting clock of Eq. 1 advances 32 ticks between
                   bursts), C=4096, 3 policies
@@ -542,6 +565,13 @@ def workload(name: str, seeds: Optional[Sequence[int]] = None,
                                      label="prefixshield_noseg"))
                 inst.append(Instance(t, POLICY_PREFIXSHIELD, 511, flags=FLAG_NO_DEBT_GATE,
                                      label="prefixshield_nogate"))
+    elif name in ("selector512x8", "selector4096x32"):
+        C, G = (512, 8) if name == "selector512x8" else (4096, 32)
+        idx = list(seeds) if seeds is not None else list(range(4))
+        for i in idx:
+            traces.append(selector_trace(G, 8000 + i, n_requests or 20000))
+            for pol in policies:
+                inst.append(Instance(len(traces) - 1, pol, C, label=POLICY_NAMES[pol]))
     elif name == "chat_bursty":
         idx = list(seeds) if seeds is not None else list(range(8))
         for i in idx:

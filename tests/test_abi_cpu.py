@@ -134,3 +134,22 @@ def test_product_path_has_no_fallback(monkeypatch):
     monkeypatch.setattr(P, "_lib", None)
     with pytest.raises(RuntimeError, match="no CPU fallback"):
         P.pc_last_error()
+
+
+def test_state_bytes_on_the_host():
+    """Per-instance state size: grows with capacity, the S3-FIFO ghost table
+    and PrefixShield's per-block prefix ids add to it, and C = 16384 does not
+    fit the 64 KiB the planner assumes without a device."""
+    T = [_trace()]
+    I = [_inst(policy=0, capacity=512), _inst(policy=0, capacity=4096), _inst(policy=1, capacity=4096),
+         _inst(policy=2, capacity=4096), _inst(policy=2, capacity=16384)]
+    b, lds = P.pc_replay_state_bytes(T, I)
+    assert b[0] < b[1] < b[3] and b[1] < b[2]
+    assert b[1] >= 4096 * (8 + 4 + 4)          # key, stamp, meta per block at least
+    assert b[3] - b[1] >= 4096 * 4             # prefix id per block
+    assert not lds[4]
+    lib = P.lib()
+    bad = (P.pc_instance_desc * 1)(_inst(capacity=0))
+    out_b = (ctypes.c_int64 * 1)()
+    out_f = (ctypes.c_int32 * 1)()
+    assert lib.pc_replay_state_bytes((P.pc_trace_desc * 1)(_trace()), 1, bad, 1, out_b, out_f) == P.PC_EINVAL

@@ -157,3 +157,51 @@ def test_chat_bursty_ticks_full_length():
     assert traces[0].n_req == 100000 and traces[0].tick is not None
     dts, okeys = _hash_all(traces)
     _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))
+
+
+def test_selector_contention_all_instances():
+    """Every request reclaims under contention from 8 / 32 indebted groups
+    (the selector measurement sizes), full length, all instances."""
+    for name in ("selector512x8", "selector4096x32"):
+        traces, insts = tg.workload(name, seeds=[0])
+        assert traces[0].n_req == 20000
+        dts, okeys = _hash_all(traces)
+        _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))
+
+
+PHASE_CHILD = r"""
+import json, sys, numpy as np
+sys.path.insert(0, sys.argv[1]); sys.path.insert(0, sys.argv[1] + "/tests")
+import paper_2608_01657_amd as P
+P.use_phase_counters()
+import oracle
+from gpu_util import assert_same
+from paper_2608_01657_amd import device as dv, tracegen as tg
+traces, insts = tg.workload("selector512x8", seeds=[0], n_requests=3000)
+t = dv.upload(traces[0]); dv.cut_and_hash(t)
+b = dv.ReplayBatch([t], insts, per_request=True); b.launch()
+res = b.results(); pr = b.per_request_arrays(); pcs = b.phase_counters()
+k, off = oracle.hash_trace(traces[0])
+out = []
+for i, spec in enumerate(insts):
+    o = oracle.replay_trace(traces[0], k, off, spec, per_request=True)
+    assert_same(res[i], o, spec.label)
+    assert np.array_equal(pr[i], o.per_request)
+    assert pcs[i]["evicting_requests"] == int((o.per_request[:, 2] > 0).sum())
+    assert all(pcs[i]["cycles_" + n] > 0 for n in P.PHASE_NAMES if n != "reclamation")
+    out.append(pcs[i])
+print(json.dumps(out))
+"""
+
+
+def test_phase_counter_library_replays_identically():
+    """The phase-counter build changes no result, and its event counts agree
+    with the per-request outputs (requests that evicted)."""
+    import json
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", PHASE_CHILD, root], capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stderr[-3000:]
+    pcs = json.loads(r.stdout.strip().splitlines()[-1])
+    assert len(pcs) == 3

@@ -522,26 +522,9 @@ struct Replayer {
             if ((e[i] >> 16) == h.tag && key[e[i] & 0xFFFFu] == k) return (int)(e[i] & 0xFFFFu);
         return -1;
     }
-    // clear the entry holding exactly `val` (if present)
-    DEV void tclear_exact(uint32_t *tb, uint32_t val, const TH &h) {
-        uint32_t e[16];
-        load_buckets(tb, h, e);
-        int at = -1;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) at = (at < 0 && e[i] == val) ? i : at;
-        if (at >= 0) tb[epos(h, at)] = kEmpty;
-    }
-    // Parallel insert without compare-and-swap.  Every inserter of a step
-    // reads its two buckets (e, the snapshot) before a barrier that no table
-    // write crosses; after it, a claim counter per bucket (ctr[b], kEmpty
-    // meaning zero) hands out distinct ranks, and rank r takes the r-th empty
-    // entry of the snapshot -- the emptier bucket first.  `touched` records
-    // the counters used, which tclaim_reset puts back to kEmpty after the
-    // next barrier.  False when both buckets are full.
-    // For the ghost table (gref != 0) an entry that left the window counts
-    // as empty (see glive).
-    // Free-entry masks of both buckets of a snapshot: bits 0-7 bucket b1,
-    // bits 8-15 bucket b2.
+    // Free-entry mask of both buckets of a snapshot (bits 0-7 bucket b1,
+    // bits 8-15 bucket b2).  In the ghost table an entry that left the
+    // window counts as free (see glive).
     DEV uint32_t free_mask(const uint32_t (&e)[16], bool ghost, uint32_t gref) const {
         uint32_t m = 0;
 #pragma unroll
@@ -551,6 +534,13 @@ struct Replayer {
         }
         return m;
     }
+    // Parallel insert without compare-and-swap.  Every inserter of a step
+    // reads its two buckets (the snapshot) before a barrier that no table
+    // write crosses; after it, a claim counter per bucket (ctr[b], kEmpty
+    // meaning zero) hands out distinct ranks, and rank r takes the r-th free
+    // entry of the snapshot -- the emptier bucket first.  `touched` records
+    // the counters used, which tclaim_reset puts back to kEmpty after the
+    // next barrier.  False when both buckets are full.
     DEV bool tclaim(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, const uint32_t (&e)[16],
                     uint32_t &touched, bool ghost = false, uint32_t gref = 0) {
         return tclaim_m(tb, ctr, val, h, free_mask(e, ghost, gref), touched);
@@ -757,7 +747,10 @@ struct Replayer {
     // s < 0: any class (no segmentation).
     DEV void ps_take(int x, int s, int ci, int k) {
         PROF_COUNT(3, 1);
+        // every live entry sits at or above head; a cursor left behind by an
+        // idle queue skips the dead stretch below it
         uint32_t c = rfl(cur[ci]);
+        if (c < head) c = head;
         int rem = k;
         while (rem > 0 && err == 0) {
             const uint32_t pos = c + tid;
@@ -789,6 +782,7 @@ struct Replayer {
     DEV uint32_t ps_headpos(int x, int s) {
         const int ci = 3 * x + (s < 0 ? 0 : s);
         uint32_t c = rfl(cur[ci]);
+        if (c < head) c = head;
         uint32_t found = 0xFFFFFFFFu;
         while (c < tail) {
             const uint32_t pos = c + tid;

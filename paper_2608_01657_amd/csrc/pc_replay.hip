@@ -501,18 +501,25 @@ struct Replayer {
     // Probe both buckets of k.  Returns the number of tag matches; `cand` is
     // the slot of the last one.  With one match the caller confirms the key
     // (together with its other loads); with several, tfind_slow decides.
-    DEV int tprobe(const TH &h, uint32_t &cand) const {
+    // `fm` receives the free-entry mask of the two buckets (bits 0-7 b1,
+    // 8-15 b2): the lookup's snapshot of the table, which a one-step
+    // request inserts with (the table does not change between the lookup
+    // and the insertion except for reclamation's clears, which only free
+    // entries).
+    DEV int tprobe(const TH &h, uint32_t &cand, uint32_t &fm) const {
         uint32_t e[16];
         load_buckets(table, h, e);
         int nm = 0;
-        uint32_t cv = 0;
+        uint32_t cv = 0, f = 0;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
             const bool mt = (e[i] >> 16) == h.tag;
             nm += mt;
             cv = mt ? e[i] : cv;
+            f |= (e[i] == kEmpty ? 1u : 0u) << i;
         }
         cand = cv & 0xFFFFu;
+        fm = f;
         return nm;
     }
     DEV int tfind_slow(uint64_t k, const TH &h) const {
@@ -1122,6 +1129,14 @@ struct Replayer {
         PROF_MARK(0);
         int hend = n, nhit = 0, nnew = 0, ndup = 0, norph = 0;
         int npromo = 0, ngated = 0;
+        // a one-step request (n <= kB) carries each position's outcome from
+        // the lookup to the insertion in registers: no second pass, no
+        // second ballot, and the lookup's bucket snapshot serves the insert
+        uint64_t c_key = 0;
+        TH c_h = {};
+        uint32_t c_slot = kNoSlot, c_mt = 0, c_fm = 0;
+        bool c_isN = false, c_rl = false, c_new = false;
+        int c_rkN = 0, c_rkRl = 0, c_rkNew = 0, c_nmiss = 0, c_hitS = 0, c_hitM = 0;
         uint64_t kcur = kn;
         for (int base = 0; base < n; base += kB) {
             const int j = base + tid;
@@ -1147,8 +1162,8 @@ struct Replayer {
                 }
             }
             // resident lookup of every key (also of duplicates: harmless)
-            uint32_t cand = 0;
-            const int ntag = act ? tprobe(h, cand) : 0;
+            uint32_t cand = 0, fm = 0;
+            const int ntag = act ? tprobe(h, cand, fm) : 0;
             bsync();
             // duplicate: an earlier position holds the same key.  It was filed
             // along the same bucket sequence, no later than the first bucket
@@ -1209,8 +1224,8 @@ struct Replayer {
             // their owner's resident count
             if constexpr (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), found, -1);
             wave_add(res, owner_of(mt), isOrph, -1);
+            uint32_t m2 = mt | kPin;
             if (isHit) {   // pin; touch
-                uint32_t m2 = mt | kPin;
                 if constexpr (policy == kS3) {
                     const uint32_t f = freq_of(mt);
                     m2 = (m2 & ~(3u << kFreqShift)) | ((f < 3 ? f + 1 : 3u) << kFreqShift);
@@ -1224,7 +1239,23 @@ struct Replayer {
             // orphans: the old block leaves; its slot and table entry are
             // reused by the new block of the same key
             if (isOrph) meta[slot] = kPin;
-            if (act) posslot[j] = dup ? kNoSlot : (found ? (uint16_t)slot : kNewMark);
+            if (n > kB) {
+                if (act) posslot[j] = dup ? kNoSlot : (found ? (uint16_t)slot : kNewMark);
+            } else {
+                c_key = k;
+                c_h = h;
+                c_fm = fm;
+                c_slot = dup ? kNoSlot : (found ? slot : (uint32_t)kNewMark);
+                c_mt = m2;
+                c_isN = nd && !found;
+                c_rl = nd;
+                c_new = nd && tid >= lim;
+                c_rkN = ma[0].rank(wid);
+                c_rkRl = tid - ma[2].rank(wid);
+                // non-duplicate positions below the first miss are hits
+                c_rkNew = c_rkRl - (lim - ma[2].below(lim).count());
+                c_nmiss = ma[0].count();
+            }
             const BMask hitm = ma[1].below(lim);
             const int nh = hitm.count(), nf = ma[1].count(), no = nf - nh;
             const int ne = ma[3].below(lim).count();
@@ -1240,6 +1271,8 @@ struct Replayer {
                 m_unp -= (nh - hs) + (no - os);
                 s_size -= os;
             }
+            c_hitS = hs;
+            c_hitM = nh - hs;
         }
         if (n > kB) {   // longer requests clear the whole set (read by all steps)
             for (uint32_t i = tid; i <= rsmask; i += kB) rset[i] = kEmpty;
@@ -1323,7 +1356,48 @@ struct Replayer {
         if (tid == 0) X.nghost = 0;
         TH hh = {};
         uint32_t touched = 0;
-        for (int base = 0; base < n; base += kB) {
+        if (n <= kB && n > 0) {
+            // one step, from the lookup's registers
+            uint32_t slot = c_slot;
+            if (c_isN) {
+                const int i = c_rkN;
+                slot = i < nfresh ? (uint32_t)(hwm + i) : vlist[i - nfresh];
+                key[slot] = c_key;
+                hh = c_h;
+                const uint32_t val = (hh.tag << 16) | slot;
+                if (!tclaim_m(table, rset, val, hh, c_fm, touched)) defer_kick(val, c_key, true);
+            }
+            nalloc = c_nmiss;
+            const uint32_t mt = c_new ? mbase : c_mt;
+            if constexpr (policy == kPS) {
+                if (c_new) pfx[slot] = p;
+            }
+            if constexpr (policy == kS3) {
+                bool gh = false;
+                if (c_new && g_cap > 0) gh = ghost_take(c_key);
+                {
+                    const uint64_t gm = ballot(gh);
+                    if (lane == 0 && gm) atomicAdd(&X.nghost, (uint32_t)popc(gm));
+                }
+                if (c_new) {
+                    const uint32_t np = tail + (uint32_t)(m - 1 - c_rkNew);
+                    log[np & lmask] = (uint16_t)slot;
+                    stamp[slot] = np;
+                    meta[slot] = mt | kInLog | (gh ? kQMain : 0u);
+                } else if (c_rl) {
+                    meta[slot] = mt & ~kPin;
+                }
+                s_unp += c_hitS;   // hits are unpinned where they are
+                m_unp += c_hitM;
+            } else if (c_rl) {
+                const uint32_t np = tail + (uint32_t)(nrel - 1 - c_rkRl);
+                log[np & lmask] = (uint16_t)slot;
+                stamp[slot] = np;
+                meta[slot] = (mt & ~kPin) | kInLog | kRes;
+            }
+            if constexpr (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), c_rl, 1);
+        }
+        for (int base = 0; n > kB && base < n; base += kB) {
             const int j = base + tid;
             const bool act = j < n;
             uint32_t slot = act ? posslot[j] : kNoSlot;

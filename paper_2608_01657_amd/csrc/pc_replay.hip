@@ -1251,10 +1251,14 @@ struct Replayer {
                 c_rl = nd;
                 c_new = nd && tid >= lim;
                 c_rkN = ma[0].rank(wid);
-                c_rkRl = tid - ma[2].rank(wid);
-                // non-duplicate positions below the first miss are hits
-                c_rkNew = c_rkRl - (lim - ma[2].below(lim).count());
                 c_nmiss = ma[0].count();
+                if constexpr (policy == kS3) {
+                    // new blocks: non-duplicates at or after the first miss
+                    // (the non-duplicates below it are hits)
+                    c_rkNew = tid - ma[2].rank(wid) - (lim - ma[2].below(lim).count());
+                } else {
+                    c_rkRl = tid - ma[2].rank(wid);
+                }
             }
             const BMask hitm = ma[1].below(lim);
             const int nh = hitm.count(), nf = ma[1].count(), no = nf - nh;

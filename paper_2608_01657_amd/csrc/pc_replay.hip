@@ -1202,9 +1202,17 @@ struct Replayer {
             const bool eligc = policy == kPS && found && proven && (int)owner_of(mt) == g &&
                                (int)contract_of(mt) == c && cls_of(mt) != (uint32_t)kReuse && cpx == p;
             const bool inS = found && !(mt & kQMain);
-            bool pa[5] = {nd && !found, found, dup, eligc, inS};
-            BMask ma[5];
-            bballot<5>(pa, ma);
+            // block-wide masks: misses, found, duplicates, and the policy's
+            // fourth (PrefixShield: promotion-eligible; S3-FIFO: in S)
+            constexpr int kM = policy == kLRU ? 3 : 4;
+            bool pa[kM];
+            pa[0] = nd && !found;
+            pa[1] = found;
+            pa[2] = dup;
+            if constexpr (policy == kPS) pa[kM - 1] = eligc;
+            if constexpr (policy == kS3) pa[kM - 1] = inS;
+            BMask ma[kM];
+            bballot<kM>(pa, ma);
             // a one-step request leaves the set empty entry by entry
             if (n <= kB && act) {
                 rset[rpos] = kEmpty;
@@ -1262,8 +1270,12 @@ struct Replayer {
             }
             const BMask hitm = ma[1].below(lim);
             const int nh = hitm.count(), nf = ma[1].count(), no = nf - nh;
-            const int ne = ma[3].below(lim).count();
-            const int hs = ma[4].below(lim).count(), os = ma[4].count() - hs;
+            int ne = 0, hs = 0, os = 0;
+            if constexpr (policy == kPS) ne = ma[kM - 1].below(lim).count();
+            if constexpr (policy == kS3) {
+                hs = ma[kM - 1].below(lim).count();
+                os = ma[kM - 1].count() - hs;
+            }
             nhit += nh;
             norph += no;
             nnew += (nf - nh) + ma[0].count();

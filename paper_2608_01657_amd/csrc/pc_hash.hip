@@ -34,8 +34,16 @@ constexpr uint64_t pow_a(int e) {
     }
     return r;
 }
-constexpr uint64_t kA1 = pow_a(1), kA2 = pow_a(2), kA4 = pow_a(4), kA8 = pow_a(8),
-                   kA16 = pow_a(16), kA32 = pow_a(32);
+constexpr uint64_t kA1 = pow_a(1), kA2 = pow_a(2), kA4 = pow_a(4), kA8 = pow_a(8);
+
+// A^0 .. A^32: the per-lane multipliers of the scan's cross-row steps
+__constant__ uint64_t kApow[33] = {
+    pow_a(0),  pow_a(1),  pow_a(2),  pow_a(3),  pow_a(4),  pow_a(5),  pow_a(6),  pow_a(7),  pow_a(8),
+    pow_a(9),  pow_a(10), pow_a(11), pow_a(12), pow_a(13), pow_a(14), pow_a(15), pow_a(16), pow_a(17),
+    pow_a(18), pow_a(19), pow_a(20), pow_a(21), pow_a(22), pow_a(23), pow_a(24), pow_a(25), pow_a(26),
+    pow_a(27), pow_a(28), pow_a(29), pow_a(30), pow_a(31), pow_a(32)};
+
+#define GLOBAL __attribute__((address_space(1)))
 
 __device__ __forceinline__ uint64_t fmix64(uint64_t z) {
     z ^= z >> 33;
@@ -69,15 +77,14 @@ __device__ __forceinline__ uint64_t quad_add(uint64_t x) {
     return x + (((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
-// 4 int32 starting at element e of `base` (16-byte aligned), zero beyond lim
-__device__ __forceinline__ uint4 load4(const int32_t *__restrict__ base, int64_t e, int64_t lim) {
-    if (e + 4 <= lim) return *reinterpret_cast<const uint4 *>(base + e);
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (e < lim) v.x = (uint32_t)base[e];
-    if (e + 1 < lim) v.y = (uint32_t)base[e + 1];
-    if (e + 2 < lim) v.z = (uint32_t)base[e + 2];
-    if (e + 3 < lim) v.w = (uint32_t)base[e + 3];
-    return v;
+// DPP move of a 64-bit value: lane L receives the source lane kCtrl names
+// (row_shr:n = 0x110+n, row_bcast:15 = 0x142, row_bcast:31 = 0x143); lanes
+// with no source, and rows outside kRowMask, receive 0.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint64_t dpp64(uint64_t x) {
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, kCtrl, kRowMask, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), kCtrl, kRowMask, 0xF, false);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
 }
 
 // ---------------------------------------------------------------- offsets
@@ -173,13 +180,97 @@ __global__ __launch_bounds__(kScanThreads) void offsets_fill(const int32_t *__re
 // ---------------------------------------------------------------- keys
 constexpr int kHashWaves = 4;
 
+// Token loads of one 64-block step: lane 4*bq + r4 holds, for q = 0..3,
+// tokens [4*r4, 4*r4 + 4) of block 16q + bq of the step.  The loads are
+// 16 bytes at 4-byte alignment (a request may start at any token).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+struct Step {
+    u32x4 v[4];
+};
+
+// Issue every load of the step starting at block `it` before any of them is
+// used.  Lanes past the request's last block re-read that block (same cache
+// lines, no extra DRAM traffic), so no load sits under a branch and every
+// address lies inside the request.
+__device__ __forceinline__ void issue(Step &S, const GLOBAL int32_t *__restrict__ tok, int32_t it, int32_t nb,
+                                      int bq, int r4) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        int32_t blk = it + 16 * q + bq;
+        blk = blk < nb ? blk : nb - 1;
+        // byte offset < 2^31: a request holds fewer than 2^31 tokens
+        const uint32_t byte = (uint32_t)blk * 64u + (uint32_t)r4 * 16u;
+        S.v[q] = *reinterpret_cast<const GLOBAL u32x4_a4 *>(reinterpret_cast<const GLOBAL uint8_t *>(tok) + byte);
+    }
+}
+
+// Keys of one 64-block step from its loaded tokens; H carries H_{k-1} of
+// the step's first block in and the last block's H_k out.
+__device__ __forceinline__ void step_keys(const Step &S, int nblk, int lane, int r4, uint32_t k0, uint32_t k1,
+                                          uint32_t k2, uint32_t k3, int src, uint64_t arow, uint64_t a31,
+                                          uint64_t &H, GLOBAL uint64_t *__restrict__ out) {
+    uint64_t dsel = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint32_t t0 = S.v[q].x, t1 = S.v[q].y, t2 = S.v[q].z, t3 = S.v[q].w;
+        uint64_t part = (uint64_t)(t0 + k0) * (uint64_t)(t1 + k1) + (uint64_t)(t2 + k2) * (uint64_t)(t3 + k3);
+        part = quad_add<0xB1>(part);   // quad_perm [1,0,3,2]
+        part = quad_add<0x4E>(part);   // quad_perm [2,3,0,1]
+        if (q == r4) dsel = part;      // lane 4b+q keeps block 16q+b
+    }
+    const uint64_t c = fmix64(dsel);
+    uint64_t v = shfl64(c, src);       // lane L now holds c of block L of the step
+    if (lane == 0) v += kA1 * H;
+    // inclusive scan of H_L = A*H_{L-1} + c_L over the 64 lanes: within each
+    // row of 16 lanes (v_L += A^d v_{L-d}), then rows 1 and 3 take the last
+    // lane of the row before them, then rows 2 and 3 take lane 31
+    v += kA1 * dpp64<0x111, 0xF>(v);
+    v += kA2 * dpp64<0x112, 0xF>(v);
+    v += kA4 * dpp64<0x114, 0xF>(v);
+    v += kA8 * dpp64<0x118, 0xF>(v);
+    v += arow * dpp64<0x142, 0xA>(v);
+    v += a31 * dpp64<0x143, 0xC>(v);
+    H = readlane64(v, nblk - 1);
+    // every lane stores (no branch, so the compiler can count the loads in
+    // flight exactly): lanes past the last block write the last block's key
+    // again, the same value to the same address
+    out[lane < nblk ? lane : nblk - 1] = fmix64(lane < nblk ? v : H);
+}
+
+// All keys of one request, two steps in flight: the loads of step s+1 are
+// issued before step s is computed (two buffers, so no register copy has
+// to wait for a load).
+__device__ __forceinline__ void hash_request(const GLOBAL int32_t *__restrict__ tok, int32_t nb, uint64_t H,
+                                             GLOBAL uint64_t *__restrict__ out, int lane) {
+    const int r4 = lane & 3, bq = lane >> 2;
+    const uint32_t k0 = kNH[4 * r4], k1 = kNH[4 * r4 + 1], k2 = kNH[4 * r4 + 2], k3 = kNH[4 * r4 + 3];
+    const int src = 4 * (lane & 15) + (lane >> 4);      // lane holding block `lane`'s digest
+    const uint64_t arow = kApow[(lane & 15) + 1];       // A^(position in row + 1)
+    const uint64_t a31 = kApow[lane >= 32 ? lane - 31 : 0];
+    Step S0, S1;
+    issue(S0, tok, 0, nb, bq, r4);
+    for (int32_t it = 0;;) {
+        issue(S1, tok, it + 64, nb, bq, r4);
+        step_keys(S0, nb - it < 64 ? nb - it : 64, lane, r4, k0, k1, k2, k3, src, arow, a31, H, out + it);
+        it += 64;
+        if (it >= nb) break;
+        issue(S0, tok, it + 64, nb, bq, r4);
+        step_keys(S1, nb - it < 64 ? nb - it : 64, lane, r4, k0, k1, k2, k3, src, arow, a31, H, out + it);
+        it += 64;
+        if (it >= nb) break;
+    }
+}
+
 __global__ __launch_bounds__(64 * kHashWaves) void hash_kernel(
     const int32_t *__restrict__ tokens, int64_t n_tokens, const int64_t *__restrict__ tok_off,
     const int32_t *__restrict__ req_len, const int32_t *__restrict__ req_ns,
     const int64_t *__restrict__ key_off, int64_t n_req, uint64_t *__restrict__ keys, int64_t n_keys,
     int32_t *__restrict__ status) {
     const int lane = threadIdx.x & 63;
-    const int64_t r = (int64_t)blockIdx.x * kHashWaves + (threadIdx.x >> 6);
+    // one request per wavefront (wave-uniform, so the descriptor is read
+    // with scalar loads)
+    const int64_t r = (int64_t)blockIdx.x * kHashWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (r >= n_req) return;
     const int64_t off = tok_off[r];
     const int32_t len = req_len[r];
@@ -190,52 +281,8 @@ __global__ __launch_bounds__(64 * kHashWaves) void hash_kernel(
         return;
     }
     if (nb == 0) return;
-    const int a = (int)(off & 3);                       // misalignment (wave-uniform)
-    const int32_t *base = tokens + (off - a);           // 16-byte aligned
-    const int64_t lim = n_tokens - (off - a);
-    const int r4 = lane & 3, bq = lane >> 2;
-    const uint32_t k0 = kNH[4 * r4], k1 = kNH[4 * r4 + 1], k2 = kNH[4 * r4 + 2], k3 = kNH[4 * r4 + 3];
-    uint64_t H = fmix64((uint64_t)(uint32_t)req_ns[r] + 1u);
-    const int src = 4 * (lane & 15) + (lane >> 4);      // lane holding block `lane`'s digest
-
-    for (int64_t it = 0; it < nb; it += 64) {
-        const int nblk = (int)((nb - it) < 64 ? (nb - it) : 64);
-        uint64_t dsel = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int blk = 16 * q + bq;                 // block within this 64-block step
-            uint64_t part = 0;
-            if (blk < nblk) {
-                const int64_t e = 16 * (it + blk) + 4 * r4;   // aligned element index
-                uint4 v = load4(base, e, lim);
-                uint32_t t0, t1, t2, t3;
-                if (a == 0) {
-                    t0 = v.x; t1 = v.y; t2 = v.z; t3 = v.w;
-                } else {
-                    uint4 w = load4(base, e + 4, lim);
-                    if (a == 1) { t0 = v.y; t1 = v.z; t2 = v.w; t3 = w.x; }
-                    else if (a == 2) { t0 = v.z; t1 = v.w; t2 = w.x; t3 = w.y; }
-                    else { t0 = v.w; t1 = w.x; t2 = w.y; t3 = w.z; }
-                }
-                part = (uint64_t)(t0 + k0) * (uint64_t)(t1 + k1) + (uint64_t)(t2 + k2) * (uint64_t)(t3 + k3);
-            }
-            part = quad_add<0xB1>(part);   // quad_perm [1,0,3,2]
-            part = quad_add<0x4E>(part);   // quad_perm [2,3,0,1]
-            if (q == r4) dsel = part;      // lane 4b+q keeps block 16q+b
-        }
-        const uint64_t c = fmix64(dsel);
-        uint64_t v = shfl64(c, src);       // lane L now holds c of block it+L
-        if (lane == 0) v += kA1 * H;
-        uint64_t u;
-        u = shfl_up64(v, 1);  if (lane >= 1)  v += kA1 * u;
-        u = shfl_up64(v, 2);  if (lane >= 2)  v += kA2 * u;
-        u = shfl_up64(v, 4);  if (lane >= 4)  v += kA4 * u;
-        u = shfl_up64(v, 8);  if (lane >= 8)  v += kA8 * u;
-        u = shfl_up64(v, 16); if (lane >= 16) v += kA16 * u;
-        u = shfl_up64(v, 32); if (lane >= 32) v += kA32 * u;
-        if (lane < nblk) keys[ko + it + lane] = fmix64(v);
-        H = readlane64(v, nblk - 1);
-    }
+    const uint64_t H = fmix64((uint64_t)(uint32_t)req_ns[r] + 1u);
+    hash_request((const GLOBAL int32_t *)(tokens + off), (int32_t)nb, H, (GLOBAL uint64_t *)(keys + ko), lane);
 }
 
 }  // namespace

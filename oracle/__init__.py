@@ -86,6 +86,13 @@ def hash_request(tokens: np.ndarray, ns: int) -> np.ndarray:
     return out
 
 
+def block_offsets(req_len) -> np.ndarray:
+    """CSR offsets of the full 16-token blocks (Sec. III-B: only full KV
+    blocks count): off[r] = sum_{i<r} floor(max(len_i, 0) / 16), r = 0..R."""
+    n = np.maximum(np.asarray(req_len, np.int64), 0) // 16
+    return np.concatenate([np.zeros(1, np.int64), np.cumsum(n, dtype=np.int64)])
+
+
 def hash_trace(trace):
     """Keys and CSR key offsets of every full block of every request."""
     R = trace.n_req

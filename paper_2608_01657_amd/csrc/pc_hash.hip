@@ -59,11 +59,6 @@ __device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
     uint32_t hi = __shfl((int)(uint32_t)(v >> 32), src);
     return ((uint64_t)hi << 32) | lo;
 }
-__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int d) {
-    uint32_t lo = __shfl_up((int)(uint32_t)v, d);
-    uint32_t hi = __shfl_up((int)(uint32_t)(v >> 32), d);
-    return ((uint64_t)hi << 32) | lo;
-}
 __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
     uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, l);
     uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
@@ -87,18 +82,47 @@ __device__ __forceinline__ uint64_t dpp64(uint64_t x) {
     return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
 }
 
+// Inclusive wavefront sum scan of a 64-bit value in DPP steps (no LDS):
+// within each row of 16 lanes, then rows 1 and 3 add the last lane of the
+// row before them, then rows 2 and 3 add lane 31.
+__device__ __forceinline__ int64_t wave_scan_add64(int64_t x) {
+    uint64_t v = (uint64_t)x;
+    v += dpp64<0x111, 0xF>(v);
+    v += dpp64<0x112, 0xF>(v);
+    v += dpp64<0x114, 0xF>(v);
+    v += dpp64<0x118, 0xF>(v);
+    v += dpp64<0x142, 0xA>(v);
+    v += dpp64<0x143, 0xC>(v);
+    return (int64_t)v;
+}
+
 // ---------------------------------------------------------------- offsets
-constexpr int kScanChunk = 4096;
+// Three launches: per-chunk sums (written where the chunk ends), a scan of
+// the chunk sums in place, then each chunk's exclusive scan from its base.
+// Thread t of a chunk owns its requests 4t..4t+3 (coalesced), and every
+// length load is issued before any is used.
 constexpr int kScanThreads = 256;
+constexpr int kScanChunk = 4 * kScanThreads;
 
 __device__ __forceinline__ int64_t nblocks_of(int32_t len) { return len > 0 ? (int64_t)(len / 16) : 0; }
 
+// blocks of requests start + 4t .. start + 4t + 3 (0 past n); the loads are
+// clamped into [0, n) so that none sits under a branch
+__device__ __forceinline__ void chunk_blocks(const int32_t *__restrict__ len, int64_t start, int64_t n,
+                                             int64_t (&nb)[4]) {
+    int32_t x[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t e = start + 4 * threadIdx.x + i;
+        x[i] = len[e < n ? e : n - 1];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) nb[i] = start + 4 * threadIdx.x + i < n ? nblocks_of(x[i]) : 0;
+}
+
 __device__ int64_t block_incl_scan(int64_t v, int64_t *sh /* [kScanThreads/64] */) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    for (int d = 1; d < 64; d <<= 1) {
-        int64_t u = (int64_t)shfl_up64((uint64_t)v, d);
-        if (lane >= d) v += u;
-    }
+    v = wave_scan_add64(v);
     if (lane == 63) sh[w] = v;
     __syncthreads();
     int64_t add = 0;
@@ -111,17 +135,11 @@ __device__ int64_t block_incl_scan(int64_t v, int64_t *sh /* [kScanThreads/64] *
 __global__ __launch_bounds__(kScanThreads) void offsets_reduce(const int32_t *__restrict__ len, int64_t n,
                                                                int64_t *__restrict__ key_off) {
     __shared__ int64_t sh[kScanThreads / 64];
-    const int64_t b = blockIdx.x, start = b * kScanChunk;
-    int64_t s = 0;
-    for (int i = threadIdx.x; i < kScanChunk; i += kScanThreads) {
-        int64_t e = start + i;
-        if (e < n) s += nblocks_of(len[e]);
-    }
-    s = block_incl_scan(s, sh);
-    if (threadIdx.x == kScanThreads - 1) {
-        int64_t pos = start + kScanChunk < n ? start + kScanChunk : n;
-        key_off[pos] = s;
-    }
+    const int64_t start = (int64_t)blockIdx.x * kScanChunk;
+    int64_t nb[4];
+    chunk_blocks(len, start, n, nb);
+    const int64_t s = block_incl_scan(nb[0] + nb[1] + nb[2] + nb[3], sh);
+    if (threadIdx.x == kScanThreads - 1) key_off[start + kScanChunk < n ? start + kScanChunk : n] = s;
 }
 
 // B: inclusive scan of the chunk sums in place; key_off[0] = 0
@@ -131,14 +149,14 @@ __global__ __launch_bounds__(kScanThreads) void offsets_chunks(int64_t n, int64_
     __shared__ int64_t last;
     int64_t carry = 0;
     for (int64_t c0 = 0; c0 < nchunks; c0 += kScanThreads) {
-        int64_t c = c0 + threadIdx.x;
+        const int64_t c = c0 + threadIdx.x;
         int64_t pos = 0;
         int64_t v = 0;
         if (c < nchunks) {
             pos = (c + 1) * kScanChunk < n ? (c + 1) * kScanChunk : n;
             v = key_off[pos];
         }
-        int64_t incl = block_incl_scan(v, sh);
+        const int64_t incl = block_incl_scan(v, sh);
         if (c < nchunks) key_off[pos] = carry + incl;
         if (threadIdx.x == kScanThreads - 1) last = incl;
         __syncthreads();
@@ -151,29 +169,18 @@ __global__ __launch_bounds__(kScanThreads) void offsets_chunks(int64_t n, int64_
 // C: exclusive scan inside each chunk, starting from the chunk's offset
 __global__ __launch_bounds__(kScanThreads) void offsets_fill(const int32_t *__restrict__ len, int64_t n,
                                                              int64_t *__restrict__ key_off) {
-    __shared__ int64_t vals[kScanChunk];
     __shared__ int64_t sh[kScanThreads / 64];
-    const int64_t b = blockIdx.x, start = b * kScanChunk;
-    const int64_t base_off = b == 0 ? 0 : key_off[start];
-    for (int i = threadIdx.x; i < kScanChunk; i += kScanThreads) {
-        int64_t e = start + i;
-        vals[i] = e < n ? nblocks_of(len[e]) : 0;
-    }
-    __syncthreads();
-    constexpr int kPer = kScanChunk / kScanThreads;
-    int64_t loc = 0;
-    for (int i = 0; i < kPer; ++i) loc += vals[threadIdx.x * kPer + i];
-    int64_t incl = block_incl_scan(loc, sh);
-    int64_t run = base_off + incl - loc;
-    for (int i = 0; i < kPer; ++i) {
-        int64_t v = vals[threadIdx.x * kPer + i];
-        vals[threadIdx.x * kPer + i] = run;
-        run += v;
-    }
-    __syncthreads();
-    for (int i = threadIdx.x; i < kScanChunk; i += kScanThreads) {
-        int64_t e = start + i;
-        if (e < n) key_off[e] = vals[i];
+    const int64_t start = (int64_t)blockIdx.x * kScanChunk;
+    const int64_t base_off = blockIdx.x == 0 ? 0 : key_off[start];
+    int64_t nb[4];
+    chunk_blocks(len, start, n, nb);
+    const int64_t loc = nb[0] + nb[1] + nb[2] + nb[3];
+    int64_t run = base_off + block_incl_scan(loc, sh) - loc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t e = start + 4 * threadIdx.x + i;
+        if (e < n) key_off[e] = run;
+        run += nb[i];
     }
 }
 
@@ -289,13 +296,11 @@ __global__ __launch_bounds__(64 * kHashWaves) void hash_kernel(
 
 hipError_t launch_block_offsets(const int32_t *len, int64_t n_req, int64_t *key_off, hipStream_t s) {
     const int64_t nchunks = (n_req + kScanChunk - 1) / kScanChunk;
-    if (nchunks > 0) {
+    if (nchunks > 0)
         hipLaunchKernelGGL(offsets_reduce, dim3((unsigned)nchunks), dim3(kScanThreads), 0, s, len, n_req, key_off);
-    }
     hipLaunchKernelGGL(offsets_chunks, dim3(1), dim3(kScanThreads), 0, s, n_req, nchunks, key_off);
-    if (nchunks > 0) {
+    if (nchunks > 0)
         hipLaunchKernelGGL(offsets_fill, dim3((unsigned)nchunks), dim3(kScanThreads), 0, s, len, n_req, key_off);
-    }
     return hipGetLastError();
 }
 

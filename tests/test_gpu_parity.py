@@ -173,3 +173,18 @@ def test_replay_normalized_debt_tiers():
         per.append([tg.Instance(0, pol, 2 * m, contracts=[(4 * Q, 0), (Q, 0), (Q, 1 << 40)], flags=fl)
                     for pol in POLICIES for fl in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0])])
     run_key_traces(kts, per)
+
+
+@pytest.mark.parametrize("n", [0, 1, 1023, 1024, 1025, 50_000, 256 * 1024, 256 * 1024 + 1, (1 << 21) + 4097])
+def test_block_offsets_sizes(n):
+    """CSR block offsets at sizes around the chunking (1024 requests per
+    chunk; the chunk-sum scan loops past 256 chunks), including negative
+    lengths, which count as no blocks."""
+    import torch
+    rng = np.random.default_rng(n)
+    lens = rng.integers(-20, 40000, n).astype(np.int32)
+    d_len = torch.from_numpy(lens).to("cuda")
+    d_off = torch.full((n + 1,), -7, dtype=torch.int64, device="cuda")
+    dv.pc_block_offsets(d_len, d_off)
+    torch.cuda.synchronize()
+    assert np.array_equal(d_off.cpu().numpy(), oracle.block_offsets(lens))

@@ -153,3 +153,16 @@ def test_golden_vectors():
         toks = np.random.Generator(np.random.PCG64(seed)).integers(-2**31, 2**31, L, dtype=np.int64).astype(np.int32)
         got = [int(x) for x in oracle.hash_request(toks, ns)]
         assert got == want
+
+
+def test_block_offsets_definition():
+    """The plain offsets definition agrees with the C oracle's hash pass
+    (which writes its own CSR offsets) and with a hand count: only full
+    16-token blocks count, and a negative length counts as none."""
+    from paper_2608_01657_amd import tracegen as tg
+    traces, _ = tg.workload("tiny", seeds=[0], n_requests=300)
+    tr = traces[0]
+    _, off = oracle.hash_trace(tr)
+    assert np.array_equal(oracle.block_offsets(tr.length), off)
+    assert list(oracle.block_offsets([0, 15, 16, 17, 31, 32, -5, 1024 + 15])) == [0, 0, 0, 1, 2, 3, 5, 5, 69]
+    assert list(oracle.block_offsets([])) == [0]

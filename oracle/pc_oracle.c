@@ -28,8 +28,9 @@
  * 2. Replay of a request trace against one cache instance, following the
  *    request hooks of Algorithm 1 and the batch reclamation of Algorithm 2,
  *    with Eqs. 1-9 in Q16 fixed point (2^16 = one block).  Policies: LRU
- *    (vLLM's free-queue order, Sec. V-A), S3-FIFO (Sec. V-A baseline) and
- *    PrefixShield.  The per-request step order, and every point where the
+ *    (vLLM's free-queue order, Sec. V-A), S3-FIFO (Sec. V-A baseline),
+ *    PrefixShield, and StaticQuota (Sec. V-A baseline: equal fixed
+ *    partitions of floor(C/G) blocks, LRU inside each, no borrowing).  The per-request step order, and every point where the
  *    paper is silent, is listed in the repository's design notes; the
  *    comments below name the paper passage each step follows.
  *
@@ -166,7 +167,7 @@ static void map_clear(Map *m) { m->cur++; m->size = 0; if (m->cur == 0) { memset
 /* Replay                                                                    */
 /* ------------------------------------------------------------------------ */
 
-enum { ORC_LRU = 0, ORC_S3FIFO = 1, ORC_PS = 2 };
+enum { ORC_LRU = 0, ORC_S3FIFO = 1, ORC_PS = 2, ORC_SQ = 3 };
 enum { ORC_NO_SEGMENTATION = 1, ORC_NO_DEBT_GATE = 2 };
 enum { PROB = 0, NORMAL = 1, REUSE = 2 };      /* Sec. III-A retention classes */
 #define SCALE 65536LL
@@ -205,7 +206,8 @@ typedef struct {
     int32_t *free_ids;
     int64_t n_free;
     Map map;          /* key -> block id of resident blocks */
-    List *lists;      /* LRU: 1; PS: G*3; S3: 2 (S, M) */
+    List *lists;      /* LRU: 1; PS: G*3; S3: 2 (S, M); SQ: G (one per partition) */
+    int64_t quota;    /* SQ: blocks per group partition */
     int n_lists;
 
     int64_t bal[64][4], last[64][4];
@@ -400,7 +402,8 @@ static void account_all(Inst *s, int64_t t) {
  * Replay one instance.
  *   keys/key_off : full-block keys, CSR offsets [n_req+1]
  *   group, contract, prefix, tick (tick may be NULL: tick = request index)
- *   policy 0 LRU, 1 S3-FIFO, 2 PrefixShield; flags 1 no segmentation, 2 no debt gate
+ *   policy 0 LRU, 1 S3-FIFO, 2 PrefixShield, 3 StaticQuota; flags 1 no
+ *   segmentation, 2 no debt gate
  *   rho_q16/beta_q16 [n_contracts]
  *   group_stats_out [n_groups][17], inst_stats_out [7]
  *   per_req_out (optional) [n_req][4]: hits, new blocks, evictions, orphans
@@ -413,7 +416,7 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
                const int64_t *rho_q16, const int64_t *beta_q16, int64_t eps_q16,
                int32_t s3_small_permille, int32_t s3_move_threshold,
                int64_t *group_stats_out, int64_t *inst_stats_out, int32_t *per_req_out) {
-    if (policy < 0 || policy > 2 || capacity < 1 || n_groups < 1 || n_groups > 64 ||
+    if (policy < 0 || policy > 3 || capacity < 1 || n_groups < 1 || n_groups > 64 ||
         n_contracts < 1 || n_contracts > 4 || eps_q16 < 0 || n_req < 0 || n_prefix < 0)
         return -1;
     if (s3_small_permille < 0 || s3_small_permille > 1000 || s3_move_threshold < 0) return -1;
@@ -422,6 +425,7 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
     Inst *s = &S;
     s->policy = policy; s->flags = flags; s->G = n_groups; s->K = n_contracts;
     s->C = capacity; s->eps = eps_q16;
+    s->quota = capacity / n_groups;   /* SQ partitions; C mod G blocks stay unused */
     int64_t rho_min = 0;
     for (int c = 0; c < n_contracts; c++) {
         if (rho_q16[c] <= 0 || beta_q16[c] < 0) return -1;
@@ -449,7 +453,7 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
     int rc = -2;
     s->blk = (Block *)calloc((size_t)capacity + 1, sizeof(Block));
     s->free_ids = (int32_t *)malloc(((size_t)capacity + 1) * sizeof(int32_t));
-    s->n_lists = (policy == ORC_PS) ? 3 * n_groups : (policy == ORC_S3FIFO ? 2 : 1);
+    s->n_lists = (policy == ORC_PS) ? 3 * n_groups : (policy == ORC_S3FIFO ? 2 : (policy == ORC_SQ ? n_groups : 1));
     s->lists = (List *)malloc((size_t)s->n_lists * sizeof(List));
     s->referenced = (uint8_t *)calloc((size_t)n_prefix + 1, 1);
     s->admitted = (uint8_t *)calloc((size_t)n_prefix + 1, 1);
@@ -488,7 +492,10 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
         s->referenced[p] = 1;
         o[G_REQUESTS]++;
         int64_t n_full = key_off[r + 1] - key_off[r];
-        int64_t n = n_full < s->C ? n_full : s->C;
+        /* a request can hold at most the space it may fill: the cache, or
+           under StaticQuota its group's partition */
+        const int64_t room = policy == ORC_SQ ? s->quota : s->C;
+        int64_t n = n_full < room ? n_full : room;
         o[G_TRUNCATED] += n_full - n;
         o[G_PROBES] += n;
 
@@ -558,8 +565,10 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
             }
         }
 
-        /* Alg. 2: truly free blocks first, then reclaim e victims */
-        int64_t free_now = s->C - s->resident_total;
+        /* Alg. 2: truly free blocks first, then reclaim e victims.  Under
+           StaticQuota the free space is what the requester's partition has
+           left, and only its own blocks are reclaimed. */
+        int64_t free_now = policy == ORC_SQ ? s->quota - s->resident[g] : s->C - s->resident_total;
         int64_t e = m - free_now;
         if (e < 0) e = 0;
         int64_t P[64], D[64];
@@ -568,6 +577,7 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
         for (int64_t i = 0; i < e; i++) {
             int32_t v;
             if (policy == ORC_LRU) v = s->lists[0].head;
+            else if (policy == ORC_SQ) v = s->lists[g].head;
             else if (policy == ORC_PS) v = ps_pick(s, P, D);
             else v = s3_evict_one(s);
             if (v < 0) { rc = -3; goto out; }
@@ -620,7 +630,8 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
                 if (x->list == 0) s->s_unpinned++; else s->m_unpinned++;
             } else {
                 x->stamp = ++s->stampctr;
-                list_append(s, policy == ORC_LRU ? 0 : ps_list(s, x->owner, x->cls), pos_blk[j]);
+                list_append(s, policy == ORC_LRU ? 0 : (policy == ORC_SQ ? x->owner : ps_list(s, x->owner, x->cls)),
+                            pos_blk[j]);
             }
         }
 

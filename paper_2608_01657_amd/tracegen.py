@@ -29,7 +29,9 @@ Q16 = 1 << 16              # fixed-point scale: 2^16 represents one block
 POLICY_LRU = 0
 POLICY_S3FIFO = 1
 POLICY_PREFIXSHIELD = 2
-POLICY_NAMES = {POLICY_LRU: "lru", POLICY_S3FIFO: "s3fifo", POLICY_PREFIXSHIELD: "prefixshield"}
+POLICY_STATICQUOTA = 3
+POLICY_NAMES = {POLICY_LRU: "lru", POLICY_S3FIFO: "s3fifo", POLICY_PREFIXSHIELD: "prefixshield",
+                POLICY_STATICQUOTA: "staticquota"}
 
 FLAG_NO_SEGMENTATION = 1   # ablation of Sec. V-D, Fig. 3a
 FLAG_NO_DEBT_GATE = 2      # ablation of Sec. V-D, Fig. 3b

@@ -11,6 +11,9 @@ Semantics (same reading as the oracle): per request -- OnRequest; lookup
 else); pin hits; drop resident blocks behind the first miss; OnTouch with
 the pre-charge debt; reclaim max(0, new - free) victims; charge and classify
 (Eqs. 1-2, Alg. 1); insert deepest-first; release deepest-first; account.
+StaticQuota (Sec. V-A baseline): each group owns floor(C/G) blocks, a
+request probes at most that many, and its victims are the requester's own
+least recently released blocks.
 """
 from __future__ import annotations
 
@@ -26,7 +29,8 @@ GROUP_FIELDS = ["requests", "probes", "hits", "misses", "charged", "evicted_owne
 
 def brute_replay(keys, key_off, group, contract, prefix, n_groups, inst, tick=None):
     C = inst.capacity
-    pol = inst.policy                  # 0 LRU, 1 S3-FIFO, 2 PrefixShield
+    pol = inst.policy                  # 0 LRU, 1 S3-FIFO, 2 PrefixShield, 3 StaticQuota
+    quota = C // n_groups
     no_seg = bool(inst.flags & 1)
     no_gate = bool(inst.flags & 2)
     eps = inst.eps_q16
@@ -93,7 +97,7 @@ def brute_replay(keys, key_off, group, contract, prefix, n_groups, inst, tick=No
         q1 = p in referenced
         referenced.add(p)
         o["requests"] += 1
-        n = min(len(ks), C)
+        n = min(len(ks), quota if pol == 3 else C)
         o["truncated"] += len(ks) - n
         o["probes"] += n
         ks = ks[:n]
@@ -141,7 +145,10 @@ def brute_replay(keys, key_off, group, contract, prefix, n_groups, inst, tick=No
                     else:
                         o["gated"] += 1
 
-        e = max(0, m - (C - len(blocks)))
+        if pol == 3:
+            e = max(0, m - (quota - sum(1 for b in blocks.values() if b["owner"] == g)))
+        else:
+            e = max(0, m - (C - len(blocks)))
         if pol == 2 and e:
             P = [ndebt(x, t) for x in range(n_groups)]
             D = [dec(x, t) for x in range(n_groups)]
@@ -149,6 +156,8 @@ def brute_replay(keys, key_off, group, contract, prefix, n_groups, inst, tick=No
             cands = [(k, b) for k, b in blocks.items() if not b["pinned"]]
             if pol == 0:
                 vk = min(cands, key=lambda kb: kb[1]["stamp"])[0]
+            elif pol == 3:
+                vk = min(((k, b) for k, b in cands if b["owner"] == g), key=lambda kb: kb[1]["stamp"])[0]
             elif pol == 2:
                 best = None
                 for x in range(n_groups):

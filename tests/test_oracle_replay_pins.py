@@ -390,3 +390,103 @@ def test_normalized_debt_crossover():
     res = oracle.replay_key_trace(_tier_trace(m, e), inst)
     ea, eb = res.groups[0]["evicted_owned"], res.groups[1]["evicted_owned"]
     assert (ea, eb) == (5, 31)
+
+
+# ---------------------------------------------------------------- StaticQuota
+
+SQ = tg.POLICY_STATICQUOTA
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_staticquota_one_group_is_lru(seed):
+    """With one group the partition is the whole cache: StaticQuota is LRU
+    bit-exactly (Sec. V-A names LRU as the base order inside a partition)."""
+    kt = tg.random_key_trace(seed, n_req=60, max_blocks=7, n_groups=1, key_universe=20, with_ticks=bool(seed % 2))
+    for C in (1, 3, 8, 20):
+        lru = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_LRU, C), per_request=True)
+        sq = oracle.replay_key_trace(kt, tg.Instance(0, SQ, C), per_request=True)
+        assert lru.groups == sq.groups and lru.inst == sq.inst
+        assert np.array_equal(lru.per_request, sq.per_request)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_staticquota_partitions_are_isolated(seed):
+    """No borrowing: a group's counters do not depend on the other groups'
+    traffic.  The same group-0 requests at the same ticks, with and without
+    three other groups interleaved, give identical group-0 counters (all but
+    the debt sum and the final debt, which are read at the other groups'
+    requests too)."""
+    rng = np.random.default_rng(seed)
+    G, R = 4, 240
+    groups = rng.integers(0, G, R).astype(np.uint8)
+    reqs = [list(int(g) * 1000 + rng.integers(0, 40, int(rng.integers(1, 9)))) for g in groups]
+    ticks = np.arange(R, dtype=np.int64) * 3
+    full = key_trace(reqs, groups=groups, n_groups=G, prefixes=[r % 17 for r in range(R)], tick=ticks)
+    sel = [r for r in range(R) if groups[r] == 0]
+    alone = key_trace([reqs[r] for r in sel], groups=[0] * len(sel), n_groups=G,
+                      prefixes=[r % 17 for r in sel], tick=ticks[sel])
+    for C in (8, 30, 101):
+        a = oracle.replay_key_trace(full, tg.Instance(0, SQ, C, contracts=[(Q // 3, 4 * Q)]))
+        b = oracle.replay_key_trace(alone, tg.Instance(0, SQ, C, contracts=[(Q // 3, 4 * Q)]))
+        ga, gb = dict(a.groups[0]), dict(b.groups[0])
+        for f in ("debt_sum_q16", "debt_end_q16"):
+            ga.pop(f), gb.pop(f)
+        assert ga == gb
+        for g in a.groups:
+            assert g["resident_max"] <= C // G
+
+
+def test_staticquota_cyclic_sweep_above_partition_never_hits():
+    """The mechanism the paper gives for StaticQuota's 0.00% victim hit
+    ratio under low-and-slow pollution (Sec. V-B): a hot set of 288 blocks
+    cycled through a 255-block partition (C = 511, two groups) never hits,
+    although LRU over the whole cache, with the peer idle, hits on every
+    revisit."""
+    K, C = 288, 511
+    reqs = [[i % K] for i in range(4 * K)]
+    kt = key_trace(reqs, prefixes=[i % K for i in range(4 * K)], n_groups=2)
+    sq = oracle.replay_key_trace(kt, tg.Instance(0, SQ, C))
+    assert sq.groups[0]["hits"] == 0 and sq.groups[0]["resident_max"] == C // 2
+    lru = oracle.replay_key_trace(kt, tg.Instance(0, tg.POLICY_LRU, C))
+    assert lru.groups[0]["hits"] == 3 * K
+    # one block fewer than the partition: every revisit hits
+    kt2 = key_trace([[i % 255] for i in range(4 * 255)], prefixes=[i % 255 for i in range(4 * 255)], n_groups=2)
+    assert oracle.replay_key_trace(kt2, tg.Instance(0, SQ, C)).groups[0]["hits"] == 3 * 255
+
+
+def test_staticquota_no_borrowing_from_idle_peer():
+    """Table III: with the peer idle, StaticQuota's active group stays at its
+    partition (254-255 of 511 there), unlike the work-conserving policies."""
+    rng = np.random.default_rng(3)
+    reqs = [list(rng.integers(0, 300, 6)) for _ in range(200)]
+    kt = key_trace(reqs, n_groups=2)
+    res = oracle.replay_key_trace(kt, tg.Instance(0, SQ, 65, contracts=[(Q // 8, 0)]))
+    assert res.groups[0]["resident_max"] == 32 and res.groups[1]["resident_max"] == 0
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_staticquota_hits_bounded_by_belady_per_partition(seed):
+    """Each group pages its own keys through a cache of floor(C/G) blocks,
+    so its hits never exceed Belady's MIN for that size."""
+    rng = np.random.default_rng(100 + seed)
+    G, R, C = 3, 150, 20
+    groups = rng.integers(0, G, R).astype(np.uint8)
+    reqs = [list(int(g) * 1000 + rng.integers(0, 15, int(rng.integers(1, 5)))) for g in groups]
+    kt = key_trace(reqs, groups=groups, n_groups=G)
+    res = oracle.replay_key_trace(kt, tg.Instance(0, SQ, C))
+    for g in range(G):
+        seq = [k for r in range(R) if groups[r] == g for k in reqs[r]]
+        assert res.groups[g]["hits"] <= belady_min_hits(seq, C // G)
+
+
+def test_staticquota_truncates_at_the_partition():
+    """A request can use at most its partition: the rest of it is truncated
+    (the capacity rule applied to the partition); C < G leaves no room."""
+    kt = key_trace([list(range(10)), list(range(10)), list(range(100, 103))], groups=[0, 0, 1], n_groups=2)
+    res = oracle.replay_key_trace(kt, tg.Instance(0, SQ, 9))   # quota 4
+    g0 = res.groups[0]
+    assert g0["probes"] == 8 and g0["truncated"] == 12 and g0["hits"] == 4 and g0["resident_max"] == 4
+    assert res.groups[1]["probes"] == 3 and res.groups[1]["truncated"] == 0
+    res = oracle.replay_key_trace(kt, tg.Instance(0, SQ, 1))   # quota 0
+    assert all(g["probes"] == 0 and g["resident_max"] == 0 for g in res.groups)
+    assert res.groups[0]["truncated"] == 20

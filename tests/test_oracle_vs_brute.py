@@ -14,7 +14,7 @@ import oracle
 from brute_force import brute_replay
 from paper_2608_01657_amd import tracegen as tg
 
-POLICIES = [tg.POLICY_LRU, tg.POLICY_S3FIFO, tg.POLICY_PREFIXSHIELD]
+POLICIES = [tg.POLICY_LRU, tg.POLICY_S3FIFO, tg.POLICY_PREFIXSHIELD, tg.POLICY_STATICQUOTA]
 
 
 def _compare(kt, inst):

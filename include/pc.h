@@ -84,7 +84,13 @@ int32_t pc_hash_blocks(const int32_t *d_tokens, int64_t n_tokens,
 /* ------------------------------------------------------------------------
  * Replay.
  * ------------------------------------------------------------------------ */
-enum { PC_LRU = 0, PC_S3FIFO = 1, PC_PREFIXSHIELD = 2 };
+/* Policies (Sec. V-A): LRU is the engine's free-queue order; S3-FIFO and
+ * StaticQuota are the paper's baselines; PrefixShield is its method (Sec.
+ * III).  StaticQuota gives every accounting group a fixed partition of
+ * floor(capacity / n_groups) blocks with LRU inside it and no borrowing: a
+ * request probes at most its partition (the rest counts as truncated) and
+ * reclaims only its own group's blocks. */
+enum { PC_LRU = 0, PC_S3FIFO = 1, PC_PREFIXSHIELD = 2, PC_STATICQUOTA = 3 };
 enum { PC_FLAG_NO_SEGMENTATION = 1,   /* Sec. V-D ablation: one retention segment    */
        PC_FLAG_NO_DEBT_GATE = 2 };    /* Sec. V-D ablation: promote regardless of debt */
 
@@ -114,7 +120,8 @@ typedef struct {
 
 typedef struct {
     int32_t trace;                 /* index into the traces array                  */
-    int32_t policy;                /* PC_LRU / PC_S3FIFO / PC_PREFIXSHIELD          */
+    int32_t policy;                /* PC_LRU / PC_S3FIFO / PC_PREFIXSHIELD /
+                                      PC_STATICQUOTA                                */
     int32_t capacity;              /* usable blocks, 1..PC_MAX_CAPACITY             */
     int32_t flags;                 /* PC_FLAG_*                                     */
     int32_t n_contracts;           /* 1..4                                          */

@@ -25,7 +25,7 @@ PHASE_EVENTS = ["evicting_requests", "log_compactions", "s3fifo_scan_batches", "
 PC_OK, PC_EINVAL, PC_ENOMEM, PC_EDEVICE, PC_EUNSUPPORTED, PC_EINTERNAL = 0, -1, -2, -3, -4, -5
 PC_BLOCK_TOKENS = 16
 PC_MAX_GROUPS, PC_MAX_CONTRACTS, PC_MAX_CAPACITY = 64, 4, 32767
-PC_LRU, PC_S3FIFO, PC_PREFIXSHIELD = 0, 1, 2
+PC_LRU, PC_S3FIFO, PC_PREFIXSHIELD, PC_STATICQUOTA = 0, 1, 2, 3
 PC_FLAG_NO_SEGMENTATION, PC_FLAG_NO_DEBT_GATE = 1, 2
 PC_STATS_RECORD_BYTES = 64 * 136 + 64
 

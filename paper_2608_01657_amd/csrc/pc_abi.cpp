@@ -114,7 +114,7 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
     for (int i = 0; i < n_inst; ++i) {
         const pc_instance_desc &s = inst[i];
         if (s.trace < 0 || s.trace >= n_traces) return fail(PC_EINVAL, "instance %d: trace index %d", i, s.trace);
-        if (s.policy < PC_LRU || s.policy > PC_PREFIXSHIELD) return fail(PC_EINVAL, "instance %d: policy %d", i, s.policy);
+        if (s.policy < PC_LRU || s.policy > PC_STATICQUOTA) return fail(PC_EINVAL, "instance %d: policy %d", i, s.policy);
         if (s.capacity < 1 || s.capacity > PC_MAX_CAPACITY)
             return fail(PC_EINVAL, "instance %d: capacity %d outside 1..%d", i, s.capacity, PC_MAX_CAPACITY);
         if (s.flags & ~(PC_FLAG_NO_SEGMENTATION | PC_FLAG_NO_DEBT_GATE))
@@ -180,11 +180,12 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         d.o_vlist = take(2 * mx);
         d.o_rcnt = take(4LL << (d.rs_log2 - 3));
         d.o_res = take(4LL * 64);
-        if (s.policy == PC_PREFIXSHIELD) {
-            d.o_pfx = take(4 * C);
+        if (s.policy == PC_PREFIXSHIELD) d.o_pfx = take(4 * C);
+        if (s.policy == PC_PREFIXSHIELD || s.policy == PC_STATICQUOTA) {   // per-(group, segment) queues
             d.o_cnt = take(4LL * 192);
             d.o_cur = take(4LL * 196);
         }
+        if (s.policy == PC_STATICQUOTA) d.o_fstack = take(2 * C);   // free-slot stack
         if (s.policy == PC_S3FIFO && d.g_cap > 0) d.o_gtable = take(32LL << d.gnb_log2);
         d.state_bytes = (int32_t)so;
         d.in_lds = so <= lds_cap ? 1 : 0;

@@ -22,7 +22,7 @@ constexpr uint32_t kPin = 1u << 14;
 constexpr uint32_t kInLog = 1u << 15;
 
 constexpr int kProb = 0, kNormal = 1, kReuse = 2;   // Sec. III-A retention classes
-constexpr int kLRU = 0, kS3 = 1, kPS = 2;
+constexpr int kLRU = 0, kS3 = 1, kPS = 2, kSQ = 3;
 constexpr int kFlagNoSeg = 1, kFlagNoGate = 2;
 
 constexpr uint32_t kEmpty = 0xFFFFFFFFu;   // empty table entry
@@ -53,7 +53,7 @@ struct DevInst {
     int32_t n_prefix_words;
     // state-region offsets (bytes)
     int32_t o_key, o_stamp, o_meta, o_table, o_log, o_posslot, o_rset, o_rkeys, o_vlist;
-    int32_t o_pfx, o_gtable, o_rcnt, o_res, o_cnt, o_cur;
+    int32_t o_pfx, o_gtable, o_rcnt, o_res, o_cnt, o_cur, o_fstack;
     // workspace offsets (bytes from workspace base)
     int64_t ws_state;      // state region when !in_lds
     int64_t ws_bits;       // uint32 [2 * n_prefix_words]: referenced, admitted

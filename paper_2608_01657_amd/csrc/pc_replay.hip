@@ -8,9 +8,10 @@
 //   pin + OnTouch       S3-FIFO frequency, or the debt-gated promotion of
 //                       Eq. 4 using the debt before this request's charge
 //   reclamation         truly free slots first, then e victims: LRU order,
-//                       S3-FIFO small/main/ghost, or PrefixShield's
+//                       S3-FIFO small/main/ghost, PrefixShield's
 //                       projected-debt argmax (Eqs. 5-8) with the
-//                       reuse-segmented order inside the group (Eq. 9)
+//                       reuse-segmented order inside the group (Eq. 9), or
+//                       StaticQuota's own partition of floor(C/G) blocks
 //   OnCacheFullBlocks   charge n_r (Eqs. 1-2), initial class, admission
 //   insert + release    new blocks take the victims' slots; every block of
 //                       the request returns to the free queue deepest first
@@ -302,6 +303,8 @@ struct Req {
 template <bool kLds, int kPol>
 struct Replayer {
     static constexpr int policy = kPol;
+    // per-(group, segment) free queues: live counts and log cursors
+    static constexpr bool kQueues = kPol == kPS || kPol == kSQ;
     Coll &X;
     const int tid, wid, lane;
     int cb;                   // ballot buffer in use
@@ -309,6 +312,7 @@ struct Replayer {
     const DevInst &I;
     const DevTrace &T;
     int C, flags, G, K, nseg;
+    int room;                 // most blocks one request may hold: C, or the StaticQuota partition
     int64_t eps;
     uint32_t nbmask, rsmask, rbmask, lmask, R, gnbmask, grmask;
     int32_t s_cap, g_cap, move_thr;
@@ -316,7 +320,7 @@ struct Replayer {
     // ---------------- arrays
     uint64_t *key, *rkeys;
     uint32_t *stamp, *meta, *table, *rset, *rcnt, *cnt, *cur, *res, *pfx, *gtable;
-    uint16_t *log, *posslot, *vlist;
+    uint16_t *log, *posslot, *vlist, *fstack;
     GLOBAL uint32_t *bits;
     GLOBAL uint64_t *gring;
     const GLOBAL uint64_t *tkeys;
@@ -330,6 +334,7 @@ struct Replayer {
     // ---------------- uniform state (identical in every wavefront)
     uint32_t head, tail;      // live log window [head, tail)
     int32_t hwm;              // slots [hwm, C) have never been used
+    int32_t ftop;             // StaticQuota: free slots on the slot stack
     int32_t nvict;            // victims of the current request
     int32_t resident;         // resident blocks (excludes blocks being created)
     int32_t s_size, s_unp, m_unp;
@@ -359,6 +364,7 @@ struct Replayer {
         G = T.n_groups;
         K = I.n_contracts;
         nseg = (policy == kPS && !(flags & kFlagNoSeg)) ? 3 : 1;
+        room = policy == kSQ ? C / G : C;
         eps = I.eps;
         nbmask = (1u << I.nb_log2) - 1u;
         rsmask = (1u << I.rs_log2) - 1u;
@@ -393,6 +399,7 @@ struct Replayer {
         log = reinterpret_cast<uint16_t *>(sbase + I.o_log);
         posslot = reinterpret_cast<uint16_t *>(sbase + I.o_posslot);
         vlist = reinterpret_cast<uint16_t *>(sbase + I.o_vlist);
+        fstack = reinterpret_cast<uint16_t *>(sbase + I.o_fstack);
         rcnt = reinterpret_cast<uint32_t *>(sbase + I.o_rcnt);
         bits = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_bits));
         gring = gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_gring));
@@ -704,14 +711,14 @@ struct Replayer {
             bsync();
         }
         tail = nw;
-        if constexpr (policy == kPS)
+        if constexpr (kQueues)
             for (int i = tid; i < 196; i += kB) cur[i] = head;
         curS = curM = head;
         bsync();
     }
     DEV void ensure_room(uint32_t k) {
         if (tail + k - head <= R) return;
-        if constexpr (policy == kPS) {   // lowest cursor of a non-empty queue bounds every live entry
+        if constexpr (kQueues) {   // lowest cursor of a non-empty queue bounds every live entry
             uint32_t m = tail;
             for (int i = lane; i < 192; i += 64)
                 if (cnt[i] > 0 && cur[i] < m) m = cur[i];
@@ -1080,6 +1087,38 @@ struct Replayer {
         if (m > head) head = m;
     }
 
+    // ============================================================ slots
+    // Slot of the i-th new block (by rank) of the request.  A work-conserving
+    // policy reclaims only once the never-used slots are gone, so its new
+    // blocks take those first and then this request's victims' slots, and
+    // no slot is ever left over.  StaticQuota reclaims inside a full
+    // partition while the cache may still have room, so its new blocks take
+    // this request's victims' slots first, then the free-slot stack, then
+    // never-used slots; victims' slots it does not need go on the stack.
+    DEV uint32_t new_slot(int i, int nfresh) const {
+        if constexpr (policy == kSQ) {
+            if (i < nvict) return vlist[i];
+            i -= nvict;
+            if (i < ftop) return fstack[ftop - 1 - i];
+            return (uint32_t)(hwm + i - ftop);
+        } else {
+            return i < nfresh ? (uint32_t)(hwm + i) : vlist[i - nfresh];
+        }
+    }
+    // after the request's last new block: account for the slots it took
+    DEV void slots_taken(int nalloc, int nfresh) {
+        if constexpr (policy == kSQ) {
+            const int uv = nalloc < nvict ? nalloc : nvict;
+            const int rest = nalloc - uv;
+            const int us = rest < ftop ? rest : ftop;
+            for (int k = tid; k < nvict - uv; k += kB) fstack[ftop + k] = vlist[uv + k];
+            ftop += (nvict - uv) - us;
+            hwm += rest - us;
+        } else {
+            hwm += nalloc < nfresh ? nalloc : nfresh;
+        }
+    }
+
     // ============================================================ one request
     DEV void put_per_request(int64_t i) {
         int32_t *o = preq + 4 * i;
@@ -1110,7 +1149,7 @@ struct Replayer {
             nfull > max_rb || t < 0 || t < tprev)
             return false;
         tprev = t;
-        const int n = (int)(nfull < C ? nfull : C);
+        const int n = (int)(nfull < room ? nfull : room);
         const bool me = lane == g;
 
         // ---- OnRequest (Alg. 1): prior reference of (g,p), then record it.
@@ -1204,7 +1243,7 @@ struct Replayer {
             const bool inS = found && !(mt & kQMain);
             // block-wide masks: misses, found, duplicates, and the policy's
             // fourth (PrefixShield: promotion-eligible; S3-FIFO: in S)
-            constexpr int kM = policy == kLRU ? 3 : 4;
+            constexpr int kM = (policy == kPS || policy == kS3) ? 4 : 3;
             bool pa[kM];
             pa[0] = nd && !found;
             pa[1] = found;
@@ -1230,7 +1269,7 @@ struct Replayer {
             const bool elig = eligc && tid < lim;
             // hits and orphans leave their free queue; orphans also leave
             // their owner's resident count
-            if constexpr (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), found, -1);
+            if constexpr (kQueues) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), found, -1);
             wave_add(res, owner_of(mt), isOrph, -1);
             uint32_t m2 = mt | kPin;
             if (isHit) {   // pin; touch
@@ -1327,11 +1366,22 @@ struct Replayer {
         nvict = 0;
         gseq0 = gseq;
         int e = m - (C - resident);
+        if constexpr (policy == kSQ) {
+            // the requester's partition: its free space is the quota less
+            // its resident blocks (orphans already removed)
+            bsync();
+            e = m - (room - (int)rfl(res[g]));
+        } else if (e > 0) {
+            // the lookup's last writes (hits' metadata, queue counts) come
+            // after its last barrier: make them visible to every wavefront
+            bsync();
+        }
         if (e < 0) e = 0;
         PROF_COUNT(0, e > 0 ? 1 : 0);
         if (e > 0) {
             if constexpr (policy == kLRU) evict_lru(e);
             else if constexpr (policy == kPS) evict_ps(e, t);
+            else if constexpr (policy == kSQ) ps_take(g, -1, 3 * g, e);
             else evict_s3(e);
         }
         if (me) c_evc += (uint64_t)e;
@@ -1377,7 +1427,7 @@ struct Replayer {
             uint32_t slot = c_slot;
             if (c_isN) {
                 const int i = c_rkN;
-                slot = i < nfresh ? (uint32_t)(hwm + i) : vlist[i - nfresh];
+                slot = new_slot(i, nfresh);
                 key[slot] = c_key;
                 hh = c_h;
                 const uint32_t val = (hh.tag << 16) | slot;
@@ -1411,7 +1461,7 @@ struct Replayer {
                 stamp[slot] = np;
                 meta[slot] = (mt & ~kPin) | kInLog | kRes;
             }
-            if constexpr (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), c_rl, 1);
+            if constexpr (kQueues) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), c_rl, 1);
         }
         for (int base = 0; n > kB && base < n; base += kB) {
             const int j = base + tid;
@@ -1435,7 +1485,7 @@ struct Replayer {
             touched = 0;
             if (isN) {
                 const int i = nalloc + ma[0].rank(wid);
-                slot = i < nfresh ? (uint32_t)(hwm + i) : vlist[i - nfresh];
+                slot = new_slot(i, nfresh);
                 key[slot] = kk;
                 const uint32_t val = (hh.tag << 16) | slot;
                 if (!tclaim(table, rset, val, hh, e, touched)) defer_kick(val, kk, true);
@@ -1471,7 +1521,7 @@ struct Replayer {
                 stamp[slot] = np;
                 meta[slot] = (mt & ~kPin) | kInLog | kRes;
             }
-            if constexpr (policy == kPS) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), rl, 1);
+            if constexpr (kQueues) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), rl, 1);
             seen += ma[1].count();
             seen_new += ma[2].count();
             if (base + kB < n) {   // another step follows: place displaced entries first
@@ -1484,7 +1534,7 @@ struct Replayer {
         else bsync();
         tclaim_reset(rset, hh, touched);
         kick_pending();
-        hwm += nalloc < nfresh ? nalloc : nfresh;
+        slots_taken(nalloc, nfresh);
         if (m > 0) {
             if (tid == 0) atomicAdd(&res[g], (uint32_t)m);
             resident += m;
@@ -1535,7 +1585,7 @@ struct Replayer {
         for (int i = tid; i < C; i += kB) meta[i] = 0;
         for (int i = tid; i < 64; i += kB) res[i] = 0u;
         for (uint32_t i = tid; i <= rbmask; i += kB) rcnt[i] = 0u;
-        if constexpr (policy == kPS)
+        if constexpr (kQueues)
             for (int i = tid; i < 196; i += kB) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
         for (int i = tid; i < 2 * I.n_prefix_words; i += kB) bits[i] = 0u;
         if (policy == kS3 && g_cap > 0) {
@@ -1546,6 +1596,7 @@ struct Replayer {
         for (uint32_t i = tid; i <= rsmask; i += kB) rset[i] = kEmpty;
         head = tail = 0;
         hwm = 0;
+        ftop = 0;
         nvict = 0;
         resident = 0;
         s_size = s_unp = m_unp = 0;
@@ -1667,6 +1718,9 @@ __global__ __launch_bounds__(kB) void replay_kernel(const DevInst *__restrict__ 
         rp.run(st, per_req);
     } else if (I.policy == kS3) {
         Replayer<kLds, kS3> rp(coll, I, T, sbase, ws);
+        rp.run(st, per_req);
+    } else if (I.policy == kSQ) {
+        Replayer<kLds, kSQ> rp(coll, I, T, sbase, ws);
         rp.run(st, per_req);
     } else {
         Replayer<kLds, kPS> rp(coll, I, T, sbase, ws);

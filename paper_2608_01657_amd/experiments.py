@@ -7,8 +7,9 @@ measures on the replay engine with the seeded synthetic traces of tracegen:
 
   attacks   victim hit ratio (mean over victim requests of cached tokens /
             prompt tokens) under no attack, one-touch pollution, low-and-slow
-            rotation and replay pollution, for LRU, S3-FIFO, PrefixShield and
-            the two ablations (no segmentation, no debt gate), with paired
+            rotation and replay pollution, for LRU, S3-FIFO, StaticQuota,
+            PrefixShield and the two ablations (no segmentation, no debt
+            gate), with paired
             bootstrap CIs over seeds (Sec. V-B, Table I; Sec. V-D, Fig. 3)
             The polluter's debt-gated and promoted blocks are reported for
             PrefixShield with and without the gate (Sec. V-D).
@@ -58,7 +59,7 @@ def attacks(seeds, n_requests=4000):
             gate[spec.label][1] += res[k][0][1]["promotions"]
         row = {lab: 100 * float(np.mean(v)) for lab, v in per.items()}
         cmp = {}
-        for a, b in [("prefixshield", "lru"), ("prefixshield", "s3fifo"),
+        for a, b in [("prefixshield", "lru"), ("prefixshield", "s3fifo"), ("prefixshield", "staticquota"),
                      ("prefixshield", "prefixshield_noseg"), ("prefixshield", "prefixshield_nogate")]:
             m, lo, hi = metrics.paired_bootstrap(per[a], per[b])
             cmp[f"{a} - {b}"] = [100 * m, 100 * lo, 100 * hi]
@@ -69,12 +70,14 @@ def attacks(seeds, n_requests=4000):
 
 def benign(seeds, n_requests=100000):
     from . import metrics, tracegen as tg
+    ALL4 = tg.ALL_POLICIES + (tg.POLICY_STATICQUOTA,)
     out = {}
     for name in ("chat", "chat_bursty"):
         if name == "chat":
-            traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests, capacities=[4096])
+            traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests, capacities=[4096],
+                                        policies=ALL4)
         else:
-            traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests)
+            traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests, policies=ALL4)
         res, pr = _run(traces, insts)
         per = defaultdict(list)
         for k, spec in enumerate(insts):

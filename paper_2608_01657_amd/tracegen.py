@@ -499,7 +499,7 @@ def workload(name: str, seeds: Optional[Sequence[int]] = None,
     attack_<kind> the paper-scale attack traces (kind in ATTACK_KINDS),
                   C=511, 4,000 requests, 10 seeds x {LRU, S3-FIFO,
                   PrefixShield, PrefixShield without segmentation, without
-                  the debt gate} -> 50
+                  the debt gate, StaticQuota} -> 60
     selector512x8, selector4096x32
                   one-touch contention from 8 / 32 groups at C = 512 / 4096
                   (the paper's selector measurement sizes), 20,000
@@ -567,6 +567,8 @@ def workload(name: str, seeds: Optional[Sequence[int]] = None,
                                      label="prefixshield_noseg"))
                 inst.append(Instance(t, POLICY_PREFIXSHIELD, 511, flags=FLAG_NO_DEBT_GATE,
                                      label="prefixshield_nogate"))
+            if POLICY_STATICQUOTA not in policies:   # the paper's partitioned baseline (Table I)
+                inst.append(Instance(t, POLICY_STATICQUOTA, 511, label=POLICY_NAMES[POLICY_STATICQUOTA]))
     elif name in ("selector512x8", "selector4096x32"):
         C, G = (512, 8) if name == "selector512x8" else (4096, 32)
         idx = list(seeds) if seeds is not None else list(range(4))

@@ -68,7 +68,7 @@ def test_workspace_size_of_a_valid_batch():
 @pytest.mark.parametrize("field,value,needle", [
     ("capacity", 0, "capacity"),
     ("capacity", P.PC_MAX_CAPACITY + 1, "capacity"),
-    ("policy", 3, "policy"),
+    ("policy", 4, "policy"),
     ("flags", 4, "flags"),
     ("n_contracts", 0, "n_contracts"),
     ("n_contracts", 5, "n_contracts"),

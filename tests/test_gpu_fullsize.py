@@ -104,9 +104,10 @@ def test_delayed_full_length_refill_sweep():
 
 def test_chat_full_length_all_capacities():
     """Capacities up to 16,384 blocks: the larger ones keep their state in the
-    workspace instead of LDS."""
-    traces, insts = tg.workload("chat", seeds=[0, 1])
-    assert all(t.n_req == 100000 for t in traces) and len(insts) == 30
+    workspace instead of LDS.  StaticQuota too: 16 partitions, so at 1,024
+    blocks a 64-block partition truncates most long prompts."""
+    traces, insts = tg.workload("chat", seeds=[0, 1], policies=tg.ALL_POLICIES + (tg.POLICY_STATICQUOTA,))
+    assert all(t.n_req == 100000 for t in traces) and len(insts) == 40
     dts, okeys = _hash_all(traces)
     sample = [k for k, i in enumerate(insts) if i.trace == 0]
     _replay_and_compare(traces, insts, dts, okeys, sample)
@@ -135,10 +136,10 @@ def test_tiers_full_length_all_instances():
 
 def test_attack_traces_all_variants_per_request():
     """The paper-scale attack traces (C = 511), every variant including the
-    two ablations, per-request outputs too."""
+    two ablations and StaticQuota, per-request outputs too."""
     for kind in tg.ATTACK_KINDS:
         traces, insts = tg.workload("attack_" + kind, seeds=[0, 1])
-        assert len(insts) == 10
+        assert len(insts) == 12
         dts, okeys = _hash_all(traces, check_keys=(0, 1))
         b = dv.ReplayBatch(dts, insts, per_request=True)
         b.launch()

@@ -13,7 +13,7 @@ from paper_2608_01657_amd import tracegen as tg
 
 pytestmark = pytest.mark.gpu
 
-POLICIES = [tg.POLICY_LRU, tg.POLICY_S3FIFO, tg.POLICY_PREFIXSHIELD]
+POLICIES = [tg.POLICY_LRU, tg.POLICY_S3FIFO, tg.POLICY_PREFIXSHIELD, tg.POLICY_STATICQUOTA]
 
 
 def _edge_trace(seed=9):
@@ -110,8 +110,8 @@ def test_replay_many_groups():
     run_key_traces(kts, per)
 
 
-def _workload_parity(name, seeds, n_requests, per_request=False, **kw):
-    traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests, **kw)
+def _workload_parity(name, seeds, n_requests, per_request=False, policies=tuple(POLICIES), **kw):
+    traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests, policies=policies, **kw)
     dts = []
     okeys = []
     for tr in traces:

@@ -12,6 +12,8 @@ namespace pcr {
 //  bit 12    S3-FIFO main queue bit 13 resident (cached or being created)
 //  bit 14    pinned by the running request
 //  bit 15    has a live entry in the free-queue log (stamp valid)
+//  bits 16-31  index of the block's entry in the main table (resident
+//              blocks; kept through cuckoo displacement)
 constexpr uint32_t kOwnerMask = 0x3Fu;
 constexpr int kContractShift = 6;
 constexpr int kClsShift = 8;
@@ -20,6 +22,8 @@ constexpr uint32_t kQMain = 1u << 12;
 constexpr uint32_t kRes = 1u << 13;
 constexpr uint32_t kPin = 1u << 14;
 constexpr uint32_t kInLog = 1u << 15;
+constexpr int kTposShift = 16;
+constexpr uint32_t kLowMeta = 0xFFFFu;
 
 constexpr int kProb = 0, kNormal = 1, kReuse = 2;   // Sec. III-A retention classes
 constexpr int kLRU = 0, kS3 = 1, kPS = 2, kSQ = 3;

@@ -554,12 +554,13 @@ struct Replayer {
     // meaning zero) hands out distinct ranks, and rank r takes the r-th free
     // entry of the snapshot -- the emptier bucket first.  `touched` records
     // the counters used, which tclaim_reset puts back to kEmpty after the
-    // next barrier.  False when both buckets are full.
-    DEV bool tclaim(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, const uint32_t (&e)[16],
-                    uint32_t &touched, bool ghost = false, uint32_t gref = 0) {
+    // next barrier.  Returns the entry's index, or kEmpty when both buckets
+    // are full.
+    DEV uint32_t tclaim(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, const uint32_t (&e)[16],
+                        uint32_t &touched, bool ghost = false, uint32_t gref = 0) {
         return tclaim_m(tb, ctr, val, h, free_mask(e, ghost, gref), touched);
     }
-    DEV bool tclaim_m(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, uint32_t fm, uint32_t &touched) {
+    DEV uint32_t tclaim_m(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, uint32_t fm, uint32_t &touched) {
         const uint32_t m1 = fm & 0xFFu, m2 = fm >> 8;
         const bool sec = __builtin_popcount(m2) > __builtin_popcount(m1);
         touched = 0;
@@ -571,11 +572,12 @@ struct Replayer {
             uint32_t r = atomicAdd(&ctr[b], 1u) + 1u;
             if (r < (uint32_t)__builtin_popcount(msk)) {
                 while (r--) msk &= msk - 1u;
-                tb[8 * b + (uint32_t)__builtin_ctz(msk)] = val;
-                return true;
+                const uint32_t at = 8 * b + (uint32_t)__builtin_ctz(msk);
+                tb[at] = val;
+                return at;
             }
         }
-        return false;
+        return kEmpty;
     }
     DEV void tclaim_reset(uint32_t *ctr, const TH &h, uint32_t touched) {
         if (touched & 1u) ctr[h.b1] = kEmpty;
@@ -588,6 +590,8 @@ struct Replayer {
         X.kkey[i] = k;
         X.kmain[i] = main ? 1u : 0u;
     }
+    // the main-table entry of slot s is now at index p
+    DEV void set_tpos(uint32_t s, uint32_t p) { meta[s] = (meta[s] & kLowMeta) | (p << kTposShift); }
     // Serial cuckoo displacement, one thread.  gref: ghost sequence that
     // decides which ghost entries are still live.
     DEV bool kick(uint32_t *tb, bool main, uint32_t val, uint64_t k, uint32_t gref) {
@@ -599,13 +603,18 @@ struct Replayer {
             const TH h = thash(ck, msk, rbmask);
             for (int i = 0; i < 16; ++i) {
                 const uint32_t p = epos(h, i);
-                if (main ? tb[p] == kEmpty : !glive(tb[p], gref)) { tb[p] = cv; return true; }
+                if (main ? tb[p] == kEmpty : !glive(tb[p], gref)) {
+                    tb[p] = cv;
+                    if (main) set_tpos(cv & 0xFFFFu, p);
+                    return true;
+                }
             }
             uint32_t b = (h.b1 == from) ? h.b2 : h.b1;
             if (from == 0xFFFFFFFFu && (it & 1)) b = h.b2;
             const uint32_t w = (uint32_t)(it * 5 + (uint32_t)(ck >> 7)) & 7u;
             const uint32_t victim = tb[8 * b + w];
             tb[8 * b + w] = cv;
+            if (main) set_tpos(cv & 0xFFFFu, 8 * b + w);
             cv = victim;
             ck = main ? key[victim & 0xFFFFu] : gring[victim & grmask];
             from = b;
@@ -653,24 +662,10 @@ struct Replayer {
     }
 
     // ============================================================ eviction core
-    // Before the barrier of a scan step, every thread that may hold a victim
-    // looks up its block's key and the table entry naming its slot (the
-    // table does not change during reclamation, except for the clears of
-    // this same step, which never move an entry).  Returns the entry's
-    // index, or kEmpty.
-    DEV uint32_t victim_entry(bool maybe, uint32_t s, uint64_t &k) const {
-        k = 0;
-        if (!maybe) return kEmpty;
-        k = key[s];
-        const TH h = thash(k, nbmask, rbmask);
-        uint32_t e[16];
-        load_buckets(table, h, e);
-        const uint32_t val = (h.tag << 16) | s;
-        uint32_t loc = kEmpty;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) loc = (loc == kEmpty && e[i] == val) ? epos(h, i) : loc;
-        return loc;
-    }
+    // A resident block's metadata carries the index of its main-table entry
+    // (set where the entry is claimed or displaced), so a victim's entry is
+    // known from the metadata the scan reads anyway.
+    DEV static uint32_t victim_entry(bool maybe, uint32_t mt) { return maybe ? (mt >> kTposShift) : kEmpty; }
     // Victims of one step: thread with v holds victim slot s with metadata mt
     // (vrank = its rank among the step's victims) and its table entry loc.
     // Every thread calls this.
@@ -740,8 +735,7 @@ struct Replayer {
             const uint32_t s = valid ? log[pos & lmask] : 0;
             const uint32_t mt = valid ? meta[s] : 0u;
             const bool live = valid && (mt & kInLog) && stamp[s] == pos;
-            uint64_t vk;
-            const uint32_t loc = victim_entry(live, s, vk);
+            const uint32_t loc = victim_entry(live, mt);
             const BMask lm = bballot1(live);
             const int rk = lm.rank(wid);
             const int tot = lm.count();
@@ -773,8 +767,7 @@ struct Replayer {
             const uint32_t mt = valid ? meta[sl] : 0;
             const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
             const bool match = live && (x < 0 || (int)owner_of(mt) == x) && (s < 0 || (int)cls_of(mt) == s);
-            uint64_t vk;
-            const uint32_t loc = victim_entry(match, sl, vk);
+            const uint32_t loc = victim_entry(match, mt);
             const BMask mm = bballot1(match);
             const int rk = mm.rank(wid);
             const int tot = mm.count();
@@ -955,6 +948,10 @@ struct Replayer {
             const bool valid = pos < lim;
             const uint32_t sl = valid ? log[pos & lmask] : 0;
             const uint32_t mt = valid ? meta[sl] : 0;
+            // a small-queue victim is remembered by the ghost: its key is
+            // read with the metadata, in the same round trip
+            const bool gho = useS && g_cap > 0;
+            const uint64_t kv = (valid && gho) ? key[sl] : 0ull;
             const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
             const bool inQ = live && (useS ? !(mt & kQMain) : (mt & kQMain) != 0);
             const bool cand = inQ && !(mt & kPin);
@@ -963,9 +960,8 @@ struct Replayer {
             // main queue: reinsert (freq > 0) or evict
             const bool mv = cand && (useS ? (int)f >= move_thr : f > 0);
             const bool maybe_ev = cand && !mv;
-            uint64_t vk;
-            const uint32_t loc = victim_entry(maybe_ev, sl, vk);
-            const bool gho = useS && g_cap > 0;
+            const uint32_t loc = victim_entry(maybe_ev, mt);
+            const uint64_t vk = maybe_ev ? kv : 0ull;
             TH hg = {};
             uint32_t gfree = 0;
             if (gho) {
@@ -1051,7 +1047,7 @@ struct Replayer {
                     if (pev && (int64_t)seq + g_cap >= (int64_t)gend) {
                         gring[seq & grmask] = vk;
                         const uint32_t val = (hg.tag << 16) | (seq & grmask);
-                        if (!tclaim_m(gtable, rset, val, hg, gfree, gtouched)) defer_kick(val, vk, false);
+                        if (tclaim_m(gtable, rset, val, hg, gfree, gtouched) == kEmpty) defer_kick(val, vk, false);
                     }
                 }
                 s3_gins += (uint64_t)nev;
@@ -1285,7 +1281,7 @@ struct Replayer {
             }
             // orphans: the old block leaves; its slot and table entry are
             // reused by the new block of the same key
-            if (isOrph) meta[slot] = kPin;
+            if (isOrph) meta[slot] = kPin | (mt & ~kLowMeta);
             if (n > kB) {
                 if (act) posslot[j] = dup ? kNoSlot : (found ? (uint16_t)slot : kNewMark);
             } else {
@@ -1425,16 +1421,22 @@ struct Replayer {
         if (n <= kB && n > 0) {
             // one step, from the lookup's registers
             uint32_t slot = c_slot;
+            // a new block's table entry: claimed now, or (both buckets full)
+            // placed by the displacement pass, which records it then; an
+            // orphan's slot keeps its entry
+            uint32_t tpos = c_mt & ~kLowMeta;
             if (c_isN) {
                 const int i = c_rkN;
                 slot = new_slot(i, nfresh);
                 key[slot] = c_key;
                 hh = c_h;
                 const uint32_t val = (hh.tag << 16) | slot;
-                if (!tclaim_m(table, rset, val, hh, c_fm, touched)) defer_kick(val, c_key, true);
+                const uint32_t at = tclaim_m(table, rset, val, hh, c_fm, touched);
+                if (at == kEmpty) defer_kick(val, c_key, true);
+                tpos = at == kEmpty ? 0u : (at << kTposShift);
             }
             nalloc = c_nmiss;
-            const uint32_t mt = c_new ? mbase : c_mt;
+            const uint32_t mt = c_new ? (mbase | tpos) : c_mt;
             if constexpr (policy == kPS) {
                 if (c_new) pfx[slot] = p;
             }
@@ -1470,7 +1472,8 @@ struct Replayer {
             const bool rl = act && slot != kNoSlot;       // every non-duplicate position
             const bool isNew = rl && j >= hend;           // new block (orphans included)
             const bool isN = slot == kNewMark;            // new block without a slot yet
-            uint32_t mt = (rl && !isNew) ? meta[slot] : 0u;
+            // hits: their metadata; orphans: the table entry their slot keeps
+            uint32_t mt = (rl && !isN) ? meta[slot] : 0u;
             // a new key reads its buckets before the barrier of the ballot
             uint64_t kk = 0;
             uint32_t e[16];
@@ -1483,16 +1486,19 @@ struct Replayer {
             BMask ma[4];
             bballot<4>(pa, ma);
             touched = 0;
+            uint32_t tpos = mt & ~kLowMeta;
             if (isN) {
                 const int i = nalloc + ma[0].rank(wid);
                 slot = new_slot(i, nfresh);
                 key[slot] = kk;
                 const uint32_t val = (hh.tag << 16) | slot;
-                if (!tclaim(table, rset, val, hh, e, touched)) defer_kick(val, kk, true);
+                const uint32_t at = tclaim(table, rset, val, hh, e, touched);
+                if (at == kEmpty) defer_kick(val, kk, true);
+                tpos = at == kEmpty ? 0u : (at << kTposShift);
             }
             nalloc += ma[0].count();
             if (isNew) {
-                mt = mbase;
+                mt = mbase | tpos;
                 if constexpr (policy == kPS) pfx[slot] = p;
             }
             if constexpr (policy == kS3) {

@@ -89,16 +89,13 @@ DEV uint32_t wave_sum32(uint32_t v) {
     for (int m = 32; m; m >>= 1) v += (uint32_t)__shfl_xor((int)v, m);
     return bcast32(v, 0);
 }
-// position of the k-th (0-based) set bit of m (k < popc(m))
+// position of the k-th (0-based) set bit of m (k < popc(m)), in one
+// wavefront step: lane l holds bit l, and the answer is the lane whose bit is
+// set with exactly k set bits below it.  Called with every lane active, with
+// m and k the same in every lane.
 DEV int nth_bit(uint64_t m, int k) {
-    int pos = 0;
-    for (int w = 32; w; w >>= 1) {
-        const uint64_t lowmask = (w == 64) ? ~0ull : ((1ull << w) - 1);
-        const int c = popc(m & lowmask);
-        if (k >= c) { k -= c; m >>= w; pos += w; }
-        else m &= lowmask;
-    }
-    return pos;
+    const bool hit = ((m >> __lane_id()) & 1ull) != 0 && mbcnt(m) == k;
+    return first_bit(ballot(hit));
 }
 // floor(a / b) for 0 < b < 2^63: below 2^53 a double-precision estimate and
 // an exact integer correction (the estimate is off by at most one or two);
@@ -516,6 +513,10 @@ struct Replayer {
     DEV int tprobe(const TH &h, uint32_t &cand, uint32_t &fm) const {
         uint32_t e[16];
         load_buckets(table, h, e);
+        return tscan(h, e, cand, fm);
+    }
+    // tprobe on buckets already loaded
+    DEV int tscan(const TH &h, const uint32_t (&e)[16], uint32_t &cand, uint32_t &fm) const {
         int nm = 0;
         uint32_t cv = 0, f = 0;
 #pragma unroll
@@ -917,10 +918,25 @@ struct Replayer {
     DEV void ghost_sweep() {
         uint32_t ns = (uint32_t)(((uint64_t)kB * gsrate + 0xFFFFu) >> 16);
         if (ns > gne) ns = gne;
-        for (uint32_t i = tid; i < ns; i += kB) {
+        // every read of the first kRounds rounds is issued before any clear
+        // (the host's sizing keeps ns below 700, within 3 rounds of kB; the
+        // loop after them only guards that bound)
+        constexpr int kRounds = 3;
+        uint32_t ev[kRounds];
+#pragma unroll
+        for (int q = 0; q < kRounds; ++q) {
+            const uint32_t i = (uint32_t)(q * kB + tid);
+            ev[q] = i < ns ? gtable[(gsw + i) & (gne - 1u)] : kEmpty;
+        }
+#pragma unroll
+        for (int q = 0; q < kRounds; ++q) {
+            const uint32_t i = (uint32_t)(q * kB + tid);
+            if (ev[q] != kEmpty && !glive(ev[q], gseq)) gtable[(gsw + i) & (gne - 1u)] = kEmpty;
+        }
+        for (uint32_t i = (uint32_t)(kRounds * kB + tid); i < ns; i += kB) {
             const uint32_t ix = (gsw + i) & (gne - 1u);
-            const uint32_t ev = gtable[ix];
-            if (ev != kEmpty && !glive(ev, gseq)) gtable[ix] = kEmpty;
+            const uint32_t e = gtable[ix];
+            if (e != kEmpty && !glive(e, gseq)) gtable[ix] = kEmpty;
         }
         gsw += ns;
     }
@@ -1179,6 +1195,10 @@ struct Replayer {
             const uint64_t k = kcur;
             if (base + kB < n) kcur = (j + kB < n) ? tkeys[ko + j + kB] : 0ull;   // next step in flight
             const TH h = thash(k, nbmask, rbmask);
+            // the table buckets load first: their latency overlaps the
+            // duplicate-set claim below
+            uint32_t te[16];
+            if (act) load_buckets(table, h, te);
             // file (tag, position) in the request's duplicate set: the first
             // bucket with room along r1, r2, r2+1, ... (a claim counter each)
             uint32_t rpos = 0, nhop = 0;
@@ -1198,7 +1218,14 @@ struct Replayer {
             }
             // resident lookup of every key (also of duplicates: harmless)
             uint32_t cand = 0, fm = 0;
-            const int ntag = act ? tprobe(h, cand, fm) : 0;
+            const int ntag = act ? tscan(h, te, cand, fm) : 0;
+            // key, metadata and prefix id of the candidate in one round trip,
+            // before the barrier: nothing writes them between the probe and
+            // the ballot, except an earlier step of this request, whose slots
+            // a non-duplicate key never names (a duplicate ignores them)
+            const uint64_t ck = ntag == 1 ? key[cand] : 0ull;
+            uint32_t mt = ntag == 1 ? meta[cand] : 0u;
+            const uint32_t cp = (policy == kPS && ntag == 1) ? pfx[cand] : 0u;
             bsync();
             // duplicate: an earlier position holds the same key.  It was filed
             // along the same bucket sequence, no later than the first bucket
@@ -1220,10 +1247,6 @@ struct Replayer {
                 }
             }
             const bool nd = act && !dup;
-            // key, metadata and prefix id of the candidate in one round trip
-            const uint64_t ck = ntag == 1 ? key[cand] : 0ull;
-            uint32_t mt = ntag == 1 ? meta[cand] : 0u;
-            const uint32_t cp = (policy == kPS && ntag == 1) ? pfx[cand] : 0u;
             int fs = (ntag == 1 && ck == k) ? (int)cand : -1;
             if (ntag > 1) {
                 fs = tfind_slow(k, h);

@@ -72,22 +72,46 @@ DEV int64_t bcast64(int64_t v, int l) {
     uint32_t hi = bcast32((uint32_t)((uint64_t)v >> 32), l);
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
-DEV int64_t xor64(int64_t v, int m) {
-    uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)(uint64_t)v, m);
-    uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)((uint64_t)v >> 32), m);
+// Wavefront reductions in DPP steps (no LDS): an inclusive scan under the
+// operation -- within each row of 16 lanes (row_shr 1, 2, 4, 8), then rows 1
+// and 3 take the last lane of the row before them (row_bcast:15), then rows 2
+// and 3 take lane 31 (row_bcast:31) -- leaves the result in lane 63.  A lane
+// with no source lane keeps `old`.  Called with every lane active.
+template <int kCtrl, int kRowMask>
+DEV uint32_t dpp32(uint32_t old, uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, kCtrl, kRowMask, 0xF, false);
+}
+template <int kCtrl, int kRowMask>
+DEV int64_t dpp64(int64_t old, int64_t v) {
+    const uint32_t lo = dpp32<kCtrl, kRowMask>((uint32_t)(uint64_t)old, (uint32_t)(uint64_t)v);
+    const uint32_t hi = dpp32<kCtrl, kRowMask>((uint32_t)((uint64_t)old >> 32), (uint32_t)((uint64_t)v >> 32));
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
+#define PC_WAVE_SCAN(v, OP, DPP, IDENT)                   \
+    do {                                                  \
+        v = OP(v, DPP<0x111, 0xF>(IDENT, v));             \
+        v = OP(v, DPP<0x112, 0xF>(IDENT, v));             \
+        v = OP(v, DPP<0x114, 0xF>(IDENT, v));             \
+        v = OP(v, DPP<0x118, 0xF>(IDENT, v));             \
+        v = OP(v, DPP<0x142, 0xA>(IDENT, v));             \
+        v = OP(v, DPP<0x143, 0xC>(IDENT, v));             \
+    } while (0)
+DEV int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+DEV uint32_t min32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+DEV uint32_t add32(uint32_t a, uint32_t b) { return a + b; }
 DEV int64_t wave_max64(int64_t v) {
-    for (int m = 32; m; m >>= 1) { int64_t u = xor64(v, m); v = u > v ? u : v; }
-    return bcast64(v, 0);
+    const int64_t own = v;
+    PC_WAVE_SCAN(v, max64, dpp64, own);
+    return bcast64(v, 63);
 }
 DEV uint32_t wave_min32(uint32_t v) {
-    for (int m = 32; m; m >>= 1) { uint32_t u = (uint32_t)__shfl_xor((int)v, m); v = u < v ? u : v; }
-    return bcast32(v, 0);
+    const uint32_t own = v;
+    PC_WAVE_SCAN(v, min32, dpp32, own);
+    return bcast32(v, 63);
 }
 DEV uint32_t wave_sum32(uint32_t v) {
-    for (int m = 32; m; m >>= 1) v += (uint32_t)__shfl_xor((int)v, m);
-    return bcast32(v, 0);
+    PC_WAVE_SCAN(v, add32, dpp32, 0u);
+    return bcast32(v, 63);
 }
 // position of the k-th (0-based) set bit of m (k < popc(m)), in one
 // wavefront step: lane l holds bit l, and the answer is the lane whose bit is

@@ -45,6 +45,8 @@
 // cursor; S3-FIFO processes queue heads 256 at a time and cuts each batch
 // where the one-at-a-time rule would switch queues.  Each shortcut
 // reproduces the one-victim-at-a-time definition exactly.
+#include <cstddef>
+
 #include "pc_internal.h"
 
 namespace pcr {
@@ -238,7 +240,7 @@ struct BMask {
 struct Coll {
     unsigned long long m[2][8][kW];   // block ballots, double-buffered
     uint32_t novf;                    // pending cuckoo displacements
-    uint32_t qf;                      // prior-reference / admitted bits of the request
+    uint32_t qf;                      // prior-reference / admitted bits of the request (read with novf)
     uint32_t nghost;                  // ghost hits among the request's new blocks
     int32_t kerr;                     // displacement failure
     uint32_t pad;
@@ -251,6 +253,8 @@ struct Coll {
     uint64_t pcnt[8];                 // event counts (thread 0)
 #endif
 };
+static_assert(offsetof(Coll, qf) == offsetof(Coll, novf) + 4 && offsetof(Coll, novf) % 8 == 0,
+              "novf and qf are read together as one 64-bit word");
 
 // Key -> two table buckets, 16-bit tag (never 0xFFFF, so empty entries never
 // match a tag), two duplicate-set buckets.  Keys are usually hash outputs
@@ -1190,9 +1194,14 @@ struct Replayer {
 
         // ---- OnRequest (Alg. 1): prior reference of (g,p), then record it.
         // Thread 0 owns the prefix bitmaps and publishes this request's two
-        // bits through LDS (X.qf, written before the last barrier).
+        // bits through LDS (X.qf, written before the last barrier).  The
+        // same read returns the number of table entries the previous
+        // request's insert left for the displacement pass (X.novf, next to
+        // X.qf): they are placed here, before this lookup reads the table.
         const uint32_t w = p >> 5, bit = 1u << (p & 31);
-        const uint32_t qf = rfl(X.qf);
+        const uint64_t nq = rfl64(*reinterpret_cast<const uint64_t *>(&X.novf));
+        if ((uint32_t)nq != 0u) kick_pending();
+        const uint32_t qf = (uint32_t)(nq >> 32);
         const bool q1 = (qf & 1u) != 0, adm = (qf & 2u) != 0;
         if (me) { c_req += 1; c_probe += (uint64_t)n; c_trunc += (uint64_t)(nfull - n); }
         const bool proven = q1 && adm;
@@ -1586,7 +1595,8 @@ struct Replayer {
         if constexpr (policy == kS3) gsync();   // ghost-ring writes of this request are visible
         else bsync();
         tclaim_reset(rset, hh, touched);
-        kick_pending();
+        // entries that found both buckets full are placed by the next
+        // request before its lookup (or after the last request)
         slots_taken(nalloc, nfresh);
         if (m > 0) {
             if (tid == 0) atomicAdd(&res[g], (uint32_t)m);
@@ -1713,6 +1723,10 @@ struct Replayer {
             q = nx;
             nx = nn;
         }
+        // table entries the last request left for the displacement pass
+        // (only their failure matters now: it is an internal error)
+        kick_pending();
+        if (err && status == 0) status = err;
         // the last completed request's quadruple (the others were written
         // while the request after them ran)
         if (preq && tid == 0 && done > pr_next) put_per_request(done - 1);

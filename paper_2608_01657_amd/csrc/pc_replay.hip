@@ -1445,14 +1445,21 @@ struct Replayer {
         if (m > 0) {
             uint32_t cl = 0;
             if (me) {
+                if (K == 1) {   // one contract (c = 0): no selection
+                    const int64_t B = eff(0, t) - (int64_t)m * kScale;
+                    bal[0] = B;
+                    last[0] = t;
+                    cl = (B < -eps || !adm) ? (uint32_t)kProb : (uint32_t)kNormal;
+                } else {
 #pragma unroll
-                for (int cc = 0; cc < 4; ++cc)
-                    if (cc == c) {
-                        const int64_t B = eff(cc, t) - (int64_t)m * kScale;
-                        bal[cc] = B;
-                        last[cc] = t;
-                        cl = (B < -eps || !adm) ? (uint32_t)kProb : (uint32_t)kNormal;
-                    }
+                    for (int cc = 0; cc < 4; ++cc)
+                        if (cc == c) {
+                            const int64_t B = eff(cc, t) - (int64_t)m * kScale;
+                            bal[cc] = B;
+                            last[cc] = t;
+                            cl = (B < -eps || !adm) ? (uint32_t)kProb : (uint32_t)kNormal;
+                        }
+                }
                 c_charged += (uint64_t)m;
             }
             cls_new = bcast32(cl, g);

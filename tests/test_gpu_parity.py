@@ -188,3 +188,23 @@ def test_block_offsets_sizes(n):
     dv.pc_block_offsets(d_len, d_off)
     torch.cuda.synchronize()
     assert np.array_equal(d_off.cpu().numpy(), oracle.block_offsets(lens))
+
+
+def test_replay_last_request_displacements():
+    """Table entries that find both buckets full are placed by the next
+    request, or after the last one.  Traces whose final requests insert a
+    full cache of fresh keys at the table's design load (C = 85: 16 buckets of
+    8, load 2/3) leave such entries behind; every policy must still match the
+    oracle with status 0."""
+    kts, per = [], []
+    for seed in range(16):
+        rng = np.random.default_rng(500 + seed)
+        C = 85
+        reqs = [list(rng.integers(1, 2**63, C, dtype=np.int64)) for _ in range(4)]
+        keys = np.array([k for r in reqs for k in r], dtype=np.int64).view(np.uint64)
+        off = np.arange(0, C * len(reqs) + 1, C, dtype=np.int64)
+        R = len(reqs)
+        kts.append(tg.KeyTrace(keys, off, np.zeros(R, np.uint8), np.zeros(R, np.uint8),
+                               np.arange(R, dtype=np.uint32), 1, R))
+        per.append([tg.Instance(0, pol, C) for pol in POLICIES])
+    run_key_traces(kts, per)

@@ -208,3 +208,55 @@ def test_replay_last_request_displacements():
                                np.arange(R, dtype=np.uint32), 1, R))
         per.append([tg.Instance(0, pol, C) for pol in POLICIES])
     run_key_traces(kts, per)
+
+
+def _append_requests(kt, reqs, group=0):
+    """KeyTrace `kt` followed by the requests `reqs` (lists of keys)."""
+    keys = np.concatenate([kt.keys] + [np.asarray(r, np.uint64) for r in reqs])
+    off = np.concatenate([kt.key_off, kt.key_off[-1] + np.cumsum([len(r) for r in reqs])]).astype(np.int64)
+    R = len(reqs)
+    return tg.KeyTrace(keys, off, np.concatenate([kt.group, np.full(R, group, np.uint8)]),
+                       np.concatenate([kt.contract, np.zeros(R, np.uint8)]),
+                       np.concatenate([kt.prefix, np.zeros(R, np.uint32)]), kt.n_groups, kt.n_prefix)
+
+
+def test_replay_max_capacity():
+    """C = PC_MAX_CAPACITY: the state lives in the workspace, the main table
+    has 2^16 entries (every bit of the entry index kept in a slot's metadata
+    word is used), the S3 ghost ring is at its 2^16 cap, and two final
+    requests are longer than the cache (33,000 fresh keys, then the same
+    keys again), so admission truncates."""
+    from paper_2608_01657_amd import PC_MAX_CAPACITY
+    C = PC_MAX_CAPACITY
+    rng = np.random.default_rng(4242)
+    kt = tg.random_key_trace(77, n_req=200, max_blocks=1500, n_groups=4, n_prefix=16, n_contracts=2,
+                             key_universe=60000)
+    long_req = list(rng.integers(1 << 40, 1 << 62, 33000, dtype=np.int64))
+    kt = _append_requests(kt, [long_req, long_req], group=1)
+    contracts = [(tg.Q16, 4 * tg.Q16), (tg.Q16 // 2, 0)]
+    insts = [tg.Instance(0, tg.POLICY_LRU, C, contracts=contracts),
+             tg.Instance(0, tg.POLICY_STATICQUOTA, C, contracts=contracts),
+             tg.Instance(0, tg.POLICY_S3FIFO, C, contracts=contracts, s3_small_permille=100),
+             tg.Instance(0, tg.POLICY_S3FIFO, C, contracts=contracts, s3_small_permille=500, s3_move_threshold=2)]
+    insts += [tg.Instance(0, tg.POLICY_PREFIXSHIELD, C, contracts=contracts, flags=f, eps_q16=tg.Q16 // 2)
+              for f in [0, 1, 2, 3]]
+    res = run_key_traces([kt], [insts])
+    for (groups, inst, _), spec in zip(res, insts):
+        assert sum(g["truncated"] for g in groups) > 0, tg.POLICY_NAMES[spec.policy]
+        assert inst["resident_max"] <= C
+
+
+def test_replay_empty_and_blockless_traces():
+    """A trace with no requests, and one whose requests hold no full block
+    (zero keys each): every counter except the request counts stays zero,
+    on both sides, for every policy."""
+    empty = tg.KeyTrace(np.zeros(0, np.uint64), np.zeros(1, np.int64), np.zeros(0, np.uint8),
+                        np.zeros(0, np.uint8), np.zeros(0, np.uint32), 1, 1)
+    R = 9
+    blockless = tg.KeyTrace(np.zeros(0, np.uint64), np.zeros(R + 1, np.int64), (np.arange(R) % 3).astype(np.uint8),
+                            np.zeros(R, np.uint8), np.arange(R, dtype=np.uint32), 3, R)
+    per = [[tg.Instance(0, pol, cap) for pol in POLICIES for cap in (1, 100)] for _ in range(2)]
+    res = run_key_traces([empty, blockless], per)
+    for groups, inst, _ in res:
+        assert all(v == 0 for v in inst.values())
+        assert all(v == 0 for g in groups for k, v in g.items() if k != "requests")

@@ -9,8 +9,10 @@
 //   c_k   = fmix64(d_k)
 //   H_k   = A * H_{k-1} + c_k  (mod 2^64),  H_-1 = fmix64(ns + 1)
 //   key_k = fmix64(H_k)
-// The chain is an affine recurrence, so a wavefront computes 64 consecutive
-// H_k with a log-step scan over lanes instead of a serial loop.
+// The chain is an affine recurrence with an odd multiplier, so it unrolls to
+//   H_k = A^k (A H_-1 + sum_{j<=k} A^-j c_j)   (A^-1: the inverse of A mod 2^64)
+// and a wavefront computes 64 consecutive H_k as a plain prefix sum of
+// A^-j c_j between two per-lane multiplications, instead of a serial loop.
 #include "pc_internal.h"
 
 namespace pcr {
@@ -34,14 +36,31 @@ constexpr uint64_t pow_a(int e) {
     }
     return r;
 }
-constexpr uint64_t kA1 = pow_a(1), kA2 = pow_a(2), kA4 = pow_a(4), kA8 = pow_a(8);
+constexpr uint64_t kA1 = pow_a(1);
 
-// A^0 .. A^32: the per-lane multipliers of the scan's cross-row steps
-__constant__ uint64_t kApow[33] = {
-    pow_a(0),  pow_a(1),  pow_a(2),  pow_a(3),  pow_a(4),  pow_a(5),  pow_a(6),  pow_a(7),  pow_a(8),
-    pow_a(9),  pow_a(10), pow_a(11), pow_a(12), pow_a(13), pow_a(14), pow_a(15), pow_a(16), pow_a(17),
-    pow_a(18), pow_a(19), pow_a(20), pow_a(21), pow_a(22), pow_a(23), pow_a(24), pow_a(25), pow_a(26),
-    pow_a(27), pow_a(28), pow_a(29), pow_a(30), pow_a(31), pow_a(32)};
+// A^-1 mod 2^64 by Newton's iteration x <- x (2 - A x): A x = 1 holds mod 2^3
+// for x = A (A odd), and every step doubles the number of correct bits.
+constexpr uint64_t inv_a() {
+    uint64_t x = kA;
+    for (int i = 0; i < 6; ++i) x *= 2 - kA * x;
+    return x;
+}
+constexpr uint64_t kAinv = inv_a();
+static_assert(kA * kAinv == 1, "A^-1 mod 2^64");
+
+// b^0 .. b^63: the per-lane multipliers A^L and A^-L of lane L
+struct PowTab {
+    uint64_t v[64];
+    constexpr explicit PowTab(uint64_t b) : v() {
+        uint64_t x = 1;
+        for (int i = 0; i < 64; ++i) {
+            v[i] = x;
+            x *= b;
+        }
+    }
+};
+__constant__ PowTab kApowL = PowTab(kA);
+__constant__ PowTab kAinvL = PowTab(kAinv);
 
 #define GLOBAL __attribute__((address_space(1)))
 
@@ -215,7 +234,7 @@ __device__ __forceinline__ void issue(Step &S, const GLOBAL int32_t *__restrict_
 // Keys of one 64-block step from its loaded tokens; H carries H_{k-1} of
 // the step's first block in and the last block's H_k out.
 __device__ __forceinline__ void step_keys(const Step &S, int nblk, int lane, int r4, uint32_t k0, uint32_t k1,
-                                          uint32_t k2, uint32_t k3, int src, uint64_t arow, uint64_t a31,
+                                          uint32_t k2, uint32_t k3, int src, uint64_t apw, uint64_t ainv,
                                           uint64_t &H, GLOBAL uint64_t *__restrict__ out) {
     uint64_t dsel = 0;
 #pragma unroll
@@ -227,17 +246,11 @@ __device__ __forceinline__ void step_keys(const Step &S, int nblk, int lane, int
         if (q == r4) dsel = part;      // lane 4b+q keeps block 16q+b
     }
     const uint64_t c = fmix64(dsel);
-    uint64_t v = shfl64(c, src);       // lane L now holds c of block L of the step
-    if (lane == 0) v += kA1 * H;
-    // inclusive scan of H_L = A*H_{L-1} + c_L over the 64 lanes: within each
-    // row of 16 lanes (v_L += A^d v_{L-d}), then rows 1 and 3 take the last
-    // lane of the row before them, then rows 2 and 3 take lane 31
-    v += kA1 * dpp64<0x111, 0xF>(v);
-    v += kA2 * dpp64<0x112, 0xF>(v);
-    v += kA4 * dpp64<0x114, 0xF>(v);
-    v += kA8 * dpp64<0x118, 0xF>(v);
-    v += arow * dpp64<0x142, 0xA>(v);
-    v += a31 * dpp64<0x143, 0xC>(v);
+    // lane L now holds A^-L c of block L of the step; lane 0 also carries
+    // the chain in: H_L = A^L (A H + sum_{j<=L} A^-j c_j)
+    uint64_t u = shfl64(c, src) * ainv;
+    if (lane == 0) u += kA1 * H;
+    const uint64_t v = (uint64_t)wave_scan_add64((int64_t)u) * apw;
     H = readlane64(v, nblk - 1);
     // every lane stores (no branch, so the compiler can count the loads in
     // flight exactly): lanes past the last block write the last block's key
@@ -253,17 +266,16 @@ __device__ __forceinline__ void hash_request(const GLOBAL int32_t *__restrict__ 
     const int r4 = lane & 3, bq = lane >> 2;
     const uint32_t k0 = kNH[4 * r4], k1 = kNH[4 * r4 + 1], k2 = kNH[4 * r4 + 2], k3 = kNH[4 * r4 + 3];
     const int src = 4 * (lane & 15) + (lane >> 4);      // lane holding block `lane`'s digest
-    const uint64_t arow = kApow[(lane & 15) + 1];       // A^(position in row + 1)
-    const uint64_t a31 = kApow[lane >= 32 ? lane - 31 : 0];
+    const uint64_t apw = kApowL.v[lane], ainv = kAinvL.v[lane];
     Step S0, S1;
     issue(S0, tok, 0, nb, bq, r4);
     for (int32_t it = 0;;) {
         issue(S1, tok, it + 64, nb, bq, r4);
-        step_keys(S0, nb - it < 64 ? nb - it : 64, lane, r4, k0, k1, k2, k3, src, arow, a31, H, out + it);
+        step_keys(S0, nb - it < 64 ? nb - it : 64, lane, r4, k0, k1, k2, k3, src, apw, ainv, H, out + it);
         it += 64;
         if (it >= nb) break;
         issue(S0, tok, it + 64, nb, bq, r4);
-        step_keys(S1, nb - it < 64 ? nb - it : 64, lane, r4, k0, k1, k2, k3, src, arow, a31, H, out + it);
+        step_keys(S1, nb - it < 64 ? nb - it : 64, lane, r4, k0, k1, k2, k3, src, apw, ainv, H, out + it);
         it += 64;
         if (it >= nb) break;
     }

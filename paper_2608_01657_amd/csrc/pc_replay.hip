@@ -185,22 +185,33 @@ struct BMask {
         for (int i = 0; i < kW; ++i) a |= w[i];
         return a != 0;
     }
-    // thread index (wid*64+lane) of the first set bit, or kB
+    // thread index (wid*64+lane) of the first set bit, or kB.  Selects, not
+    // branches: the masks are wave-uniform, and a branch per word costs more
+    // than the word's find-first-set.
     DEV int first() const {
+        int r = kB;
 #pragma unroll
-        for (int i = 0; i < kW; ++i)
-            if (w[i]) return 64 * i + first_bit(w[i]);
-        return kB;
+        for (int i = kW - 1; i >= 0; --i) r = w[i] ? 64 * i + first_bit(w[i]) : r;
+        return r;
     }
-    // thread index of the k-th set bit (k < count())
+    // thread index of the k-th set bit (k < count()), or kB: the word that
+    // holds it is picked by running popcounts, then one lane-parallel step
+    // finds the bit.  Called with every lane active.
     DEV int nth(int k) const {
+        uint64_t sel = 0;
+        int off = kB;
+        bool done = false;
 #pragma unroll
         for (int i = 0; i < kW; ++i) {
             const int c = popc(w[i]);
-            if (k < c) return 64 * i + nth_bit(w[i], k);
-            k -= c;
+            const bool take = !done && k < c;
+            sel = take ? w[i] : sel;
+            off = take ? 64 * i : off;
+            k = (!done && !take) ? k - c : k;
+            done = done || take;
         }
-        return kB;
+        const int b = nth_bit(sel, k);
+        return done ? off + b : kB;
     }
     // keep only bits of threads below index t
     DEV BMask below(int t) const {
@@ -983,6 +994,12 @@ struct Replayer {
                 spS = curS; spM = curM;
                 keptS = keptM = 0xFFFFFFFFu;
             }
+            // the queue sizes are wave-uniform; saying so keeps the batch
+            // cut below in scalar code instead of exec-masked vector code
+            rem = (int)rfl((uint32_t)rem);
+            s_size = (int)rfl((uint32_t)s_size);
+            s_unp = (int)rfl((uint32_t)s_unp);
+            m_unp = (int)rfl((uint32_t)m_unp);
             const bool useS = (s_size >= s_cap && s_unp > 0) || (m_unp == 0);
             PROF_COUNT(2, 1);
             const uint32_t sp = useS ? spS : spM;

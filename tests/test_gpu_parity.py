@@ -260,3 +260,41 @@ def test_replay_empty_and_blockless_traces():
     for groups, inst, _ in res:
         assert all(v == 0 for v in inst.values())
         assert all(v == 0 for g in groups for k, v in g.items() if k != "requests")
+
+
+def test_hash_out_of_range_requests_are_skipped():
+    """A request whose token range leaves the token buffer, whose length or
+    offset is negative, or whose keys would pass n_keys, sets the status to
+    PC_EINVAL and writes nothing; every other request still gets its keys."""
+    import torch
+    import paper_2608_01657_amd as P
+    rng = np.random.default_rng(21)
+    R = 40
+    lens = rng.integers(0, 3000, R).astype(np.int32)
+    toks = rng.integers(0, 32000, int(lens.sum()) + 64, dtype=np.int64).astype(np.int32)
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    lens[-1] = max(int(lens[-1]), 64)              # the last request has keys
+    bad = {5: "tokens", 17: "length", 30: "offset", R - 1: "keys"}
+    offs[5] = len(toks) - 10                       # runs past the token buffer
+    lens[5] = 100
+    lens[17] = -5
+    offs[30] = -3
+    key_off = oracle.block_offsets(lens)
+    n_keys = int(key_off[-1]) - 1                  # the last request's keys do not fit
+    ns = (np.arange(R) % 5).astype(np.int32)
+    dev = torch.device("cuda")
+    sentinel = 0x5A5A5A5A5A5A5A5A
+    d_keys = torch.full((n_keys,), sentinel, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    P.pc_hash_blocks(torch.from_numpy(toks).to(dev), torch.from_numpy(offs).to(dev),
+                     torch.from_numpy(lens).to(dev), torch.from_numpy(ns).to(dev),
+                     torch.from_numpy(key_off).to(dev), d_keys, status, None)
+    assert int(status.item()) == P.PC_EINVAL
+    keys = d_keys.cpu().numpy()
+    for r in range(R):
+        a, b = int(key_off[r]), min(int(key_off[r + 1]), n_keys)
+        if r in bad:
+            assert np.all(keys[a:b] == sentinel), f"request {r} ({bad[r]}) wrote keys"
+            continue
+        want = oracle.hash_request(toks[offs[r]:offs[r] + lens[r]], int(ns[r])).view(np.int64)
+        assert np.array_equal(keys[a:b], want), f"request {r}"

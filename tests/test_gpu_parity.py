@@ -298,3 +298,53 @@ def test_hash_out_of_range_requests_are_skipped():
             continue
         want = oracle.hash_request(toks[offs[r]:offs[r] + lens[r]], int(ns[r])).view(np.int64)
         assert np.array_equal(keys[a:b], want), f"request {r}"
+
+
+def _prefix_trace(kt, k):
+    """The first k requests of key trace kt."""
+    return tg.KeyTrace(kt.keys[:int(kt.key_off[k])], kt.key_off[:k + 1].copy(), kt.group[:k].copy(),
+                       kt.contract[:k].copy(), kt.prefix[:k].copy(), kt.n_groups, kt.n_prefix,
+                       None if kt.tick is None else kt.tick[:k].copy())
+
+
+def test_replay_malformed_request_stops_the_instance():
+    """A request with a group, contract or prefix id out of range, or a tick
+    below the previous one, stops its instance: status PC_EINVAL, every
+    counter zero, the quadruples of the requests before it as the oracle
+    gives them for that prefix of the trace; an instance of a well-formed
+    trace in the same batch is unaffected."""
+    import paper_2608_01657_amd as P
+    base = tg.random_key_trace(4040, n_req=80, max_blocks=24, n_groups=3, n_prefix=9, n_contracts=2,
+                               key_universe=60, with_ticks=True)
+    k = 50
+    kts, what = [base], ["well-formed"]
+    for kind in ["group", "contract", "prefix", "tick"]:
+        kt = tg.KeyTrace(base.keys.copy(), base.key_off.copy(), base.group.copy(), base.contract.copy(),
+                         base.prefix.copy(), base.n_groups, base.n_prefix, base.tick.copy())
+        if kind == "group":
+            kt.group[k] = 3
+        elif kind == "contract":
+            kt.contract[k] = 2
+        elif kind == "prefix":
+            kt.prefix[k] = base.n_prefix
+        else:
+            kt.tick[k] = kt.tick[k - 1] - 1
+        kts.append(kt)
+        what.append(kind)
+    contracts = [(tg.Q16, 8 * tg.Q16), (tg.Q16 // 3, 2 * tg.Q16)]
+    dts = [dv.upload_keys(kt) for kt in kts]
+    insts = [tg.Instance(ti, pol, 40, contracts=contracts) for ti in range(len(kts)) for pol in POLICIES]
+    res, pr = replay_gpu(dts, insts, per_request=True)
+    for j, inst in enumerate(insts):
+        label = f"{what[inst.trace]} trace, {tg.POLICY_NAMES[inst.policy]}"
+        groups, istats, status = res[j]
+        if inst.trace == 0:
+            o = oracle.replay_key_trace(kts[0], inst, per_request=True)
+            assert_same(res[j], o, label)
+            assert np.array_equal(pr[j], o.per_request), label
+            continue
+        assert status == P.PC_EINVAL, label
+        assert all(v == 0 for v in istats.values()), label
+        assert all(v == 0 for g in groups for v in g.values()), label
+        o = oracle.replay_key_trace(_prefix_trace(kts[inst.trace], k), inst, per_request=True)
+        assert np.array_equal(pr[j][:k], o.per_request), label

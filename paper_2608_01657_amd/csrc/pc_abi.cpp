@@ -157,8 +157,10 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         d.log_log2 = ceil_log2(s.capacity + maxn + 128);
         if (s.policy == PC_S3FIFO && d.g_cap > 0) {
             d.gnb_log2 = std::max(1, ceil_log2((int64_t)d.g_cap * 3 / 16 + 1));
-            // ghost ring: 2 g_cap + 256 positions (at most 2^16), see the ghost sweep
-            d.gr_log2 = std::min(16, ceil_log2(2 * (int64_t)d.g_cap + 256));
+            // ghost ring: 4 g_cap + 256 positions (at most 2^16), see the ghost
+            // sweep: any ring of at least 2 g_cap + 256 gives the same ghost; a
+            // longer one (HBM) lets each scan batch sweep fewer table entries
+            d.gr_log2 = std::min(16, ceil_log2(4 * (int64_t)d.g_cap + 256));
         }
         // request duplicate set: 8-entry buckets, at most half full; between
         // lookups it also holds the per-bucket claim counters of both tables

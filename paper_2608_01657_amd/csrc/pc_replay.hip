@@ -930,7 +930,9 @@ struct Replayer {
     // Between two visits of an entry fewer than 256 + span insertions happen,
     // so an entry seen live at one visit (age < g_cap) has age below
     // g_cap + 256 + span = 2^gr when it is seen next, and is cleared then if
-    // dead.  (2^gr = min(2^16, next power of two >= 2 g_cap + 256).)
+    // dead.  Any 2^gr of at least 2 g_cap + 256 works (span >= g_cap); the
+    // host takes min(2^16, next power of two >= 4 g_cap + 256), so span is
+    // at least 3 g_cap and the sweep proportionally lighter.
     DEV bool glive(uint32_t e, uint32_t gref) const {
         return e != kEmpty && ((gref - 1u - (e & 0xFFFFu)) & grmask) < (uint32_t)g_cap;
     }

@@ -65,8 +65,8 @@ int32_t pc_block_offsets(const int32_t *d_req_len, int64_t n_req, int32_t block_
  * where fmix64 is the MurmurHash3 finalizer, A = 0x9E3779B97F4A7C15 and
  * K[i] = floor(frac(sqrt(p_i)) * 2^31) + 1 for the first 16 primes.
  *
- *   d_tokens   [n_tokens] int32; a request may start at any token, and
- *              requests may alias.
+ *   d_tokens   [n_tokens] int32, 4-byte aligned (else PC_EINVAL); a
+ *              request may start at any token, and requests may alias.
  *   d_req_tok_off, d_req_len, d_req_ns  [n_req]: start, length, namespace.
  *   d_key_off  [n_req+1] output of pc_block_offsets (or any offsets with
  *              room for floor(len/16) keys per request).

@@ -254,7 +254,7 @@ int32_t pc_hash_blocks(const int32_t *d_tokens, int64_t n_tokens, const int64_t 
         return fail(PC_EINVAL, "null request array");
     if (n_tokens > 0 && !d_tokens) return fail(PC_EINVAL, "null tokens");
     if (n_keys > 0 && !d_keys) return fail(PC_EINVAL, "null keys");
-    if (((uintptr_t)d_tokens & 15) != 0) return fail(PC_EINVAL, "d_tokens must be 16-byte aligned");
+    if (((uintptr_t)d_tokens & 3) != 0) return fail(PC_EINVAL, "d_tokens must be 4-byte aligned");
     hipError_t e = pcr::launch_hash(d_tokens, n_tokens, d_req_tok_off, d_req_len, d_req_ns, d_key_off, n_req, d_keys,
                                     n_keys, d_status, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "hash launch");

@@ -114,7 +114,8 @@ def test_hash_rejects_before_launch():
     # only 16-token blocks are implemented
     assert lib.pc_hash_blocks(FAKE, 64, FAKE, FAKE, FAKE, FAKE, 1, 32, FAKE, 4, st, None) == P.PC_EUNSUPPORTED
     assert lib.pc_hash_blocks(FAKE, 64, FAKE, FAKE, FAKE, FAKE, 1, 16, FAKE, 4, None, None) == P.PC_EINVAL
-    assert lib.pc_hash_blocks(FAKE + 4, 64, FAKE, FAKE, FAKE, FAKE, 1, 16, FAKE, 4, st, None) == P.PC_EINVAL
+    # tokens are int32: a buffer off 4-byte alignment is refused
+    assert lib.pc_hash_blocks(FAKE + 2, 64, FAKE, FAKE, FAKE, FAKE, 1, 16, FAKE, 4, st, None) == P.PC_EINVAL
     assert lib.pc_hash_blocks(FAKE, -1, FAKE, FAKE, FAKE, FAKE, 1, 16, FAKE, 4, st, None) == P.PC_EINVAL
     assert lib.pc_block_offsets(FAKE, 4, 8, FAKE, None) == P.PC_EUNSUPPORTED
 

@@ -348,3 +348,31 @@ def test_replay_malformed_request_stops_the_instance():
         assert all(v == 0 for g in groups for v in g.values()), label
         o = oracle.replay_key_trace(_prefix_trace(kts[inst.trace], k), inst, per_request=True)
         assert np.array_equal(pr[j][:k], o.per_request), label
+
+
+def test_hash_token_buffer_at_any_int32_offset():
+    """The token buffer itself may start at any int32 (the kernel's token
+    loads assume 4-byte alignment only): the same requests hashed from views
+    that start 0..3 tokens into an allocation give the oracle's keys."""
+    import torch
+    import paper_2608_01657_amd as P
+    rng = np.random.default_rng(77)
+    lens = rng.integers(0, 2500, 30).astype(np.int32)
+    toks = rng.integers(-2**31, 2**31, int(lens.sum()) + 8, dtype=np.int64).astype(np.int32)
+    offs = np.concatenate([[0], np.cumsum(lens[:-1])]).astype(np.int64)
+    ns = (np.arange(30) % 4).astype(np.int32)
+    key_off = oracle.block_offsets(lens)
+    want = np.concatenate([oracle.hash_request(toks[offs[r]:offs[r] + lens[r]], int(ns[r])) for r in range(30)])
+    dev = torch.device("cuda")
+    for shift in range(4):
+        base = torch.zeros(len(toks) + 4, dtype=torch.int32, device=dev)
+        view = base[shift:shift + len(toks)]
+        view.copy_(torch.from_numpy(toks))
+        assert view.data_ptr() % 16 == 4 * shift
+        keys = torch.empty(max(int(key_off[-1]), 1), dtype=torch.int64, device=dev)
+        status = torch.zeros(1, dtype=torch.int32, device=dev)
+        P.pc_hash_blocks(view, torch.from_numpy(offs).to(dev), torch.from_numpy(lens).to(dev),
+                         torch.from_numpy(ns).to(dev), torch.from_numpy(key_off).to(dev),
+                         keys[:int(key_off[-1])], status, None)
+        assert int(status.item()) == 0
+        assert np.array_equal(keys[:int(key_off[-1])].cpu().numpy().view(np.uint64), want), f"shift {shift}"

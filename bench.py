@@ -43,7 +43,8 @@ def parse():
     ap.add_argument("--seeds", type=int, default=None, help="number of traces (default: the workload's)")
     ap.add_argument("--requests", type=int, default=None, help="requests per trace (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-requests", type=int, default=25000)
+    ap.add_argument("--cpu-sample-requests", type=int, default=0,
+                    help="requests per trace in the oracle baseline (0: all of them)")
     ap.add_argument("--phase-profile", action="store_true",
                     help="use the phase-counter library and add per-phase cycles, reclamation latency per "
                          "evicting request and state bytes per cached block to the JSON line")
@@ -245,15 +246,15 @@ def phase_report(batch, insts, traces, replay_ms):
 
 def cpu_baseline(traces, insts, sample_requests):
     """The oracle (plain single-threaded C per instance) on the host cores:
-    hash of the first `sample_requests` requests of every trace, then replay
-    of every instance over them, one thread per task."""
+    hash of the first `sample_requests` requests of every trace (all of them
+    if 0), then replay of every instance over them, one thread per task."""
     import oracle
     from paper_2608_01657_amd import tracegen as tg
 
     cores = min(16, os.cpu_count() or 1)
     sub = []
     for tr in traces:
-        n = min(sample_requests, tr.n_req)
+        n = tr.n_req if sample_requests <= 0 else min(sample_requests, tr.n_req)
         sub.append(tg.Trace(tr.name, tr.tokens, tr.tok_off[:n], tr.length[:n], tr.group[:n], tr.contract[:n],
                             tr.prefix[:n], tr.n_groups, tr.n_prefix, None if tr.tick is None else tr.tick[:n]))
     t0 = time.perf_counter()
@@ -264,7 +265,8 @@ def cpu_baseline(traces, insts, sample_requests):
     wall = time.perf_counter() - t0
     probes = sum(sum(g["probes"] for g in r.groups) for r in results)
     return {"value": probes / wall, "unit": "probes/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {sub[0].n_req} requests of each of the {len(sub)} traces, all {len(insts)} "
+            "sample": f"{'all' if all(s.n_req == t.n_req for s, t in zip(sub, traces)) else 'first'} "
+                      f"{sub[0].n_req} requests of each of the {len(sub)} traces, all {len(insts)} "
                       f"instances: oracle hash + replay, {probes} probes in {wall:.2f}s wall"}
 
 

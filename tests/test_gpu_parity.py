@@ -376,3 +376,47 @@ def test_hash_token_buffer_at_any_int32_offset():
                          keys[:int(key_off[-1])], status, None)
         assert int(status.item()) == 0
         assert np.array_equal(keys[:int(key_off[-1])].cpu().numpy().view(np.uint64), want), f"shift {shift}"
+
+
+def test_replay_step_boundary():
+    """Requests of 255, 256, 257, 511, 512 and 513 blocks, on both sides of
+    the 256-position lookup step (one-step requests keep their outcome in
+    registers, longer ones go through the position arrays), with shared
+    prefixes, duplicates within a request and keys reused across requests so
+    that hits, orphans and duplicates all occur; every policy and
+    PrefixShield flag at capacities below, at and above one step."""
+    kts, per = [], []
+    for seed in range(6):
+        rng = np.random.default_rng(9000 + seed)
+        G = 3
+        reqs, groups = [], []
+        hist = []
+        for r in range(40):
+            n = int(rng.choice([255, 256, 257, 511, 512, 513]))
+            if hist and rng.random() < 0.6:
+                src = hist[int(rng.integers(0, len(hist)))]
+                ks = list(src[:int(rng.integers(0, len(src) + 1))])
+            else:
+                ks = []
+            while len(ks) < n:
+                ks.append(int(rng.integers(1, 1500)))    # small universe: reuse and duplicates
+            ks = ks[:n]
+            hist.append(ks)
+            reqs.append(ks)
+            groups.append(int(rng.integers(0, G)))
+        keys = np.array([k for r in reqs for k in r], dtype=np.uint64)
+        off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.int64)
+        R = len(reqs)
+        kts.append(tg.KeyTrace(keys, off, np.array(groups, np.uint8), (np.arange(R) % 2).astype(np.uint8),
+                               (np.array(groups) * 3 + np.arange(R) % 3).astype(np.uint32), G, 3 * G))
+        contracts = [(tg.Q16, 64 * tg.Q16), (tg.Q16 // 4, 16 * tg.Q16)]
+        insts = []
+        for pol in POLICIES:
+            for cap in (200, 256, 300, 700):
+                for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                    insts.append(tg.Instance(0, pol, cap, contracts=contracts, flags=flags))
+        per.append(insts)
+    res = run_key_traces(kts, per)
+    # the crafted traces must actually produce duplicates and orphans
+    assert sum(g["dups"] for groups, _, _ in res for g in groups) > 0
+    assert sum(g["orphans"] for groups, _, _ in res for g in groups) > 0

@@ -420,3 +420,29 @@ def test_replay_step_boundary():
     # the crafted traces must actually produce duplicates and orphans
     assert sum(g["dups"] for groups, _, _ in res for g in groups) > 0
     assert sum(g["orphans"] for groups, _, _ in res for g in groups) > 0
+
+
+def test_replay_extreme_debt_parameters():
+    """Refill at the ABI's limits: rho up to 2^40 and beta, eps up to 2^50
+    (Q16), tick gaps up to 2^40 and runs of equal ticks, so that rho * dt
+    needs more than 64 bits and balances swing over most of the int64 range
+    the accounting allows; every policy, PrefixShield with and without its
+    debt gate."""
+    kts, per = [], []
+    for seed in range(8):
+        rng = np.random.default_rng(7700 + seed)
+        kt = tg.random_key_trace(7700 + seed, n_req=120, max_blocks=40, n_groups=4, n_prefix=16,
+                                 n_contracts=3, key_universe=150, with_ticks=False)
+        R = kt.n_req
+        gaps = np.where(rng.random(R) < 0.3, 0, rng.integers(0, 1 << 40, R, dtype=np.int64))
+        kt.tick = np.cumsum(gaps).astype(np.int64)
+        insts = []
+        for pol in POLICIES:
+            for flags in ([0, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                contracts = [(int(rng.choice([1, 7, 1 << 20, 1 << 40])), int(rng.choice([0, 5, 1 << 50])))
+                             for _ in range(3)]
+                insts.append(tg.Instance(0, pol, int(rng.integers(20, 120)), contracts=contracts, flags=flags,
+                                         eps_q16=int(rng.choice([0, 1 << 30, 1 << 50]))))
+        kts.append(kt)
+        per.append(insts)
+    run_key_traces(kts, per)

@@ -446,3 +446,28 @@ def test_replay_extreme_debt_parameters():
         kts.append(kt)
         per.append(insts)
     run_key_traces(kts, per)
+
+
+def test_replay_capacity_at_most_groups():
+    """Capacities from 1 to a little above the number of groups: StaticQuota
+    partitions of floor(C/G) = 0 (every probe truncated, nothing cached) and
+    of one or two blocks, and the other policies at the same tiny sizes."""
+    kts, per = [], []
+    for seed in range(6):
+        G = 5 + seed % 4
+        kt = tg.random_key_trace(8800 + seed, n_req=150, max_blocks=12, n_groups=G, n_prefix=4 * G,
+                                 n_contracts=2, key_universe=30, with_ticks=bool(seed % 2))
+        insts = [tg.Instance(0, pol, cap, contracts=[(tg.Q16, 2 * tg.Q16), (tg.Q16 // 2, 0)])
+                 for pol in POLICIES for cap in range(1, G + 4)]
+        kts.append(kt)
+        per.append(insts)
+    res = run_key_traces(kts, per)
+    # StaticQuota below one block per group caches nothing
+    k = 0
+    for kt, insts in zip(kts, per):
+        for inst in insts:
+            groups, istats, _ = res[k]
+            k += 1
+            if inst.policy == tg.POLICY_STATICQUOTA and inst.capacity < kt.n_groups:
+                assert all(g["hits"] == 0 and g["charged"] == 0 for g in groups)
+                assert istats["resident_max"] == 0

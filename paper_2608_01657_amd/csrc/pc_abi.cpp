@@ -191,6 +191,15 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         if (s.policy == PC_S3FIFO && d.g_cap > 0) d.o_gtable = take(32LL << d.gnb_log2);
         d.state_bytes = (int32_t)so;
         d.in_lds = so <= lds_cap ? 1 : 0;
+        {   // the kernel's compile-time copy for the default 4096-block layout
+            const bool s3 = s.policy == PC_S3FIFO;
+            const bool fix = d.in_lds && s.capacity == pcr::kFixC && d.s_cap == pcr::kFixScap &&
+                             d.g_cap == pcr::kFixGcap && d.move_thr == pcr::kFixMoveThr &&
+                             d.nb_log2 == pcr::kFixNbLog2 && d.rs_log2 == pcr::kFixRsLog2 &&
+                             d.log_log2 == pcr::kFixLogLog2 && d.gnb_log2 == (s3 ? pcr::kFixGnbLog2S3 : 0) &&
+                             d.gr_log2 == (s3 ? pcr::kFixGrLog2S3 : 0);
+            d.fixc = fix ? pcr::kFixC : 0;
+        }
         (d.in_lds ? lds_ids : glb_ids).push_back(i);
         if (d.in_lds) P.lds_bytes = std::max(P.lds_bytes, d.state_bytes);
         cost[i] = (double)t.n_keys * (s.policy == PC_LRU ? 1.0 : 1.4) + (double)t.n_req * 16.0;

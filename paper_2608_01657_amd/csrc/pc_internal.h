@@ -30,6 +30,17 @@ constexpr int kLRU = 0, kS3 = 1, kPS = 2, kSQ = 3;
 constexpr int kFlagNoSeg = 1, kFlagNoGate = 2;
 
 constexpr uint32_t kEmpty = 0xFFFFFFFFu;   // empty table entry
+
+// The default layout of a 4096-block instance (S3-FIFO small queue 10 %, move
+// threshold 1) on traces whose requests hold at most 512 blocks: every such
+// trace gives these sizes, and its state fits LDS.  The host marks an
+// instance with DevInst::fixc = kFixC when its derived parameters equal these
+// exactly, and the replay kernel then runs a copy compiled with them as
+// constants.
+constexpr int32_t kFixC = 4096;
+constexpr int32_t kFixNbLog2 = 10, kFixRsLog2 = 10, kFixLogLog2 = 13;
+constexpr int32_t kFixGnbLog2S3 = 10, kFixGrLog2S3 = 14;    // S3-FIFO; other policies: 0, 0
+constexpr int32_t kFixScap = 409, kFixGcap = 3687, kFixMoveThr = 1;
 constexpr uint16_t kNoSlot = 0xFFFF;
 
 // Stats record offsets (int64 words): 64 groups x 17, then instance x 8.
@@ -58,6 +69,7 @@ struct DevInst {
     // state-region offsets (bytes)
     int32_t o_key, o_stamp, o_meta, o_table, o_log, o_posslot, o_rset, o_rkeys, o_vlist;
     int32_t o_pfx, o_gtable, o_rcnt, o_res, o_cnt, o_cur, o_fstack;
+    int32_t fixc;          // kFixC: the kernel takes the parameters below as constants
     // workspace offsets (bytes from workspace base)
     int64_t ws_state;      // state region when !in_lds
     int64_t ws_bits;       // uint32 [2 * n_prefix_words]: referenced, admitted

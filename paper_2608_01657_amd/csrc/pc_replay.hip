@@ -334,10 +334,66 @@ struct Req {
     DEV int64_t nfull() const { return kend - ko; }
 };
 
+// Parameters derived from an instance's capacity and S3-FIFO settings.
+// kFix = 0: read from its descriptor.  kFix = kFixC: the default 4096-block
+// layout, by the same formulas from constants, so that they fold into the
+// instructions instead of holding scalar registers.
+template <int kPol, int kFix>
+struct Params {
+    int C;
+    uint32_t nbmask, rsmask, rbmask, lmask, R, gnbmask, grmask;
+    int32_t s_cap, g_cap, move_thr;
+    uint32_t gne, gspan;      // ghost table entries; sweep span (ring - g_cap - 256)
+    uint64_t gsrate;          // ceil(gne * 2^16 / gspan): entries swept per insertion, Q16
+    DEV void set_params(const DevInst &I) {
+        C = I.capacity;
+        nbmask = (1u << I.nb_log2) - 1u;
+        rsmask = (1u << I.rs_log2) - 1u;
+        rbmask = rsmask >> 3;
+        R = 1u << I.log_log2;
+        lmask = R - 1u;
+        gnbmask = (1u << I.gnb_log2) - 1u;
+        grmask = (1u << I.gr_log2) - 1u;
+        gne = 8u << I.gnb_log2;
+        gspan = (grmask + 1u) - (uint32_t)I.g_cap - (uint32_t)kB;
+        gsrate = I.g_cap > 0 ? (((uint64_t)gne << 16) + gspan - 1) / gspan : 0;
+        s_cap = I.s_cap;
+        g_cap = I.g_cap;
+        move_thr = I.move_thr;
+    }
+};
+template <int kPol>
+struct Params<kPol, kFixC> {
+    static constexpr int32_t kGnb = kPol == kS3 ? kFixGnbLog2S3 : 0, kGr = kPol == kS3 ? kFixGrLog2S3 : 0;
+    static constexpr int C = kFixC;
+    static constexpr uint32_t nbmask = (1u << kFixNbLog2) - 1u, rsmask = (1u << kFixRsLog2) - 1u;
+    static constexpr uint32_t rbmask = rsmask >> 3, R = 1u << kFixLogLog2, lmask = R - 1u;
+    static constexpr uint32_t gnbmask = (1u << kGnb) - 1u, grmask = (1u << kGr) - 1u;
+    static constexpr int32_t s_cap = kFixScap, g_cap = kFixGcap, move_thr = kFixMoveThr;
+    static constexpr uint32_t gne = 8u << kGnb, gspan = (grmask + 1u) - (uint32_t)g_cap - (uint32_t)kB;
+    static constexpr uint64_t gsrate = g_cap > 0 ? (((uint64_t)gne << 16) + gspan - 1) / gspan : 0;
+    DEV void set_params(const DevInst &) {}
+};
+
 // kPol is the instance's policy: each policy gets its own specialized copy
 // of the request loop (no runtime policy tests, fewer live registers).
-template <bool kLds, int kPol>
-struct Replayer {
+template <bool kLds, int kPol, int kFix = 0>
+struct Replayer : Params<kPol, kFix> {
+    using Pm = Params<kPol, kFix>;
+    using Pm::C;
+    using Pm::nbmask;
+    using Pm::rsmask;
+    using Pm::rbmask;
+    using Pm::lmask;
+    using Pm::R;
+    using Pm::gnbmask;
+    using Pm::grmask;
+    using Pm::s_cap;
+    using Pm::g_cap;
+    using Pm::move_thr;
+    using Pm::gne;
+    using Pm::gspan;
+    using Pm::gsrate;
     static constexpr int policy = kPol;
     // per-(group, segment) free queues: live counts and log cursors
     static constexpr bool kQueues = kPol == kPS || kPol == kSQ;
@@ -347,11 +403,9 @@ struct Replayer {
     // ---------------- configuration (uniform)
     const DevInst &I;
     const DevTrace &T;
-    int C, flags, G, K, nseg;
+    int flags, G, K, nseg;
     int room;                 // most blocks one request may hold: C, or the StaticQuota partition
     int64_t eps;
-    uint32_t nbmask, rsmask, rbmask, lmask, R, gnbmask, grmask;
-    int32_t s_cap, g_cap, move_thr;
     int64_t rho[4], beta[4], invw[4];   // kept in VGPRs
     // ---------------- arrays
     uint64_t *key, *rkeys;
@@ -377,8 +431,6 @@ struct Replayer {
     uint32_t gseq, curS, curM;
     uint32_t gseq0;           // gseq when this request's reclamation began
     uint32_t gsw;             // ghost sweep cursor
-    uint32_t gne, gspan;      // ghost table entries; sweep span (ring - g_cap - 256)
-    uint64_t gsrate;          // ceil(gne * 2^16 / gspan): entries swept per insertion, Q16
     int32_t rmax;
     int32_t err;
     // ---------------- statistics and group state (lane x = group x, VGPRs)
@@ -395,26 +447,13 @@ struct Replayer {
     DEV Replayer(Coll &coll, const DevInst &inst, const DevTrace &tr, uint8_t *sbase, uint8_t *ws)
         : X(coll), tid((int)threadIdx.x), wid((int)rfl(threadIdx.x >> 6)), lane((int)__lane_id()), cb(0),
           I(inst), T(tr) {
-        C = I.capacity;
+        this->set_params(I);
         flags = I.flags;
         G = T.n_groups;
         K = I.n_contracts;
         nseg = (policy == kPS && !(flags & kFlagNoSeg)) ? 3 : 1;
         room = policy == kSQ ? C / G : C;
         eps = I.eps;
-        nbmask = (1u << I.nb_log2) - 1u;
-        rsmask = (1u << I.rs_log2) - 1u;
-        rbmask = rsmask >> 3;
-        R = 1u << I.log_log2;
-        lmask = R - 1u;
-        gnbmask = (1u << I.gnb_log2) - 1u;
-        grmask = (1u << I.gr_log2) - 1u;
-        gne = 8u << I.gnb_log2;
-        gspan = (grmask + 1u) - (uint32_t)I.g_cap - (uint32_t)kB;
-        gsrate = I.g_cap > 0 ? (((uint64_t)gne << 16) + gspan - 1) / gspan : 0;
-        s_cap = I.s_cap;
-        g_cap = I.g_cap;
-        move_thr = I.move_thr;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             rho[c] = in_vgpr(I.rho[c]);
@@ -1792,6 +1831,22 @@ struct Replayer {
     }
 };
 
+// One instance: the compile-time copy for the default 4096-block layout when
+// the host marked it (LDS state only), else the general one.
+template <bool kLds, int kPol>
+DEV void run_instance(Coll &coll, const DevInst &I, const DevTrace &T, uint8_t *sbase, uint8_t *ws, int64_t *st,
+                      int32_t *per_req) {
+    if constexpr (kLds) {
+        if (I.fixc == kFixC) {
+            Replayer<kLds, kPol, kFixC> rp(coll, I, T, sbase, ws);
+            rp.run(st, per_req);
+            return;
+        }
+    }
+    Replayer<kLds, kPol, 0> rp(coll, I, T, sbase, ws);
+    rp.run(st, per_req);
+}
+
 template <bool kLds>
 __global__ __launch_bounds__(kB) void replay_kernel(const DevInst *__restrict__ insts,
                                                     const DevTrace *__restrict__ traces,
@@ -1806,19 +1861,10 @@ __global__ __launch_bounds__(kB) void replay_kernel(const DevInst *__restrict__ 
     if constexpr (kLds) sbase = smem;
     else sbase = ws + I.ws_state;
     int64_t *st = stats + (int64_t)id * kRecordWords;
-    if (I.policy == kLRU) {
-        Replayer<kLds, kLRU> rp(coll, I, T, sbase, ws);
-        rp.run(st, per_req);
-    } else if (I.policy == kS3) {
-        Replayer<kLds, kS3> rp(coll, I, T, sbase, ws);
-        rp.run(st, per_req);
-    } else if (I.policy == kSQ) {
-        Replayer<kLds, kSQ> rp(coll, I, T, sbase, ws);
-        rp.run(st, per_req);
-    } else {
-        Replayer<kLds, kPS> rp(coll, I, T, sbase, ws);
-        rp.run(st, per_req);
-    }
+    if (I.policy == kLRU) run_instance<kLds, kLRU>(coll, I, T, sbase, ws, st, per_req);
+    else if (I.policy == kS3) run_instance<kLds, kS3>(coll, I, T, sbase, ws, st, per_req);
+    else if (I.policy == kSQ) run_instance<kLds, kSQ>(coll, I, T, sbase, ws, st, per_req);
+    else run_instance<kLds, kPS>(coll, I, T, sbase, ws, st, per_req);
 }
 
 }  // namespace

@@ -471,3 +471,42 @@ def test_replay_capacity_at_most_groups():
             if inst.policy == tg.POLICY_STATICQUOTA and inst.capacity < kt.n_groups:
                 assert all(g["hits"] == 0 and g["charged"] == 0 for g in groups)
                 assert istats["resident_max"] == 0
+
+
+def test_replay_default_4096_layout():
+    """4096-block instances with default S3-FIFO settings, on traces of at
+    most 512 blocks per request, run the kernel's copy compiled for that
+    layout; with other settings or capacities they run the general one.
+    Both against the oracle on crafted traces that overflow the cache
+    (duplicates, orphans, requests past one lookup step), every policy."""
+    kts, per = [], []
+    for seed in range(3):
+        rng = np.random.default_rng(6100 + seed)
+        G = 4
+        reqs, groups, hist = [], [], []
+        for r in range(90):
+            n = int(rng.choice([40, 200, 256, 257, 400, 512]))
+            ks = list(hist[int(rng.integers(0, len(hist)))][:int(rng.integers(0, 300))]) if hist and rng.random() < 0.5 else []
+            while len(ks) < n:
+                ks.append(int(rng.integers(1, 12000)))
+            ks = ks[:n]
+            hist.append(ks)
+            reqs.append(ks)
+            groups.append(int(rng.integers(0, G)))
+        keys = np.array([k for r in reqs for k in r], dtype=np.uint64)
+        off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.int64)
+        R = len(reqs)
+        kts.append(tg.KeyTrace(keys, off, np.array(groups, np.uint8), (np.arange(R) % 2).astype(np.uint8),
+                               (np.array(groups) * 2 + np.arange(R) % 2).astype(np.uint32), G, 2 * G,
+                               np.cumsum(rng.integers(0, 3, R)).astype(np.int64)))
+        contracts = [(tg.Q16 * 40, 192 * tg.Q16), (tg.Q16 * 16, 128 * tg.Q16)]
+        insts = []
+        for pol in POLICIES:
+            for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                insts.append(tg.Instance(0, pol, 4096, contracts=contracts, flags=flags))
+        insts.append(tg.Instance(0, tg.POLICY_S3FIFO, 4096, contracts=contracts, s3_small_permille=250))
+        insts.append(tg.Instance(0, tg.POLICY_S3FIFO, 4096, contracts=contracts, s3_move_threshold=2))
+        insts.append(tg.Instance(0, tg.POLICY_LRU, 4095, contracts=contracts))
+        per.append(insts)
+    res = run_key_traces(kts, per)
+    assert sum(inst["evictions"] for _, inst, _ in res) > 0

@@ -150,7 +150,12 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         d.s_cap = (int32_t)scap;
         d.g_cap = (int32_t)(s.capacity - scap);
         d.move_thr = s.s3_move_threshold;
-        const int64_t maxn = std::min<int64_t>(t.max_req_blocks, s.capacity);
+        int64_t maxn = std::min<int64_t>(t.max_req_blocks, s.capacity);
+        // a candidate for the kernel's default-layout copy is laid out for
+        // requests of kFixMaxn blocks (maxn only sizes buffers)
+        if (s.capacity == pcr::kFixC && maxn <= pcr::kFixMaxn && d.s_cap == pcr::kFixScap &&
+            d.move_thr == pcr::kFixMoveThr)
+            maxn = pcr::kFixMaxn;
         d.maxn = (int32_t)maxn;
         // main table: 8-entry buckets, load <= 2/3
         d.nb_log2 = std::max(1, ceil_log2((int64_t)s.capacity * 3 / 16 + 1));
@@ -193,7 +198,14 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         d.in_lds = so <= lds_cap ? 1 : 0;
         {   // the kernel's compile-time copy for the default 4096-block layout
             const bool s3 = s.policy == PC_S3FIFO;
-            const bool fix = d.in_lds && s.capacity == pcr::kFixC && d.s_cap == pcr::kFixScap &&
+            const pcr::FixOffsets f = pcr::fix_offsets(s.policy);
+            const bool offs = d.o_key == f.o_key && d.o_stamp == f.o_stamp && d.o_meta == f.o_meta &&
+                              d.o_table == f.o_table && d.o_log == f.o_log && d.o_rkeys == f.o_rkeys &&
+                              d.o_rset == f.o_rset && d.o_posslot == f.o_posslot && d.o_vlist == f.o_vlist &&
+                              d.o_rcnt == f.o_rcnt && d.o_res == f.o_res && d.o_pfx == f.o_pfx &&
+                              d.o_cnt == f.o_cnt && d.o_cur == f.o_cur && d.o_fstack == f.o_fstack &&
+                              d.o_gtable == f.o_gtable && d.state_bytes == f.end;
+            const bool fix = offs && d.in_lds && s.capacity == pcr::kFixC && d.s_cap == pcr::kFixScap &&
                              d.g_cap == pcr::kFixGcap && d.move_thr == pcr::kFixMoveThr &&
                              d.nb_log2 == pcr::kFixNbLog2 && d.rs_log2 == pcr::kFixRsLog2 &&
                              d.log_log2 == pcr::kFixLogLog2 && d.gnb_log2 == (s3 ? pcr::kFixGnbLog2S3 : 0) &&

@@ -41,6 +41,40 @@ constexpr int32_t kFixC = 4096;
 constexpr int32_t kFixNbLog2 = 10, kFixRsLog2 = 10, kFixLogLog2 = 13;
 constexpr int32_t kFixGnbLog2S3 = 10, kFixGrLog2S3 = 14;    // S3-FIFO; other policies: 0, 0
 constexpr int32_t kFixScap = 409, kFixGcap = 3687, kFixMoveThr = 1;
+constexpr int32_t kFixMaxn = 512;   // the host lays such instances out for requests of 512 blocks
+
+// State-region offsets of that layout, in the order the host allocates them
+// (16-byte aligned regions): equal to the host's for every marked instance.
+struct FixOffsets {
+    int32_t o_key, o_stamp, o_meta, o_table, o_log, o_rkeys, o_rset, o_posslot, o_vlist, o_rcnt, o_res;
+    int32_t o_pfx, o_cnt, o_cur, o_fstack, o_gtable, end;
+};
+constexpr FixOffsets fix_offsets(int policy) {
+    FixOffsets f{};
+    int32_t so = 0;
+    auto take = [&so](int32_t bytes) { const int32_t o = so; so = (so + bytes + 15) / 16 * 16; return o; };
+    const int32_t C = kFixC, mx = kFixMaxn;
+    f.o_key = take(8 * C);
+    f.o_stamp = take(4 * C);
+    f.o_meta = take(4 * C);
+    f.o_table = take(32 << kFixNbLog2);
+    f.o_log = take(2 << kFixLogLog2);
+    f.o_rkeys = take(8 * mx);
+    f.o_rset = take(4 << kFixRsLog2);
+    f.o_posslot = take(2 * mx);
+    f.o_vlist = take(2 * mx);
+    f.o_rcnt = take(4 << (kFixRsLog2 - 3));
+    f.o_res = take(4 * 64);
+    if (policy == kPS) f.o_pfx = take(4 * C);
+    if (policy == kPS || policy == kSQ) {
+        f.o_cnt = take(4 * 192);
+        f.o_cur = take(4 * 196);
+    }
+    if (policy == kSQ) f.o_fstack = take(2 * C);
+    if (policy == kS3) f.o_gtable = take(32 << kFixGnbLog2S3);
+    f.end = so;
+    return f;
+}
 constexpr uint16_t kNoSlot = 0xFFFF;
 
 // Stats record offsets (int64 words): 64 groups x 17, then instance x 8.

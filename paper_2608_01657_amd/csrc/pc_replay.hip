@@ -460,22 +460,26 @@ struct Replayer : Params<kPol, kFix> {
             beta[c] = in_vgpr(I.beta[c]);
             invw[c] = in_vgpr(I.invw[c]);
         }
-        key = reinterpret_cast<uint64_t *>(sbase + I.o_key);
-        rkeys = reinterpret_cast<uint64_t *>(sbase + I.o_rkeys);
-        stamp = reinterpret_cast<uint32_t *>(sbase + I.o_stamp);
-        meta = reinterpret_cast<uint32_t *>(sbase + I.o_meta);
-        table = reinterpret_cast<uint32_t *>(sbase + I.o_table);
-        rset = reinterpret_cast<uint32_t *>(sbase + I.o_rset);
-        cnt = reinterpret_cast<uint32_t *>(sbase + I.o_cnt);
-        cur = reinterpret_cast<uint32_t *>(sbase + I.o_cur);
-        res = reinterpret_cast<uint32_t *>(sbase + I.o_res);
-        pfx = reinterpret_cast<uint32_t *>(sbase + I.o_pfx);
-        gtable = reinterpret_cast<uint32_t *>(sbase + I.o_gtable);
-        log = reinterpret_cast<uint16_t *>(sbase + I.o_log);
-        posslot = reinterpret_cast<uint16_t *>(sbase + I.o_posslot);
-        vlist = reinterpret_cast<uint16_t *>(sbase + I.o_vlist);
-        fstack = reinterpret_cast<uint16_t *>(sbase + I.o_fstack);
-        rcnt = reinterpret_cast<uint32_t *>(sbase + I.o_rcnt);
+        // the default-layout copy takes its array offsets as constants (the
+        // host marks an instance for it only when they equal its own)
+        constexpr bool fx = kFix == kFixC;
+        constexpr FixOffsets F = fix_offsets(kPol);
+        key = reinterpret_cast<uint64_t *>(sbase + (fx ? F.o_key : I.o_key));
+        rkeys = reinterpret_cast<uint64_t *>(sbase + (fx ? F.o_rkeys : I.o_rkeys));
+        stamp = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_stamp : I.o_stamp));
+        meta = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_meta : I.o_meta));
+        table = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_table : I.o_table));
+        rset = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_rset : I.o_rset));
+        cnt = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_cnt : I.o_cnt));
+        cur = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_cur : I.o_cur));
+        res = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_res : I.o_res));
+        pfx = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_pfx : I.o_pfx));
+        gtable = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_gtable : I.o_gtable));
+        log = reinterpret_cast<uint16_t *>(sbase + (fx ? F.o_log : I.o_log));
+        posslot = reinterpret_cast<uint16_t *>(sbase + (fx ? F.o_posslot : I.o_posslot));
+        vlist = reinterpret_cast<uint16_t *>(sbase + (fx ? F.o_vlist : I.o_vlist));
+        fstack = reinterpret_cast<uint16_t *>(sbase + (fx ? F.o_fstack : I.o_fstack));
+        rcnt = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_rcnt : I.o_rcnt));
         bits = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_bits));
         gring = gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_gring));
         n_req = T.n_req;

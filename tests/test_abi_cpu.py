@@ -154,3 +154,24 @@ def test_state_bytes_on_the_host():
     out_b = (ctypes.c_int64 * 1)()
     out_f = (ctypes.c_int32 * 1)()
     assert lib.pc_replay_state_bytes((P.pc_trace_desc * 1)(_trace()), 1, bad, 1, out_b, out_f) == P.PC_EINVAL
+
+
+def test_default_4096_layout_is_sized_for_512_block_requests():
+    """A 4096-block instance with default S3-FIFO settings is a candidate for
+    the kernel's compile-time copy, so the planner lays it out for requests
+    of 512 blocks whatever its trace's longest request (the buffers that
+    depend on it only grow); other settings keep the trace's own sizing.
+    The sizes are those of the layout's allocation order: 125,696 bytes for
+    LRU, 158,464 for S3-FIFO, 143,632 for PrefixShield."""
+    short = _trace(max_req_blocks=100)
+    full = _trace(max_req_blocks=512)
+    for pol, want in ((0, 125696), (1, 158464), (2, 143632)):
+        b, _ = P.pc_replay_state_bytes([short, full], [_inst(policy=pol, capacity=4096, trace=0),
+                                                       _inst(policy=pol, capacity=4096, trace=1)])
+        assert list(b) == [want, want]
+    # a non-default small queue, or another capacity, keeps the short sizing
+    b, _ = P.pc_replay_state_bytes([short, full], [_inst(policy=1, capacity=4096, trace=0, s3_small_permille=250),
+                                                   _inst(policy=1, capacity=4096, trace=1, s3_small_permille=250),
+                                                   _inst(policy=0, capacity=4095, trace=0),
+                                                   _inst(policy=0, capacity=4095, trace=1)])
+    assert b[0] < b[1] and b[2] < b[3]

@@ -206,6 +206,7 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
                               d.o_cnt == f.o_cnt && d.o_cur == f.o_cur && d.o_fstack == f.o_fstack &&
                               d.o_gtable == f.o_gtable && d.state_bytes == f.end;
             const bool fix = offs && d.in_lds && s.capacity == pcr::kFixC && d.s_cap == pcr::kFixScap &&
+                             s.n_contracts == 1 && s.eps_q16 == 0 && s.flags == 0 &&
                              d.g_cap == pcr::kFixGcap && d.move_thr == pcr::kFixMoveThr &&
                              d.nb_log2 == pcr::kFixNbLog2 && d.rs_log2 == pcr::kFixRsLog2 &&
                              d.log_log2 == pcr::kFixLogLog2 && d.gnb_log2 == (s3 ? pcr::kFixGnbLog2S3 : 0) &&

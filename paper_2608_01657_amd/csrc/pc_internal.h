@@ -32,8 +32,9 @@ constexpr int kFlagNoSeg = 1, kFlagNoGate = 2;
 constexpr uint32_t kEmpty = 0xFFFFFFFFu;   // empty table entry
 
 // The default layout of a 4096-block instance (S3-FIFO small queue 10 %, move
-// threshold 1) on traces whose requests hold at most 512 blocks: every such
-// trace gives these sizes, and its state fits LDS.  The host marks an
+// threshold 1, one contract, eps = 0, no ablation flags) on traces whose
+// requests hold at most 512 blocks: every such trace gives these sizes, and
+// its state fits LDS.  The host marks an
 // instance with DevInst::fixc = kFixC when its derived parameters equal these
 // exactly, and the replay kernel then runs a copy compiled with them as
 // constants.

@@ -345,7 +345,13 @@ struct Params {
     int32_t s_cap, g_cap, move_thr;
     uint32_t gne, gspan;      // ghost table entries; sweep span (ring - g_cap - 256)
     uint64_t gsrate;          // ceil(gne * 2^16 / gspan): entries swept per insertion, Q16
+    int flags, K, nseg;
+    int64_t eps;
     DEV void set_params(const DevInst &I) {
+        flags = I.flags;
+        K = I.n_contracts;
+        nseg = (kPol == kPS && !(flags & kFlagNoSeg)) ? 3 : 1;
+        eps = I.eps;
         C = I.capacity;
         nbmask = (1u << I.nb_log2) - 1u;
         rsmask = (1u << I.rs_log2) - 1u;
@@ -372,6 +378,9 @@ struct Params<kPol, kFixC> {
     static constexpr int32_t s_cap = kFixScap, g_cap = kFixGcap, move_thr = kFixMoveThr;
     static constexpr uint32_t gne = 8u << kGnb, gspan = (grmask + 1u) - (uint32_t)g_cap - (uint32_t)kB;
     static constexpr uint64_t gsrate = g_cap > 0 ? (((uint64_t)gne << 16) + gspan - 1) / gspan : 0;
+    // one contract, eps = 0, no ablation flags
+    static constexpr int flags = 0, K = 1, nseg = kPol == kPS ? 3 : 1;
+    static constexpr int64_t eps = 0;
     DEV void set_params(const DevInst &) {}
 };
 
@@ -394,6 +403,10 @@ struct Replayer : Params<kPol, kFix> {
     using Pm::gne;
     using Pm::gspan;
     using Pm::gsrate;
+    using Pm::flags;
+    using Pm::K;
+    using Pm::nseg;
+    using Pm::eps;
     static constexpr int policy = kPol;
     // per-(group, segment) free queues: live counts and log cursors
     static constexpr bool kQueues = kPol == kPS || kPol == kSQ;
@@ -403,9 +416,8 @@ struct Replayer : Params<kPol, kFix> {
     // ---------------- configuration (uniform)
     const DevInst &I;
     const DevTrace &T;
-    int flags, G, K, nseg;
+    int G;
     int room;                 // most blocks one request may hold: C, or the StaticQuota partition
-    int64_t eps;
     int64_t rho[4], beta[4], invw[4];   // kept in VGPRs
     // ---------------- arrays
     uint64_t *key, *rkeys;
@@ -448,12 +460,8 @@ struct Replayer : Params<kPol, kFix> {
         : X(coll), tid((int)threadIdx.x), wid((int)rfl(threadIdx.x >> 6)), lane((int)__lane_id()), cb(0),
           I(inst), T(tr) {
         this->set_params(I);
-        flags = I.flags;
         G = T.n_groups;
-        K = I.n_contracts;
-        nseg = (policy == kPS && !(flags & kFlagNoSeg)) ? 3 : 1;
         room = policy == kSQ ? C / G : C;
-        eps = I.eps;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             rho[c] = in_vgpr(I.rho[c]);

@@ -474,11 +474,12 @@ def test_replay_capacity_at_most_groups():
 
 
 def test_replay_default_4096_layout():
-    """4096-block instances with default S3-FIFO settings, on traces of at
-    most 512 blocks per request, run the kernel's copy compiled for that
-    layout; with other settings or capacities they run the general one.
-    Both against the oracle on crafted traces that overflow the cache
-    (duplicates, orphans, requests past one lookup step), every policy."""
+    """4096-block instances with default S3-FIFO settings, one contract,
+    eps = 0 and no flags, on traces of at most 512 blocks per request, run
+    the kernel's copy compiled for that layout; with other settings,
+    contracts or capacities they run the general one.  Both against the
+    oracle on crafted traces that overflow the cache (duplicates, orphans,
+    requests past one lookup step), every policy."""
     kts, per = [], []
     for seed in range(3):
         rng = np.random.default_rng(6100 + seed)
@@ -496,17 +497,21 @@ def test_replay_default_4096_layout():
         keys = np.array([k for r in reqs for k in r], dtype=np.uint64)
         off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.int64)
         R = len(reqs)
-        kts.append(tg.KeyTrace(keys, off, np.array(groups, np.uint8), (np.arange(R) % 2).astype(np.uint8),
-                               (np.array(groups) * 2 + np.arange(R) % 2).astype(np.uint32), G, 2 * G,
-                               np.cumsum(rng.integers(0, 3, R)).astype(np.int64)))
-        contracts = [(tg.Q16 * 40, 192 * tg.Q16), (tg.Q16 * 16, 128 * tg.Q16)]
-        insts = []
-        for pol in POLICIES:
-            for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
-                insts.append(tg.Instance(0, pol, 4096, contracts=contracts, flags=flags))
-        insts.append(tg.Instance(0, tg.POLICY_S3FIFO, 4096, contracts=contracts, s3_small_permille=250))
-        insts.append(tg.Instance(0, tg.POLICY_S3FIFO, 4096, contracts=contracts, s3_move_threshold=2))
-        insts.append(tg.Instance(0, tg.POLICY_LRU, 4095, contracts=contracts))
-        per.append(insts)
+        ticks = np.cumsum(rng.integers(0, 3, R)).astype(np.int64)
+        grp = np.array(groups, np.uint8)
+        pfx = (np.array(groups) * 2 + np.arange(R) % 2).astype(np.uint32)
+        one = [(tg.Q16 * 40 // 6, 192 * tg.Q16)]
+        two = [(tg.Q16 * 40, 192 * tg.Q16), (tg.Q16 * 16, 128 * tg.Q16)]
+        # one contract: the compile-time copy
+        kts.append(tg.KeyTrace(keys, off, grp, np.zeros(R, np.uint8), pfx, G, 2 * G, ticks))
+        per.append([tg.Instance(0, pol, 4096, contracts=one) for pol in POLICIES] +
+                   [tg.Instance(0, tg.POLICY_PREFIXSHIELD, 4096, contracts=one, flags=f) for f in (1, 2)] +
+                   [tg.Instance(0, tg.POLICY_PREFIXSHIELD, 4096, contracts=one, eps_q16=4 * tg.Q16),
+                    tg.Instance(0, tg.POLICY_LRU, 4095, contracts=one)])
+        # two contracts, other S3-FIFO settings: the general copy
+        kts.append(tg.KeyTrace(keys, off, grp, (np.arange(R) % 2).astype(np.uint8), pfx, G, 2 * G, ticks))
+        per.append([tg.Instance(0, pol, 4096, contracts=two) for pol in POLICIES] +
+                   [tg.Instance(0, tg.POLICY_S3FIFO, 4096, contracts=two, s3_small_permille=250),
+                    tg.Instance(0, tg.POLICY_S3FIFO, 4096, contracts=two, s3_move_threshold=2)])
     res = run_key_traces(kts, per)
     assert sum(inst["evictions"] for _, inst, _ in res) > 0

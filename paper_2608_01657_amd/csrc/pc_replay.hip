@@ -757,6 +757,15 @@ struct Replayer : Params<kPol, kFix> {
     // (set where the entry is claimed or displaced), so a victim's entry is
     // known from the metadata the scan reads anyway.
     DEV static uint32_t victim_entry(bool maybe, uint32_t mt) { return maybe ? (mt >> kTposShift) : kEmpty; }
+    // Slot named by log position pos, or slot 0 past the tail.  The load is
+    // unconditional (the masked position is always inside the log) and the
+    // entry is used only when valid, since the log past the tail may never
+    // have been written; so every slot index is below C, and a scan can load
+    // the slot's metadata, stamp and key together without a branch.
+    DEV uint32_t slot_at(uint32_t pos, bool valid) const {
+        const uint32_t e = log[pos & lmask];
+        return valid ? e : 0u;
+    }
     // Victims of one step: thread with v holds victim slot s with metadata mt
     // (vrank = its rank among the step's victims) and its table entry loc.
     // Every thread calls this.
@@ -785,8 +794,9 @@ struct Replayer : Params<kPol, kFix> {
         for (uint32_t p0 = head; p0 < tail; p0 += kB) {
             const uint32_t pos = p0 + tid;
             const bool valid = pos < tail;
-            const uint32_t s = valid ? log[pos & lmask] : 0;
-            const bool live = valid && (meta[s] & kInLog) && stamp[s] == pos;
+            const uint32_t s = slot_at(pos, valid);
+            const uint32_t mt = meta[s], st = stamp[s];
+            const bool live = valid && (mt & kInLog) && st == pos;
             const BMask lm = bballot1(live);   // every read of this step is done
             if (live) {
                 const uint32_t np = nw + (uint32_t)lm.rank(wid);
@@ -823,9 +833,9 @@ struct Replayer : Params<kPol, kFix> {
         while (rem > 0 && err == 0) {
             const uint32_t pos = head + tid;
             const bool valid = pos < tail;
-            const uint32_t s = valid ? log[pos & lmask] : 0;
-            const uint32_t mt = valid ? meta[s] : 0u;
-            const bool live = valid && (mt & kInLog) && stamp[s] == pos;
+            const uint32_t s = slot_at(pos, valid);
+            const uint32_t mt = meta[s], st = stamp[s];
+            const bool live = valid && (mt & kInLog) && st == pos;
             const uint32_t loc = victim_entry(live, mt);
             const BMask lm = bballot1(live);
             const int rk = lm.rank(wid);
@@ -854,9 +864,9 @@ struct Replayer : Params<kPol, kFix> {
         while (rem > 0 && err == 0) {
             const uint32_t pos = c + tid;
             const bool valid = pos < tail;
-            const uint32_t sl = valid ? log[pos & lmask] : 0;
-            const uint32_t mt = valid ? meta[sl] : 0;
-            const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
+            const uint32_t sl = slot_at(pos, valid);
+            const uint32_t mt = meta[sl], st = stamp[sl];
+            const bool live = valid && (mt & kInLog) && st == pos;
             const bool match = live && (x < 0 || (int)owner_of(mt) == x) && (s < 0 || (int)cls_of(mt) == s);
             const uint32_t loc = victim_entry(match, mt);
             const BMask mm = bballot1(match);
@@ -885,9 +895,9 @@ struct Replayer : Params<kPol, kFix> {
         while (c < tail) {
             const uint32_t pos = c + tid;
             const bool valid = pos < tail;
-            const uint32_t sl = valid ? log[pos & lmask] : 0;
-            const uint32_t mt = valid ? meta[sl] : 0;
-            const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
+            const uint32_t sl = slot_at(pos, valid);
+            const uint32_t mt = meta[sl], st = stamp[sl];
+            const bool live = valid && (mt & kInLog) && st == pos;
             const bool match = live && (int)owner_of(mt) == x && (s < 0 || (int)cls_of(mt) == s);
             const BMask mm = bballot1(match);
             if (mm.any()) { found = c + (uint32_t)mm.first(); c = found; break; }
@@ -994,13 +1004,21 @@ struct Replayer : Params<kPol, kFix> {
         const TH h = thash(k, gnbmask, rbmask);
         uint32_t e[16];
         load_buckets(gtable, h, e);
-        const uint32_t nown = gseq - gseq0;
+        // entries with the key's tag first (branch-free): a match is rare,
+        // and only a lane with one checks liveness and reads the ring
+        uint32_t tm = 0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) tm |= ((e[i] >> 16) == h.tag ? 1u : 0u) << i;
         int at = -1;
-        for (int i = 0; i < 16; ++i) {
-            const uint32_t pos = e[i] & 0xFFFFu;
-            if (at < 0 && (e[i] >> 16) == h.tag && glive(e[i], gseq) && ((gseq - 1u - pos) & grmask) >= nown &&
-                gring[pos & grmask] == k)
-                at = i;
+        if (tm != 0u) {
+            const uint32_t nown = gseq - gseq0;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const uint32_t pos = e[i] & 0xFFFFu;
+                if (at < 0 && ((tm >> i) & 1u) && glive(e[i], gseq) && ((gseq - 1u - pos) & grmask) >= nown &&
+                    gring[pos & grmask] == k)
+                    at = i;
+            }
         }
         if (at >= 0) gtable[epos(h, at)] = kEmpty;
         return at >= 0;
@@ -1060,13 +1078,13 @@ struct Replayer : Params<kPol, kFix> {
             if (sp >= lim) { err = kErrInternal; break; }
             const uint32_t pos = sp + tid;
             const bool valid = pos < lim;
-            const uint32_t sl = valid ? log[pos & lmask] : 0;
-            const uint32_t mt = valid ? meta[sl] : 0;
+            const uint32_t sl = slot_at(pos, valid);
             // a small-queue victim is remembered by the ghost: its key is
-            // read with the metadata, in the same round trip
+            // read with the metadata and stamp, in the same round trip
             const bool gho = useS && g_cap > 0;
-            const uint64_t kv = (valid && gho) ? key[sl] : 0ull;
-            const bool live = valid && (mt & kInLog) && stamp[sl] == pos;
+            const uint32_t mt = meta[sl], st = stamp[sl];
+            const uint64_t kv = gho ? key[sl] : 0ull;
+            const bool live = valid && (mt & kInLog) && st == pos;
             const bool inQ = live && (useS ? !(mt & kQMain) : (mt & kQMain) != 0);
             const bool cand = inQ && !(mt & kPin);
             const uint32_t f = freq_of(mt);
@@ -1341,10 +1359,17 @@ struct Replayer : Params<kPol, kFix> {
                     const uint4 *q4 = reinterpret_cast<const uint4 *>(rset + 8u * b);
                     const uint4 a0 = q4[0], a1 = q4[1];
                     const uint32_t ev[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+                    // earlier positions with the key's tag (branch-free; rare),
+                    // then their keys
+                    uint32_t tm = 0;
 #pragma unroll
                     for (int i = 0; i < 8; ++i)
-                        if ((ev[i] >> 16) == h.tag && (ev[i] & 0xFFFFu) < (uint32_t)j)
-                            dup = dup || rkeys[ev[i] & 0xFFFFu] == k;
+                        tm |= ((ev[i] >> 16) == h.tag && (ev[i] & 0xFFFFu) < (uint32_t)j ? 1u : 0u) << i;
+                    if (tm != 0u) {
+#pragma unroll
+                        for (int i = 0; i < 8; ++i)
+                            if ((tm >> i) & 1u) dup = dup || rkeys[ev[i] & 0xFFFFu] == k;
+                    }
                     if (dup || cn <= 8u) break;
                     b = hop == 0 ? h.r2 : ((b + 1u) & rbmask);
                 }

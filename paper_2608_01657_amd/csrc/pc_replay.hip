@@ -1050,6 +1050,32 @@ struct Replayer : Params<kPol, kFix> {
         }
         gsw += ns;
     }
+    // First position of the batch's cut: the first candidate whose counts of
+    // candidates (cr), moves (mr) and evictions (er) before it fail the
+    // batch's conditions -- small queue: (cr >= la and (munp or mr >= 1)) or
+    // er >= lim; main queue: er >= lim -- or kB.  Lane l evaluates thread
+    // positions 64 w + l of every word w with running counts, so the cut
+    // takes one ballot per word instead of serial scans of the masks.
+    // Called with every lane active.
+    DEV static int s3_stop(const BMask &candm, const BMask &mvm, const BMask &evm, bool small, int la, bool munp,
+                           int lim) {
+        uint64_t fm[kW];
+        int pc = 0, pm = 0, pe = 0;
+#pragma unroll
+        for (int w = 0; w < kW; ++w) {
+            const uint64_t cw = candm.w[w], mw = mvm.w[w], ew = evm.w[w];
+            const int cr = pc + mbcnt(cw), mr = pm + mbcnt(mw), er = pe + mbcnt(ew);
+            const bool f = small ? ((cr >= la && (munp || mr >= 1)) || er >= lim) : er >= lim;
+            fm[w] = ballot(f) & cw;
+            pc += popc(cw);
+            pm += popc(mw);
+            pe += popc(ew);
+        }
+        int stop = kB;
+#pragma unroll
+        for (int w = kW - 1; w >= 0; --w) stop = fm[w] ? 64 * w + first_bit(fm[w]) : stop;
+        return stop;
+    }
     // One scan step per batch: the queue in use (S or M, Z18) is scanned from
     // its cursor; candidates are its live unpinned entries.  Everything a
     // victim needs that does not depend on which candidates end up as
@@ -1114,36 +1140,15 @@ struct Replayer : Params<kPol, kFix> {
             // processed: each condition below holds on a prefix of them, so
             // `stop` (first candidate not processed, kB if none) is the
             // earliest position where one of them starts to fail.
-            const int ncand = candm.count(), nevall = evm.count();
-            int stop;
-            if (useS) {
-                // |S| - (earlier candidates) >= S_cap and unpinned S left
-                const int la = min(s_size - s_cap + 1, s_unp);
-                const int pa = la <= 0 ? candm.first() : (la < ncand ? candm.nth(la) : kB);
-                // ... or M has no unpinned block and nothing moved there yet
-                int pb;
-                if (m_unp > 0) pb = candm.first();
-                else if (mvm.any()) {
-                    const BMask a = candm.from(mvm.first() + 1);
-                    pb = a.any() ? a.first() : kB;
-                } else pb = kB;
-                // fewer than `rem` evictions before it
-                int pc = kB;
-                if (rem <= nevall) {
-                    const BMask a = candm.from(evm.nth(rem - 1) + 1);
-                    pc = a.any() ? a.first() : kB;
-                }
-                stop = min(max(pa, pb), pc);
-            } else {
-                // fewer than min(rem, unpinned M) evictions before it
-                const int q = min(rem, m_unp);
-                stop = kB;
-                if (q <= 0) stop = candm.first();
-                else if (q <= nevall) {
-                    const BMask a = candm.from(evm.nth(q - 1) + 1);
-                    stop = a.any() ? a.first() : kB;
-                }
-            }
+            // Small queue: a candidate may be processed while |S| less the
+            // candidates before it is still >= S_cap with unpinned S left
+            // (rank < la), or while M has no unpinned block and nothing moved
+            // there before it; main queue: while fewer than min(rem, unpinned
+            // M) evictions precede it; both: while fewer than `rem`.  Each
+            // condition fails from some candidate on, so `stop` is the first
+            // candidate where the combination fails (kB if none).
+            const int stop = useS ? s3_stop(candm, mvm, evm, true, min(s_size - s_cap + 1, s_unp), m_unp > 0, rem)
+                                  : s3_stop(candm, mvm, evm, false, 0, false, min(rem, m_unp));
             const bool proc = cand && tid < stop;
             const BMask pmm = mvm.below(stop), pem = evm.below(stop);
             const int nmv = pmm.count(), nev = pem.count();

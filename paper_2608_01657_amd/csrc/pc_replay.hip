@@ -741,16 +741,6 @@ struct Replayer : Params<kPol, kFix> {
             act &= ~m;
         }
     }
-    // evictions by owner, counted in lane `owner` of this wavefront
-    DEV void wave_count_evicted(uint32_t o, bool active) {
-        uint64_t act = ballot(active);
-        while (act) {
-            const uint32_t x = __builtin_amdgcn_readlane(o, first_bit(act));
-            const uint64_t m = ballot(active && o == x);
-            if ((uint32_t)lane == x) evw += (uint64_t)popc(m);
-            act &= ~m;
-        }
-    }
 
     // ============================================================ eviction core
     // A resident block's metadata carries the index of its main-table entry
@@ -771,8 +761,18 @@ struct Replayer : Params<kPol, kFix> {
     // Every thread calls this.
     DEV void evict_elems(bool v, uint32_t s, uint32_t mt, int vrank, uint32_t loc) {
         const uint32_t o = owner_of(mt);
-        wave_count_evicted(o, v);
-        wave_add(res, o, v, -1);
+        // per distinct owner among the victims: evictions counted in lane
+        // `owner`, and one atomic on the owner's resident count
+        uint64_t act = ballot(v);
+        while (act) {
+            const int l = first_bit(act);
+            const uint32_t x = __builtin_amdgcn_readlane(o, l);
+            const uint64_t m = ballot(v && o == x);
+            const int c = popc(m);
+            if ((uint32_t)lane == x) evw += (uint64_t)c;
+            if (lane == l) atomicAdd(&res[x], (uint32_t)(-c));
+            act &= ~m;
+        }
         if (v) {
             if (loc != kEmpty) table[loc] = kEmpty;
             meta[s] = 0;
@@ -883,8 +883,10 @@ struct Replayer : Params<kPol, kFix> {
             if (nv == 0 && c >= tail) err = kErrInternal;
             bsync();
         }
-        if (tid == 0) cur[ci] = c;
-        bsync();
+        // every wavefront stores the (same) cursor, so each one's next read
+        // of it follows its own store; the loop's barriers already order
+        // every read of this call before these stores
+        if (lane == 0) cur[ci] = c;
     }
     // Oldest live entry of queue (x, s); advances that queue's cursor to it.
     DEV uint32_t ps_headpos(int x, int s) {

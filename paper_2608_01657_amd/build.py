@@ -25,6 +25,11 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, 
          # packed FP32 instructions stay off (none are needed: the path is integer)
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-result"]
+# The replay kernel runs one wavefront per SIMD, so no other wavefront hides
+# its latencies: the machine scheduler that maximises instruction-level
+# parallelism beats the default one, which schedules for occupancy
+# (3.5 % less replay time on the one-touch C = 4096 batch, identical results).
+SOURCE_FLAGS = {"pc_replay.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]}
 
 
 def _hipcc() -> str:
@@ -46,7 +51,7 @@ def _build_one(lib_path, build_dir, extra, verbose):
 
     def compile_one(src):
         obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
-        cmd = [hipcc, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc, *FLAGS, *SOURCE_FLAGS.get(src, []), *extra, "-c", os.path.join(CSRC, src), "-o", obj]
         if src.endswith(".cpp"):
             cmd = [hipcc, *FLAGS, *extra, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)

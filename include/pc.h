@@ -113,6 +113,10 @@ typedef struct {
     int32_t max_req_blocks;        /* >= every d_key_off[r+1]-d_key_off[r]          */
 } pc_trace_desc;
 
+/* A service contract (Eqs. 1-2).  The contracts of one instance are weighted
+ * by w_c = rho_c / rho_min (Eq. 5), and 1/w_c is kept in Q16, so their refill
+ * rates may differ by a factor 2^16 at most (else PC_EINVAL): Eq. 8's
+ * per-victim decrement 1/W_g is then at least one Q16 unit. */
 typedef struct {
     int64_t rho_q16;               /* refill rate per tick, > 0 (Prop. 1), <= 2^40  */
     int64_t beta_q16;              /* burst capacity, 0..2^50                        */
@@ -171,7 +175,11 @@ int32_t pc_replay_state_bytes(const pc_trace_desc *traces, int32_t n_traces,
                               int64_t *bytes_out, int32_t *in_lds_out);
 
 /* Replay every instance over its trace, one workgroup per instance; queued
- * on `stream`.
+ * on `stream`.  Per request it runs the hooks of Alg. 1 (OnRequest, OnTouch
+ * with the debt gate of Eq. 4, OnCacheFullBlocks metering Eqs. 1-3) and,
+ * when the cache is full, the reclamation of Alg. 2 (PrefixShield: Eqs. 5-9;
+ * LRU, S3-FIFO and StaticQuota: the baselines of Sec. V-A) under the same
+ * debt accounting.
  *   d_workspace   device memory of at least pc_replay_workspace_bytes()
  *                 bytes, 256-byte aligned; its contents need not be zeroed.
  *   d_stats       n_inst * PC_STATS_RECORD_BYTES bytes, written at the end.
@@ -185,7 +193,10 @@ int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces,
                         int32_t *d_per_request, void *stream);
 
 /* Synchronize `stream`, copy the stats of one instance (or of all n_inst
- * when instance == -1) to the host and decode them.
+ * when instance == -1) to the host and decode them: per-group hits, misses
+ * and evictions, charged blocks (Eq. 2), the raw debt D_g of Eq. 3 (final,
+ * maximum and sum over requests, whose mean is the "mean debt" of Sec. V-D)
+ * and occupancy (Table III).
  *   groups_out  [max_groups] (or [n_inst][max_groups] for instance == -1)
  *   inst_out    [1] (or [n_inst]) */
 int32_t pc_get_stats(const void *d_stats, int32_t n_inst, int32_t instance,

@@ -271,12 +271,14 @@ static int64_t norm_debt(const Inst *s, int g, int64_t t) {
     }
     return d;
 }
-/* Eq. 8: 1/W_g, the smallest one-block decrement among indebted contracts */
+/* Eq. 8: 1/W_g, the smallest one-block decrement among indebted contracts
+   (0 when no contract of the group is indebted; every invw_c is >= 1, so an
+   indebted group always has a positive decrement) */
 static int64_t debt_decrement(const Inst *s, int g, int64_t t) {
-    int64_t m = 0;
+    int64_t m = -1;
     for (int c = 0; c < s->K; c++)
-        if (eff_balance(s, g, c, t) < 0 && (m == 0 || s->invw[c] < m)) m = s->invw[c];
-    return m;
+        if (eff_balance(s, g, c, t) < 0 && (m < 0 || s->invw[c] < m)) m = s->invw[c];
+    return m < 0 ? 0 : m;
 }
 
 static int32_t alloc_block(Inst *s) {
@@ -432,8 +434,13 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
         s->rho[c] = rho_q16[c]; s->beta[c] = beta_q16[c];
         if (c == 0 || rho_q16[c] < rho_min) rho_min = rho_q16[c];
     }
-    for (int c = 0; c < n_contracts; c++)   /* 1/w_c = rho_min/rho_c, Q16, rounded down */
+    /* 1/w_c = rho_min/rho_c, Q16, rounded down.  Eq. 8 needs a positive
+       decrement 1/W_g, and Q16 represents 1/w_c only down to 2^-16: rates
+       that differ by more than a factor 2^16 are rejected. */
+    for (int c = 0; c < n_contracts; c++) {
         s->invw[c] = (int64_t)(((__int128)rho_min << 16) / s->rho[c]);
+        if (s->invw[c] < 1) return -1;
+    }
     for (int64_t r = 0; r < n_req; r++) {
         if (group[r] >= n_groups || contract[r] >= n_contracts || prefix[r] >= n_prefix) return -1;
         if (key_off[r + 1] < key_off[r]) return -1;

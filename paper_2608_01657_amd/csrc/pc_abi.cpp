@@ -144,7 +144,14 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
             d.beta[c] = s.contract[c].beta_q16;
             if (c == 0 || d.rho[c] < rmin) rmin = d.rho[c];
         }
-        for (int c = 0; c < s.n_contracts; ++c) d.invw[c] = (rmin << 16) / d.rho[c];   // 1/w_c in Q16
+        // 1/w_c in Q16 (Eq. 5); Eq. 8's decrement 1/W_g must be positive, and
+        // Q16 holds 1/w_c only down to 2^-16
+        for (int c = 0; c < s.n_contracts; ++c) {
+            d.invw[c] = (rmin << 16) / d.rho[c];
+            if (d.invw[c] < 1)
+                return fail(PC_EINVAL, "instance %d contract %d: refill rates of one instance may differ by at most "
+                            "a factor 2^16", i, c);
+        }
         int64_t scap = (int64_t)s.capacity * s.s3_small_permille / 1000;
         if (scap < 1) scap = 1;
         d.s_cap = (int32_t)scap;

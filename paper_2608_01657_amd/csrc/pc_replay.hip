@@ -125,9 +125,9 @@ DEV int nth_bit(uint64_t m, int k) {
 }
 // floor(a / b) for 0 < b < 2^63: below 2^53 a double-precision estimate and
 // an exact integer correction (the estimate is off by at most one or two);
-// above, plain shift-and-subtract.
+// above, plain shift-and-subtract.  b = 0 returns 0 (callers never pass it).
 DEV uint64_t udiv64(uint64_t a, uint64_t b) {
-    if (a < b) return 0;
+    if (a < b || b == 0) return 0;
     if (a >> 53) {
         uint64_t q = 0, r = 0;
         for (int i = 63; i >= 0; --i) {
@@ -575,13 +575,15 @@ struct Replayer : Params<kPol, kFix> {
             }
         return d;
     }
-    DEV int64_t decrement(int64_t t) const {  // Eq. 8: 1/W_g
+    // Eq. 8: 1/W_g, the smallest decrement among indebted contracts, or 0
+    // when none is indebted (the host keeps every invw at 1 or more)
+    DEV int64_t decrement(int64_t t) const {
         if (K == 1) return eff(0, t) < 0 ? kScale : 0;
-        int64_t m = 0;
+        int64_t m = -1;
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-            if (c < K && eff(c, t) < 0 && (m == 0 || invw[c] < m)) m = invw[c];
-        return m;
+            if (c < K && eff(c, t) < 0 && (m < 0 || invw[c] < m)) m = invw[c];
+        return m < 0 ? 0 : m;
     }
 
     // ============================================================ tables
@@ -945,6 +947,7 @@ struct Replayer : Params<kPol, kFix> {
                 }
             }
             const int64_t Pg = bcast64(P, gs), Dg = bcast64(D, gs);
+            if (Dg <= 0) { err = kErrInternal; break; }   // an indebted group has a positive decrement
             const int ag = (int)bcast32(avail, gs);
             const int64_t p2 = wave_max64((inE && lane != gs) ? P : -1);
             const int64_t thr = p2 > eps ? p2 : eps;

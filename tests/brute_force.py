@@ -39,6 +39,8 @@ def brute_replay(keys, key_off, group, contract, prefix, n_groups, inst, tick=No
     K = len(rhos)
     rmin = min(rhos)
     invw = [(rmin << 16) // r for r in rhos]
+    if min(invw) < 1:
+        raise ValueError("refill rates differ by more than a factor 2^16")
     s_cap = max(1, C * inst.s3_small_permille // 1000)
     g_cap = C - s_cap
     T = inst.s3_move_threshold

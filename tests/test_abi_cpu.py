@@ -90,6 +90,21 @@ def test_contract_validation():
     assert _ws(_trace(), i) == P.PC_EINVAL and "beta" in P.pc_last_error()
 
 
+def test_contract_rate_ratio_limit():
+    """Eq. 8 needs a positive decrement 1/W_g; in Q16, 1/w_c = rho_min/rho_c
+    is representable down to 2^-16, so rates of one instance may differ by a
+    factor 2^16 at most."""
+    for slow, fast, ok in [(1, 1 << 16, True), (1, (1 << 16) + 1, False), (1 << 24, 1 << 40, True),
+                           (3, 3 << 16, True), (3, (3 << 16) + 3, False)]:
+        i = _inst(n_contracts=2)
+        i.contract[0].rho_q16, i.contract[1].rho_q16 = slow, fast
+        rc = _ws(_trace(), i)
+        if ok:
+            assert rc > 0, P.pc_last_error()
+        else:
+            assert rc == P.PC_EINVAL and "2^16" in P.pc_last_error()
+
+
 @pytest.mark.parametrize("field,value", [
     ("n_groups", 0), ("n_groups", 65), ("n_req", -1), ("d_keys", 0), ("d_key_off", 0),
 ])

@@ -81,12 +81,14 @@ def test_replay_random_key_traces(chunk):
         for pol in POLICIES:
             for flags in ([0, 1, 2, 3] if pol == tg.POLICY_PREFIXSHIELD else [0]):
                 cap = int(rng.integers(1, 90))
-                contracts = [(int(rng.integers(1, 3 * tg.Q16)), int(rng.integers(0, 40)) * tg.Q16)
+                contracts = [(int(rng.integers(3, 3 * tg.Q16)), int(rng.integers(0, 40)) * tg.Q16)
                              for _ in range(nc)]
+                # S3-FIFO also with a one-block small queue (0), no ghost
+                # (1000), every head moving (threshold 0) and none (4)
                 insts.append(tg.Instance(0, pol, cap, contracts=contracts, flags=flags,
                                          eps_q16=int(rng.choice([0, tg.Q16 // 2, 3 * tg.Q16])),
-                                         s3_small_permille=int(rng.choice([100, 250, 500])),
-                                         s3_move_threshold=int(rng.choice([1, 2]))))
+                                         s3_small_permille=int(rng.choice([0, 1, 100, 250, 500, 1000])),
+                                         s3_move_threshold=int(rng.choice([0, 1, 2, 4]))))
         kts.append(kt)
         per.append(insts)
     run_key_traces(kts, per)
@@ -439,13 +441,37 @@ def test_replay_extreme_debt_parameters():
         insts = []
         for pol in POLICIES:
             for flags in ([0, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
-                contracts = [(int(rng.choice([1, 7, 1 << 20, 1 << 40])), int(rng.choice([0, 5, 1 << 50])))
-                             for _ in range(3)]
+                # rates up to 2^40, at most a factor 2^16 apart (the Q16 limit of 1/w)
+                base = int(rng.choice([1, 7, 1 << 20, 1 << 24]))
+                contracts = [(min(1 << 40, base * int(rng.choice([1, 3, 1 << 10, 1 << 16]))),
+                              int(rng.choice([0, 5, 1 << 50]))) for _ in range(3)]
                 insts.append(tg.Instance(0, pol, int(rng.integers(20, 120)), contracts=contracts, flags=flags,
                                          eps_q16=int(rng.choice([0, 1 << 30, 1 << 50]))))
         kts.append(kt)
         per.append(insts)
     run_key_traces(kts, per)
+
+
+def test_replay_rate_ratio_at_the_q16_limit():
+    """Two contracts 2^16 apart in refill rate (the fast one's 1/w is one
+    Q16 unit, the smallest positive decrement of Eq. 8), both indebted by
+    groups that use both, with equal ticks so that no debt refills and
+    PrefixShield's victim runs are long: every policy, PrefixShield with and
+    without segmentation and its gate, per-request outputs too."""
+    kts, per = [], []
+    for seed in range(6):
+        rng = np.random.default_rng(5150 + seed)
+        kt = tg.random_key_trace(5150 + seed, n_req=200, max_blocks=30, n_groups=4, n_prefix=16,
+                                 n_contracts=2, key_universe=120)
+        kt.tick = np.zeros(kt.n_req, np.int64)
+        slow = int(rng.choice([1, 1 << 24]))
+        contracts = [(slow, 0), (slow << 16, 0)]
+        insts = [tg.Instance(0, pol, int(rng.integers(16, 100)), contracts=contracts, flags=flags)
+                 for pol in POLICIES for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0])]
+        kts.append(kt)
+        per.append(insts)
+    res = run_key_traces(kts, per)
+    assert sum(g["evicted_owned"] for groups, _, _ in res for g in groups) > 0
 
 
 def test_replay_capacity_at_most_groups():

@@ -38,9 +38,12 @@ def _instances(rng, n_contracts):
                 beta = int(rng.integers(0, 6)) * tg.Q16 + int(rng.integers(0, 2)) * int(rng.integers(0, tg.Q16))
                 contracts.append((rho, beta))
             eps = int(rng.choice([0, 0, tg.Q16 // 2, 2 * tg.Q16]))
+            # S3-FIFO: a small queue of one block (0), no ghost at all (1000),
+            # every head moving (threshold 0) and none ever moving (4 > the
+            # frequency cap of 3)
             out.append(tg.Instance(0, pol, cap, contracts=contracts, flags=flags, eps_q16=eps,
-                                   s3_small_permille=int(rng.choice([100, 250, 500])),
-                                   s3_move_threshold=int(rng.choice([1, 2]))))
+                                   s3_small_permille=int(rng.choice([0, 1, 100, 250, 500, 1000])),
+                                   s3_move_threshold=int(rng.choice([0, 1, 2, 4]))))
     return out
 
 
@@ -64,3 +67,25 @@ def test_tiny_workload_prefix_short(cap, pol):
     for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
         inst = tg.Instance(0, pol, cap, contracts=[(tg.Q16 // 2, 8 * tg.Q16)], flags=flags)
         _compare(kt, inst)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_rate_ratio_at_the_q16_limit(seed):
+    """Two contracts whose refill rates differ by exactly 2^16 (1/w of the
+    fast one is 2^-16 in Q16, the smallest positive decrement of Eq. 8),
+    both indebted by groups that share them, equal ticks so that no debt is
+    refilled: the oracle agrees with the brute force on every counter and
+    every request; one more unit of ratio is rejected by both."""
+    rng = np.random.default_rng(900 + seed)
+    kt = tg.random_key_trace(900 + seed, n_req=40, max_blocks=8, n_groups=3, n_prefix=6, n_contracts=2,
+                             key_universe=30)
+    kt.tick = np.zeros(kt.n_req, np.int64)
+    slow = int(rng.choice([1, 5, 1 << 20]))
+    for pol in POLICIES:
+        inst = tg.Instance(0, pol, int(rng.integers(4, 14)), contracts=[(slow, 0), (slow << 16, 0)])
+        _compare(kt, inst)
+    bad = tg.Instance(0, tg.POLICY_PREFIXSHIELD, 8, contracts=[(slow, 0), ((slow << 16) + 1, 0)])
+    with pytest.raises(ValueError):
+        oracle.replay_key_trace(kt, bad)
+    with pytest.raises(ValueError):
+        brute_replay(kt.keys, kt.key_off, kt.group, kt.contract, kt.prefix, kt.n_groups, bad, tick=kt.tick)

@@ -110,26 +110,41 @@ def _lognormal_len(rng, mu, sigma, size, lo=1, hi=None) -> np.ndarray:
 
 
 class _Stream:
-    """Builds a token stream from request views; fresh tokens are drawn lazily."""
+    """Builds a token stream from request parts: each request is an optional
+    prefix (an existing token array) followed by n fresh uniform tokens.
+    The parts are only recorded; tokens() allocates the stream once and draws
+    every fresh token in one call, in request order -- the same values as
+    drawing each request's fresh tokens as it comes (bounded integer draws
+    of a numpy Generator do not depend on how a run of them is split into
+    calls), with one copy of the data instead of three."""
 
     def __init__(self, rng):
         self.rng = rng
-        self.parts: List[np.ndarray] = []
+        self.parts: List[tuple] = []   # (offset, prefix or None, n_fresh)
         self.pos = 0
+        self.n_fresh = 0
 
-    def append(self, toks: np.ndarray) -> int:
+    def add(self, prefix: Optional[np.ndarray], n_fresh: int) -> int:
+        """Append a request of prefix + n_fresh fresh tokens; return its offset."""
         off = self.pos
-        self.parts.append(np.asarray(toks, dtype=np.int32))
-        self.pos += len(toks)
+        lp = 0 if prefix is None else len(prefix)
+        self.parts.append((off, prefix, int(n_fresh)))
+        self.pos += lp + int(n_fresh)
+        self.n_fresh += int(n_fresh)
         return off
 
-    def fresh(self, n: int) -> np.ndarray:
-        return self.rng.integers(0, VOCAB, size=n, dtype=np.int32)
-
     def tokens(self) -> np.ndarray:
-        if not self.parts:
-            return np.zeros(0, np.int32)
-        return np.concatenate(self.parts)
+        out = np.empty(self.pos, np.int32)
+        fresh = self.rng.integers(0, VOCAB, size=self.n_fresh, dtype=np.int32)
+        fo = 0
+        for off, prefix, nf in self.parts:
+            lp = 0
+            if prefix is not None:
+                lp = len(prefix)
+                out[off:off + lp] = prefix
+            out[off + lp:off + lp + nf] = fresh[fo:fo + nf]
+            fo += nf
+        return out
 
 
 def _finish(name, stream, offs, lens, groups, prefixes, n_groups, n_prefix, roles):
@@ -158,12 +173,10 @@ def onetouch_tiny(seed: int = 1000, n_requests: int = 4000) -> Trace:
     vi = pi = 0
     for r in range(n_requests):
         if r % 2 == 0:
-            t = np.concatenate([hot[z[vi]], st.fresh(64)])
-            offs.append(st.append(t)); lens.append(len(t)); groups.append(0)
+            offs.append(st.add(hot[z[vi]], 64)); lens.append(512 + 64); groups.append(0)
             prefixes.append(int(z[vi])); vi += 1
         else:
-            t = st.fresh(512)
-            offs.append(st.append(t)); lens.append(512); groups.append(1)
+            offs.append(st.add(None, 512)); lens.append(512); groups.append(1)
             prefixes.append(4 + pi); pi += 1
     return _finish(f"onetouch_tiny_s{seed}", st, offs, lens, groups, prefixes,
                    2, 4 + pi, {0: "victim", 1: "polluter"})
@@ -182,8 +195,7 @@ class _VictimSource:
         return _zipf_choice(self.rng, self.s, self.n_hot, count)
 
     def emit(self, st: _Stream, z: int):
-        t = np.concatenate([self.hot[z], st.fresh(self.suffix)])
-        return st.append(t), len(t), self.pid_base + int(z)
+        return st.add(self.hot[z], self.suffix), len(self.hot[z]) + self.suffix, self.pid_base + int(z)
 
 
 def _polluter_lengths(rng, n):
@@ -205,7 +217,7 @@ def onetouch_4096(seed: int = 2000, n_requests: int = 50000) -> Trace:
         if roles[r] == 0:
             o, L, pid = vic.emit(st, z[vi]); vi += 1; g = 0
         else:
-            L = int(plen[pi]); o = st.append(st.fresh(L)); pid = 32 + pi; pi += 1; g = 1
+            L = int(plen[pi]); o = st.add(None, L); pid = 32 + pi; pi += 1; g = 1
         offs.append(o); lens.append(L); groups.append(g); prefixes.append(pid)
     return _finish(f"onetouch_4096_s{seed}", st, offs, lens, groups, prefixes,
                    2, 32 + npol, {0: "victim", 1: "polluter"})
@@ -231,7 +243,7 @@ def two_pass(seed: int = 3000, n_requests: int = 80000) -> Trace:
             o, L, pid = vic.emit(st, z[vi]); vi += 1; g = 0
         else:
             if pi < n_unique:
-                L = int(plen[pi]); o = st.append(st.fresh(L)); pol_views.append((o, L))
+                L = int(plen[pi]); o = st.add(None, L); pol_views.append((o, L))
                 pid = 32 + pi
             else:
                 k = pi - n_unique
@@ -280,15 +292,14 @@ def attack_trace(kind: str, seed: int = 7000, n_requests: int = 4000) -> Trace:
     vi = pi = 0
     for r in range(n_requests):
         if not pol[r]:
-            t = np.concatenate([hot[z[vi]], st.fresh(64)])
-            offs.append(st.append(t)); lens.append(len(t)); groups.append(0)
+            offs.append(st.add(hot[z[vi]], 64)); lens.append(1536 + 64); groups.append(0)
             prefixes.append(int(z[vi])); vi += 1
         else:
             if kind == "replay" and pi % 2 == 1:
                 k = pi // 2
                 o = views[k]; pid = 4 + k
             else:
-                o = st.append(st.fresh(1536)); views.append(o); pid = 4 + len(views) - 1
+                o = st.add(None, 1536); views.append(o); pid = 4 + len(views) - 1
             offs.append(o); lens.append(1536); groups.append(1); prefixes.append(pid); pi += 1
     return _finish(f"attack_{kind}_s{seed}", st, offs, lens, groups, prefixes,
                    2, 4 + max(n_unique, 1), {0: "victim", 1: "polluter"})
@@ -309,7 +320,7 @@ def selector_trace(n_groups: int, seed: int = 8000, n_requests: int = 20000) -> 
     offs, lens, groups, prefixes = [], [], [], []
     for r in range(n_requests):
         L = int(L_[r])
-        offs.append(st.append(st.fresh(L))); lens.append(L); groups.append(int(groups_[r])); prefixes.append(r)
+        offs.append(st.add(None, L)); lens.append(L); groups.append(int(groups_[r])); prefixes.append(r)
     return _finish(f"selector_g{n_groups}_s{seed}", st, offs, lens, groups, prefixes, n_groups, n_requests, {})
 
 
@@ -343,7 +354,7 @@ def delayed_replay(seed: int = 4000, n_requests: int = 200000) -> Trace:
     for r in range(n_requests):
         if kinds[r] == 7:
             if r < b1:
-                L = int(plen[pi]); o = st.append(st.fresh(L)); pol_views.append((o, L))
+                L = int(plen[pi]); o = st.add(None, L); pol_views.append((o, L))
                 pid = 80 + pi
             else:
                 k = pi - n_unique
@@ -355,8 +366,7 @@ def delayed_replay(seed: int = 4000, n_requests: int = 200000) -> Trace:
             g = int(other_groups[oi])
             if g < 6:
                 zz = int(zb[oi])
-                t = np.concatenate([benign_hot[g][zz], st.fresh(128)])
-                o = st.append(t); L = len(t); pid = 8 * g + zz
+                o = st.add(benign_hot[g][zz], 128); L = 2048 + 128; pid = 8 * g + zz
             else:
                 o, L, pid = vic.emit(st, zv[oi])
             oi += 1
@@ -401,11 +411,10 @@ def tiered_contracts(seed: int = 6000, n_requests: int = 50000) -> Trace:
             o, L, pid = vic.emit(st, zv[r]); c = 0
         elif g in (1, 2, 3):
             z = int(zb[r])
-            t = np.concatenate([hot[g][z], st.fresh(128)])
-            o = st.append(t); L = len(t); pid = 32 + 8 * (g - 1) + z
+            o = st.add(hot[g][z], 128); L = 2048 + 128; pid = 32 + 8 * (g - 1) + z
             c = 1 if g == 1 else 2 if g == 2 else (1 if z < 4 else 2)
         else:
-            L = int(plen[r]); o = st.append(st.fresh(L)); pid = 56 + n_unique; n_unique += 1
+            L = int(plen[r]); o = st.add(None, L); pid = 56 + n_unique; n_unique += 1
             c = 0 if g == 4 else 2
         offs.append(o); lens.append(L); groups.append(g); prefixes.append(pid); contracts.append(c)
     tr = _finish(f"tiered_contracts_s{seed}", st, offs, lens, groups, prefixes, 6, 56 + n_unique,

@@ -6,9 +6,12 @@ resident in HBM: block offsets and chained keys for every trace (hashing),
 then replay of every instance (LRU, S3-FIFO, PrefixShield) from an empty
 cache.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload onetouch4096|scale1024|...]
+  python bench.py [--steps K] [--warmup W] [--workload scale1024|onetouch4096|chat|...]
 
-value = block probes / s of the whole step (requests/s is reported beside it).
+The default workload is the 1,024-instance batch: 16 one-touch traces of
+50,000 requests, each replayed by 64 concurrent 4096-block instances (LRU,
+S3-FIFO, PrefixShield at 62 refill rates).  value = block probes / s of the
+whole step (requests/s is reported beside it).
 """
 from __future__ import annotations
 
@@ -23,10 +26,11 @@ import numpy as np
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 ROOT = os.path.dirname(os.path.abspath(__file__))
-# measured HBM bytes of the replay kernel for the default batch (rocprofv3
-# FETCH_SIZE / WRITE_SIZE, calibrated against a device copy); valid only for
-# the kernel source it was measured on
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "replay_kernel_onetouch4096_hbm_traffic.txt")
+# Counter summaries of the replay kernel per workload (rocprofv3, committed
+# under profiles/): calibrated HBM bytes (FETCH_SIZE / WRITE_SIZE against a
+# device copy) and LDS / occupancy figures.  Each is valid only for the batch
+# and the kernel source it was measured on.
+PROFILES = os.path.join(ROOT, "profiles")
 # what the replay kernel is built from: its sources and its compiler flags
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_01657_amd", *f) for f in
                   (("csrc", "pc_replay.hip"), ("csrc", "pc_internal.h"), ("build.py",))]
@@ -41,12 +45,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="onetouch4096")
+    ap.add_argument("--workload", default="scale1024")
     ap.add_argument("--seeds", type=int, default=None, help="number of traces (default: the workload's)")
     ap.add_argument("--requests", type=int, default=None, help="requests per trace (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-requests", type=int, default=0,
                     help="requests per trace in the oracle baseline (0: all of them)")
+    ap.add_argument("--cpu-sample-traces", type=int, default=0,
+                    help="traces whose instances the oracle baseline replays (0: enough for one instance "
+                         "per host thread)")
     ap.add_argument("--phase-profile", action="store_true",
                     help="use the phase-counter library and add per-phase cycles, reclamation latency per "
                          "evicting request and state bytes per cached block to the JSON line")
@@ -65,22 +72,45 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic(workload, n_traces, n_req):
-    """HBM bytes per replay launch from the committed counter summary, or
-    None when it was taken on another kernel source or another batch."""
-    if not os.path.exists(TRAFFIC_PROFILE):
+def profile_keys(path, workload, n_traces, n_req):
+    """The key: value lines of a committed counter summary, or None when it
+    is missing or was taken on another batch or kernel source."""
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_PROFILE):
-        if ":" in line and not line.startswith("#"):
+    for line in open(path):
+        if ":" in line and not line.startswith("#") and not line.startswith(" "):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
     if kv.get("kernel_source_sha256") != kernel_source_hash():
         return None
     if kv.get("batch") != f"{workload} traces={n_traces} requests={n_req}":
         return None
+    return kv
+
+
+def measured_traffic(workload, n_traces, n_req):
+    """HBM bytes per replay launch (calibrated FETCH_SIZE + WRITE_SIZE)."""
+    kv = profile_keys(os.path.join(PROFILES, f"replay_kernel_{workload}_hbm_traffic.txt"), workload, n_traces, n_req)
     try:
-        return int(kv["traffic_bytes_per_launch"])
+        return int(kv["traffic_bytes_per_launch"]) if kv else None
+    except (KeyError, ValueError):
+        return None
+
+
+def measured_lds(workload, n_traces, n_req):
+    """LDS side of the replay roofline from the committed counter summary:
+    the fraction of kernel cycles a CU's LDS is busy, the share of those
+    cycles lost to bank conflicts, and workgroups (instances) per busy CU."""
+    kv = profile_keys(os.path.join(PROFILES, f"replay_kernel_{workload}_lds_occupancy.txt"), workload, n_traces,
+                      n_req)
+    if not kv:
+        return None
+    try:
+        return {"lds_busy_frac": float(kv["lds_busy_per_cu_frac"]),
+                "bank_conflict_frac_of_busy": float(kv["lds_bank_conflict_frac"]),
+                "instances_per_cu": float(kv["mean_workgroups_per_active_cu"]),
+                "source": f"profiles/replay_kernel_{workload}_lds_occupancy.txt"}
     except (KeyError, ValueError):
         return None
 
@@ -177,6 +207,7 @@ def main():
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round((replay_gbs if dominant == "replay" else hash_gbs) / HBM_PEAK_GBS, 6),
             "traffic": measured_traffic(args.workload, len(traces), traces[0].n_req) if dominant == "replay" else None,
+            "lds": measured_lds(args.workload, len(traces), traces[0].n_req) if dominant == "replay" else None,
             "bytes_per_launch": int(replay_bytes if dominant == "replay" else hash_bytes),
             "avg_launch_ms": round(replay_ms if dominant == "replay" else hash_ms, 4)}
     roof_hash = {"kernel": "hash_kernel (+ block offsets)", "bound": "hbm", "achieved": round(hash_gbs, 2),
@@ -186,7 +217,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(traces, insts, args.cpu_sample_requests)
+        cpu = cpu_baseline(traces, insts, args.cpu_sample_requests, args.cpu_sample_traces)
 
     phases = phase_report(batch, insts, traces, replay_ms) if args.phase_profile else None
 
@@ -246,30 +277,60 @@ def phase_report(batch, insts, traces, replay_ms):
     return rep
 
 
-def cpu_baseline(traces, insts, sample_requests):
-    """The oracle (plain single-threaded C per instance) on the host cores:
-    hash of the first `sample_requests` requests of every trace (all of them
-    if 0), then replay of every instance over them, one thread per task."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(traces, insts, sample_requests, sample_traces):
+    """The oracle (plain single-threaded C per instance) on the host cores,
+    one instance per thread on every host core: hash of the sampled traces
+    (their first `sample_requests` requests, all if 0), then replay of every
+    instance of those traces.  The sample is the first traces of the
+    workload, enough of them for one instance per thread (the instances of
+    one trace are the workload's mix of policies and parameters)."""
     import oracle
     from paper_2608_01657_amd import tracegen as tg
 
-    cores = min(16, os.cpu_count() or 1)
+    nproc = os.cpu_count() or 1
+    n_tr = sample_traces
+    if n_tr <= 0:
+        n_tr, per = 0, 0
+        while n_tr < len(traces) and per < nproc:
+            per += sum(1 for i in insts if i.trace == n_tr)
+            n_tr += 1
+    n_tr = max(1, min(n_tr, len(traces)))
     sub = []
-    for tr in traces:
+    for tr in traces[:n_tr]:
         n = tr.n_req if sample_requests <= 0 else min(sample_requests, tr.n_req)
         sub.append(tg.Trace(tr.name, tr.tokens, tr.tok_off[:n], tr.length[:n], tr.group[:n], tr.contract[:n],
                             tr.prefix[:n], tr.n_groups, tr.n_prefix, None if tr.tick is None else tr.tick[:n]))
+    sample = [i for i in insts if i.trace < n_tr]
+    threads = max(1, min(nproc, len(sample)))
     t0 = time.perf_counter()
-    with ThreadPoolExecutor(max_workers=cores) as ex:
+    c0 = time.process_time()
+    with ThreadPoolExecutor(max_workers=threads) as ex:
         hashed = list(ex.map(oracle.hash_trace, sub))
         results = list(ex.map(lambda i: oracle.replay_trace(sub[i.trace], hashed[i.trace][0],
-                                                             hashed[i.trace][1], i), insts))
+                                                             hashed[i.trace][1], i), sample))
     wall = time.perf_counter() - t0
+    cpu_s = time.process_time() - c0
     probes = sum(sum(g["probes"] for g in r.groups) for r in results)
-    return {"value": probes / wall, "unit": "probes/s", "cores": cores, "kind": "oracle",
-            "sample": f"{'all' if all(s.n_req == t.n_req for s, t in zip(sub, traces)) else 'first'} "
-                      f"{sub[0].n_req} requests of each of the {len(sub)} traces, all {len(insts)} "
-                      f"instances: oracle hash + replay, {probes} probes in {wall:.2f}s wall"}
+    reqs = sum(sub[i.trace].n_req for i in sample)
+    return {"value": probes / wall, "unit": "probes/s", "cores": threads, "kind": "oracle",
+            "nproc": nproc, "cpu_model": cpu_model(),
+            "requests_per_s": reqs / wall, "probes_per_s_per_thread": probes / cpu_s if cpu_s > 0 else None,
+            "sample": f"{'all' if all(s.n_req == t.n_req for s, t in zip(sub, traces)) else 'the first'} "
+                      f"{sub[0].n_req} requests of trace{'s' if n_tr > 1 else ''} 0"
+                      f"{'-' + str(n_tr - 1) if n_tr > 1 else ''} of {len(traces)}, all {len(sample)} of their "
+                      f"instances (of {len(insts)}): oracle hash + replay, {probes} probes, "
+                      f"{cpu_s:.1f}s CPU in {wall:.2f}s wall on {threads} threads"}
 
 
 if __name__ == "__main__":

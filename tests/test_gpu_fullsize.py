@@ -1,17 +1,23 @@
-"""GPU parity at the full sizes of the five workloads.
+"""GPU parity at the full sizes of the five workloads and the 1,024-instance
+scale batch: every instance of every workload is compared with the oracle.
 
-Every instance is a full-length trace.  The one-touch 4096-block batch is
-replayed exactly as bench.py times it (16 traces x 3 policies = 48
-instances, 50,000 requests each, one batch) and every instance is compared
-with the oracle.  The larger batches are replayed on a sample of their seeds
-(the trace length, capacities, policies and refill sweep are the full ones);
-there the oracle checks a sample of instances and every instance is checked
-against invariants that hold at any size."""
+Each workload is replayed as bench.py times it: all its traces keyed on the
+GPU, then every instance in one pc_replay_batch launch.  The oracle keys every
+trace (compared with the GPU's keys in full) and replays every instance, one
+host thread per instance.  Traces are generated one seed at a time and their
+token arrays dropped once keyed, so host memory holds only keys and request
+descriptors; the oracle works on the seeds already keyed while the next seed
+is generated.  Every instance is also checked against invariants that hold
+at any size."""
+import dataclasses
 import os
+import sys
+import time
 from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 import pytest
+import torch
 
 import oracle
 from gpu_util import assert_same
@@ -21,6 +27,10 @@ from paper_2608_01657_amd import tracegen as tg
 pytestmark = pytest.mark.gpu
 
 WORKERS = min(16, os.cpu_count() or 1)
+
+
+def _log(msg):
+    print(f"[fullsize {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
 def _hash_all(traces, check_keys=(0,)):
@@ -78,51 +88,117 @@ def _replay_and_compare(traces, insts, dts, okeys, oracle_ids):
     return res
 
 
+@dataclasses.dataclass
+class _Requests:
+    """A trace without its tokens: what the replay (both sides) reads."""
+    name: str
+    group: np.ndarray
+    contract: np.ndarray
+    prefix: np.ndarray
+    n_groups: int
+    n_prefix: int
+    tick: object
+    n_req: int
+
+
+def _full_workload(name, n_seeds, policies=tg.ALL_POLICIES):
+    """Every seed of workload `name`: keys on both sides (compared in full),
+    all instances replayed in one GPU launch and every one compared with the
+    oracle.  Returns the number of instances compared."""
+    t0 = time.time()
+    pool = ThreadPoolExecutor(WORKERS)
+    dts, reqs, insts, key_futs, orc_futs = [], [], [], [], []
+
+    def oracle_replay(k, spec):
+        okeys, ooff = key_futs[spec.trace].result()
+        return k, oracle.replay_trace(reqs[spec.trace], okeys, ooff, spec)
+
+    try:
+        for i in range(n_seeds):
+            trs, its = tg.workload(name, seeds=[i], policies=policies)
+            tr = trs[0]
+            ti = len(dts)
+            t = dv.upload(tr)
+            dv.cut_and_hash(t)
+            key_futs.append(pool.submit(oracle.hash_trace, tr))
+            t.tokens = t.tokens[:0]          # keys are made: the replay never reads tokens
+            dts.append(t)
+            reqs.append(_Requests(tr.name, tr.group, tr.contract, tr.prefix, tr.n_groups, tr.n_prefix, tr.tick,
+                                  tr.n_req))
+            del tr, trs
+            for spec in its:
+                k = len(insts)
+                insts.append(dataclasses.replace(spec, trace=ti))
+                orc_futs.append(pool.submit(oracle_replay, k, insts[k]))
+            if i % 8 == 7 or i == n_seeds - 1:
+                _log(f"{name}: {i + 1}/{n_seeds} seeds generated and keyed ({time.time() - t0:.0f}s)")
+        torch.cuda.synchronize()
+        for i, t in enumerate(dts):
+            assert int(t.status.item()) == 0, f"{name} seed {i}: hash status"
+            okeys, ooff = key_futs[i].result()
+            assert np.array_equal(t.key_off.cpu().numpy(), ooff), f"{name} seed {i}: key offsets differ"
+            keys = t.keys[:t.n_keys].cpu().numpy().view(np.uint64)
+            bad = np.flatnonzero(keys != okeys)
+            assert bad.size == 0, f"{name} seed {i}: {bad.size} keys differ, first at {bad[:5]}"
+        b = dv.ReplayBatch(dts, insts)
+        b.launch()
+        res = b.results()
+        _log(f"{name}: {len(insts)} instances replayed on the GPU ({time.time() - t0:.0f}s)")
+        for n_done, f in enumerate(orc_futs):
+            k, o = f.result()
+            spec = insts[k]
+            assert_same(res[k], o, f"{name} instance {k} ({spec.label}, seed {spec.trace})")
+            _invariants(res[k][0], res[k][1], spec, reqs[spec.trace].n_req)
+            if n_done % 256 == 255:
+                _log(f"{name}: {n_done + 1}/{len(insts)} instances equal to the oracle ({time.time() - t0:.0f}s)")
+        _log(f"{name}: all {len(insts)} instances equal to the oracle ({time.time() - t0:.0f}s)")
+        return len(insts)
+    finally:
+        pool.shutdown(wait=True, cancel_futures=True)
+
+
+@pytest.mark.timeout(900)
 def test_onetouch4096_bench_batch_all_instances():
-    traces, insts = tg.workload("onetouch4096")
-    assert len(insts) == 48 and all(t.n_req == 50000 for t in traces)
-    dts, okeys = _hash_all(traces, check_keys=range(len(traces)))
-    _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))
+    """Config 2: 16 seeds x 3 policies = 48 concurrent 4096-block instances."""
+    assert _full_workload("onetouch4096", 16) == 48
 
 
-def test_twopass_full_length_sampled_seeds():
-    traces, insts = tg.workload("twopass", seeds=[0, 1, 2, 3])
-    assert all(t.n_req == 80000 for t in traces)
+@pytest.mark.timeout(900)
+def test_twopass_all_instances():
+    """Config 3: 32 seeds x 3 policies = 96 instances of 80,000 requests."""
+    assert _full_workload("twopass", 32) == 96
+
+
+@pytest.mark.timeout(900)
+def test_delayed_all_instances():
+    """Config 4: 8 seeds x 8 refill rates x 3 policies = 192 instances of
+    200,000 requests; the middle rates clear the polluter's debt inside the
+    50,000-request gap (Sec. V-D's delayed replay)."""
+    assert _full_workload("delayed", 8) == 192
+
+
+@pytest.mark.timeout(900)
+def test_chat_all_instances():
+    """Config 5: 64 seeds x 5 capacities (1K-16K blocks; 8K and 16K keep
+    their state in the workspace) x 3 policies = 960 instances of 100,000
+    requests."""
+    assert _full_workload("chat", 64) == 960
+
+
+@pytest.mark.timeout(900)
+def test_scale1024_all_instances():
+    """1,024 concurrent 4096-block instances (16 traces x LRU, S3-FIFO and
+    PrefixShield at 62 refill rates), as bench.py times them."""
+    assert _full_workload("scale1024", 16) == 1024
+
+
+def test_chat_staticquota_full_length():
+    """StaticQuota on the conversational traces: 16 partitions, so at 1,024
+    blocks a 64-block partition truncates most long prompts; every capacity."""
+    traces, insts = tg.workload("chat", seeds=[0, 1], policies=(tg.POLICY_STATICQUOTA,))
+    assert all(t.n_req == 100000 for t in traces) and len(insts) == 10
     dts, okeys = _hash_all(traces)
     _replay_and_compare(traces, insts, dts, okeys, range(len(insts)))
-
-
-def test_delayed_full_length_refill_sweep():
-    traces, insts = tg.workload("delayed", seeds=[0, 1])
-    assert all(t.n_req == 200000 for t in traces) and len(insts) == 48
-    dts, okeys = _hash_all(traces)
-    # oracle: every policy at the lowest and highest refill rate of seed 0
-    sample = [k for k, i in enumerate(insts) if i.trace == 0 and ("_rho1" == i.label[-5:] or i.label.endswith("_rho128"))]
-    assert len(sample) == 6
-    _replay_and_compare(traces, insts, dts, okeys, sample)
-
-
-def test_chat_full_length_all_capacities():
-    """Capacities up to 16,384 blocks: the larger ones keep their state in the
-    workspace instead of LDS.  StaticQuota too: 16 partitions, so at 1,024
-    blocks a 64-block partition truncates most long prompts."""
-    traces, insts = tg.workload("chat", seeds=[0, 1], policies=tg.ALL_POLICIES + (tg.POLICY_STATICQUOTA,))
-    assert all(t.n_req == 100000 for t in traces) and len(insts) == 40
-    dts, okeys = _hash_all(traces)
-    sample = [k for k, i in enumerate(insts) if i.trace == 0]
-    _replay_and_compare(traces, insts, dts, okeys, sample)
-
-
-def test_scale1024_sampled():
-    """1,024 concurrent 4096-block instances (16 traces x 64 policy variants);
-    the oracle checks LRU, S3-FIFO and three refill rates of one trace."""
-    traces, insts = tg.workload("scale1024")
-    assert len(insts) == 1024
-    dts, okeys = _hash_all(traces)
-    sample = [k for k, i in enumerate(insts) if i.trace == 5 and
-              (i.policy != tg.POLICY_PREFIXSHIELD or i.label.split("rho")[-1] in ("1/4", "16/4", "62/4"))]
-    assert len(sample) == 5
-    _replay_and_compare(traces, insts, dts, okeys, sample)
 
 
 def test_tiers_full_length_all_instances():

@@ -192,6 +192,27 @@ int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces,
                         void *d_workspace, int64_t workspace_bytes, void *d_stats,
                         int32_t *d_per_request, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid allocation): the same
+ * replay as pc_replay_batch, with the workspace taken from a static device
+ * array of PC_STATIC_WORKSPACE_BYTES that the library holds on every GPU it
+ * runs on, until the process ends.  The call allocates no device memory and
+ * no pinned host memory; the caller still passes d_stats and d_per_request
+ * (as for pc_replay_batch).
+ *   - A batch whose workspace (pc_replay_workspace_bytes) exceeds
+ *     PC_STATIC_WORKSPACE_BYTES is rejected with PC_ENOMEM, queuing nothing.
+ *   - Every call on one GPU uses that GPU's one array.  The kernels clear
+ *     what they need, so a call never depends on an earlier call's
+ *     contents, but calls whose work overlaps on one GPU (other streams, or
+ *     another host thread) race on the array and give undefined results:
+ *     order them on one stream.
+ *   - The descriptor upload copies from pageable host memory, which the
+ *     runtime has read when the call returns. */
+#define PC_STATIC_WORKSPACE_BYTES (64LL << 20)
+int32_t pc_replay_batch_static(const pc_trace_desc *traces, int32_t n_traces,
+                               const pc_instance_desc *inst, int32_t n_inst, void *d_stats,
+                               int32_t *d_per_request, void *stream);
+
 /* Synchronize `stream`, copy the stats of one instance (or of all n_inst
  * when instance == -1) to the host and decode them: per-group hits, misses
  * and evictions, charged blocks (Eq. 2), the raw debt D_g of Eq. 3 (final,

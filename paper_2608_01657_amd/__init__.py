@@ -74,7 +74,8 @@ class pc_instance_stats(ctypes.Structure):
 
 
 EXPORTS = ["pc_last_error", "pc_block_offsets", "pc_hash_blocks", "pc_replay_workspace_bytes",
-           "pc_replay_state_bytes", "pc_replay_batch", "pc_get_stats"]
+           "pc_replay_state_bytes", "pc_replay_batch", "pc_replay_batch_static", "pc_get_stats"]
+PC_STATIC_WORKSPACE_BYTES = 64 << 20
 
 _lib = None
 
@@ -122,6 +123,9 @@ def lib():
         L.pc_replay_batch.restype = i32
         L.pc_replay_batch.argtypes = [ctypes.POINTER(pc_trace_desc), i32, ctypes.POINTER(pc_instance_desc),
                                       i32, P, i64, P, P, P]
+        L.pc_replay_batch_static.restype = i32
+        L.pc_replay_batch_static.argtypes = [ctypes.POINTER(pc_trace_desc), i32, ctypes.POINTER(pc_instance_desc),
+                                             i32, P, P, P]
         L.pc_get_stats.restype = i32
         L.pc_get_stats.argtypes = [P, i32, i32, ctypes.POINTER(pc_group_stats), i32,
                                    ctypes.POINTER(pc_instance_stats), P]
@@ -197,6 +201,13 @@ def pc_replay_batch(traces, instances, workspace, stats, per_request=None, strea
     return _check(lib().pc_replay_batch(T, len(traces), I, len(instances), _ptr(workspace),
                                         int(workspace.numel() * workspace.element_size()), _ptr(stats),
                                         _ptr(per_request), _stream(stream)))
+
+
+def pc_replay_batch_static(traces, instances, stats, per_request=None, stream=None):
+    """pc_replay_batch on the library's static workspace (allocates nothing)."""
+    T, I = _descs(traces, instances)
+    return _check(lib().pc_replay_batch_static(T, len(traces), I, len(instances), _ptr(stats),
+                                               _ptr(per_request), _stream(stream)))
 
 
 def pc_get_stats(stats, n_inst: int, instance: int = -1, max_groups: int = 64, stream=None):

@@ -312,6 +312,63 @@ int32_t pc_replay_state_bytes(const pc_trace_desc *traces, int32_t n_traces, con
     return ok();
 }
 
+}  // extern "C"
+
+namespace {
+
+// Descriptor header of a planned batch (DevInst[], DevTrace[], order[]), as
+// the kernels find it at the start of the workspace.
+void fill_header(const Plan &P, int32_t n_traces, int32_t n_inst, uint8_t *h) {
+    const size_t o_tr = align_up((int64_t)sizeof(pcr::DevInst) * n_inst, 256);
+    const size_t o_ord = align_up((int64_t)o_tr + (int64_t)sizeof(pcr::DevTrace) * n_traces, 256);
+    std::memset(h, 0, (size_t)P.hdr_bytes);
+    std::memcpy(h, P.di.data(), sizeof(pcr::DevInst) * n_inst);
+    if (n_traces) std::memcpy(h + o_tr, P.dt.data(), sizeof(pcr::DevTrace) * n_traces);
+    std::memcpy(h + o_ord, P.order.data(), sizeof(int32_t) * n_inst);
+}
+
+// Launches of a planned batch whose header is already queued for upload to
+// the start of `ws`.
+int32_t launch_planned(const Plan &P, int32_t n_traces, int32_t n_inst, uint8_t *ws, void *d_stats,
+                       int32_t *d_per_request, hipStream_t s) {
+    const size_t o_tr = align_up((int64_t)sizeof(pcr::DevInst) * n_inst, 256);
+    const size_t o_ord = align_up((int64_t)o_tr + (int64_t)sizeof(pcr::DevTrace) * n_traces, 256);
+    const pcr::DevInst *d_inst = (const pcr::DevInst *)ws;
+    const pcr::DevTrace *d_tr = (const pcr::DevTrace *)(ws + o_tr);
+    const int32_t *d_ord = (const int32_t *)(ws + o_ord);
+    hipError_t e;
+    if (P.n_lds > 0) {
+        e = pcr::launch_replay(d_inst, d_tr, d_ord, P.n_lds, P.lds_bytes, true, ws, (int64_t *)d_stats, d_per_request, s);
+        if (e != hipSuccess) return hip_fail(e, "replay launch (LDS)");
+    }
+    if (n_inst - P.n_lds > 0) {
+        e = pcr::launch_replay(d_inst, d_tr, d_ord + P.n_lds, n_inst - P.n_lds, 0, false, ws, (int64_t *)d_stats,
+                               d_per_request, s);
+        if (e != hipSuccess) return hip_fail(e, "replay launch (workspace)");
+    }
+    return ok();
+}
+
+struct StaticScratch {
+    std::mutex mu;
+    void *ptr[64] = {};
+    // descriptor header staging (pageable host memory: the copy from it has
+    // completed when hipMemcpyAsync returns)
+    std::vector<uint8_t> host;
+};
+StaticScratch g_static;
+
+}  // namespace
+
+// ---- the entry point that allocates nothing takes its workspace from this
+// array.  Each GPU the library runs on holds its own copy until the process
+// ends.  Host code never uses the array's name as an address (on the host it
+// only names the symbol): the device address comes from hipGetSymbolAddress,
+// once per device with that device current, and is kept in g_static.ptr.
+static __device__ __align__(256) uint8_t scratch[PC_STATIC_WORKSPACE_BYTES];
+
+extern "C" {
+
 int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst, int32_t n_inst,
                         void *d_workspace, int64_t workspace_bytes, void *d_stats, int32_t *d_per_request,
                         void *stream) {
@@ -325,9 +382,6 @@ int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces, const pc_
         return fail(PC_ENOMEM, "workspace %lld bytes < required %lld", (long long)workspace_bytes, (long long)P.ws_bytes);
     hipStream_t s = (hipStream_t)stream;
     uint8_t *ws = (uint8_t *)d_workspace;
-    const size_t o_inst = 0;
-    const size_t o_tr = align_up((int64_t)sizeof(pcr::DevInst) * n_inst, 256);
-    const size_t o_ord = align_up((int64_t)o_tr + (int64_t)sizeof(pcr::DevTrace) * n_traces, 256);
     const size_t nbytes = (size_t)P.hdr_bytes;
     {
         std::lock_guard<std::mutex> lk(g_stage.mu);
@@ -349,31 +403,46 @@ int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces, const pc_
             e = hipEventCreateWithFlags(&g_stage.done, hipEventDisableTiming);
             if (e != hipSuccess) return hip_fail(e, "event create");
         }
-        uint8_t *h = (uint8_t *)g_stage.buf;
-        std::memset(h, 0, nbytes);
-        std::memcpy(h + o_inst, P.di.data(), sizeof(pcr::DevInst) * n_inst);
-        if (n_traces) std::memcpy(h + o_tr, P.dt.data(), sizeof(pcr::DevTrace) * n_traces);
-        std::memcpy(h + o_ord, P.order.data(), sizeof(int32_t) * n_inst);
-        e = hipMemcpyAsync(ws, h, nbytes, hipMemcpyHostToDevice, s);
+        fill_header(P, n_traces, n_inst, (uint8_t *)g_stage.buf);
+        e = hipMemcpyAsync(ws, g_stage.buf, nbytes, hipMemcpyHostToDevice, s);
         if (e != hipSuccess) return hip_fail(e, "descriptor upload");
         e = hipEventRecord(g_stage.done, s);
         if (e != hipSuccess) return hip_fail(e, "event record");
         g_stage.pending = true;
     }
-    const pcr::DevInst *d_inst = (const pcr::DevInst *)(ws + o_inst);
-    const pcr::DevTrace *d_tr = (const pcr::DevTrace *)(ws + o_tr);
-    const int32_t *d_ord = (const int32_t *)(ws + o_ord);
-    hipError_t e;
-    if (P.n_lds > 0) {
-        e = pcr::launch_replay(d_inst, d_tr, d_ord, P.n_lds, P.lds_bytes, true, ws, (int64_t *)d_stats, d_per_request, s);
-        if (e != hipSuccess) return hip_fail(e, "replay launch (LDS)");
+    return launch_planned(P, n_traces, n_inst, ws, d_stats, d_per_request, s);
+}
+
+int32_t pc_replay_batch_static(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst,
+                               int32_t n_inst, void *d_stats, int32_t *d_per_request, void *stream) {
+    Plan P;
+    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_limit(), P);
+    if (rc != PC_OK) return rc;
+    if (n_inst == 0) return ok();
+    if (!d_stats) return fail(PC_EINVAL, "null stats");
+    if (P.ws_bytes > (int64_t)PC_STATIC_WORKSPACE_BYTES)
+        return fail(PC_ENOMEM, "batch needs %lld workspace bytes, more than the %lld of the static workspace",
+                    (long long)P.ws_bytes, (long long)PC_STATIC_WORKSPACE_BYTES);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "current device");
+    if (dev < 0 || dev >= 64) return fail(PC_EUNSUPPORTED, "device %d (at most 64 devices)", dev);
+    hipStream_t s = (hipStream_t)stream;
+    std::lock_guard<std::mutex> lk(g_static.mu);
+    if (!g_static.ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "static workspace address");
+        if (!p || ((uintptr_t)p & 255) != 0) return fail(PC_EDEVICE, "static workspace is not 256-byte aligned");
+        g_static.ptr[dev] = p;
     }
-    if (n_inst - P.n_lds > 0) {
-        e = pcr::launch_replay(d_inst, d_tr, d_ord + P.n_lds, n_inst - P.n_lds, 0, false, ws, (int64_t *)d_stats,
-                               d_per_request, s);
-        if (e != hipSuccess) return hip_fail(e, "replay launch (workspace)");
-    }
-    return ok();
+    uint8_t *ws = (uint8_t *)g_static.ptr[dev];
+    const size_t nbytes = (size_t)P.hdr_bytes;
+    if (g_static.host.size() < nbytes) g_static.host.resize(nbytes);
+    fill_header(P, n_traces, n_inst, g_static.host.data());
+    e = hipMemcpyAsync(ws, g_static.host.data(), nbytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "descriptor upload");
+    return launch_planned(P, n_traces, n_inst, ws, d_stats, d_per_request, s);
 }
 
 int32_t pc_get_stats(const void *d_stats, int32_t n_inst, int32_t instance, pc_group_stats *groups_out,

@@ -190,3 +190,25 @@ def test_default_4096_layout_is_sized_for_512_block_requests():
                                                    _inst(policy=0, capacity=4095, trace=0),
                                                    _inst(policy=0, capacity=4095, trace=1)])
     assert b[0] < b[1] and b[2] < b[3]
+
+
+def test_static_entry_rejects_batches_beyond_its_array():
+    """The entry point that allocates nothing refuses, on the host, a batch
+    whose workspace exceeds the static array (PC_ENOMEM), and a null stats
+    pointer (PC_EINVAL)."""
+    lib = P.lib()
+    t = _trace(n_prefix=1 << 31)            # prefix bitmaps alone need 512 MiB
+    T = (P.pc_trace_desc * 1)(t)
+    I = (P.pc_instance_desc * 1)(_inst())
+    need = lib.pc_replay_workspace_bytes(T, 1, I, 1)
+    assert need > P.PC_STATIC_WORKSPACE_BYTES
+    assert lib.pc_replay_batch_static(T, 1, I, 1, FAKE, None, None) == P.PC_ENOMEM
+    assert "static workspace" in P.pc_last_error()
+    T = (P.pc_trace_desc * 1)(_trace())
+    assert lib.pc_replay_batch_static(T, 1, I, 1, None, None, None) == P.PC_EINVAL
+
+
+def test_static_workspace_size_matches_header():
+    src = open(os.path.join(ROOT, "include", "pc.h")).read()
+    m = re.search(r"#define PC_STATIC_WORKSPACE_BYTES \((\d+)LL << (\d+)\)", src)
+    assert m and (int(m.group(1)) << int(m.group(2))) == P.PC_STATIC_WORKSPACE_BYTES

@@ -259,7 +259,7 @@ def phase_report(batch, insts, traces, replay_ms):
     pcs = batch.phase_counters()
     totals = [sum(pc[f"cycles_{n}"] for n in P.PHASE_NAMES) for pc in pcs]
     mhz = max(totals) / (replay_ms * 1e3)   # cycles per microsecond
-    sbytes, in_lds = P.pc_replay_state_bytes(batch.tdesc, batch.idesc)
+    sbytes, layout = P.pc_replay_state_bytes(batch.tdesc, batch.idesc)
     rep = {"clock_cycles_per_us": round(mhz, 1)}
     for pol in sorted({i.policy for i in insts}):
         ks = [k for k, i in enumerate(insts) if i.policy == pol]
@@ -270,7 +270,7 @@ def phase_report(batch, insts, traces, replay_ms):
         r["reclaim_us_per_evicting_request"] = round(sum(pcs[k]["cycles_reclamation"] for k in ks) / max(ev, 1) / mhz, 3)
         r["evicting_requests"] = ev
         r["state_bytes_per_block"] = round(float(np.mean([sbytes[k] / insts[k].capacity for k in ks])), 1)
-        r["state_in_lds"] = all(in_lds[k] for k in ks)
+        r["state_layout"] = sorted({P.LAYOUT_NAMES[layout[k]] for k in ks})
         for n in P.PHASE_EVENTS[1:]:
             r[n] = sum(pcs[k][n] for k in ks)
         rep[tg.POLICY_NAMES[pol]] = r

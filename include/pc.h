@@ -165,17 +165,26 @@ int64_t pc_replay_workspace_bytes(const pc_trace_desc *traces, int32_t n_traces,
                                   const pc_instance_desc *inst, int32_t n_inst);
 
 /* Per-instance replay state (the cache metadata: block keys and metadata,
- * the free-queue log, the block and ghost tables, per-request scratch) that
- * pc_replay_batch would use for this batch: bytes_out[i] bytes, kept in LDS
- * (in_lds_out[i] = 1) or in the workspace (0).  Host only; validates like
- * pc_replay_workspace_bytes.  The per-prefix bitmaps and the S3-FIFO ghost
- * ring live in the workspace and are not counted. */
+ * stamps, the free-queue log, the block and ghost tables, per-request
+ * scratch) that pc_replay_batch would use for this batch: bytes_out[i]
+ * bytes, laid out as layout_out[i] says:
+ *   PC_LAYOUT_LDS     all of it in LDS
+ *   PC_LAYOUT_HYBRID  block keys and prefix ids in the workspace, the rest
+ *                     in LDS (chosen when it lets more instances share a CU)
+ *   PC_LAYOUT_WS      all of it in the workspace (when it does not fit LDS)
+ * Host only; validates like pc_replay_workspace_bytes.  The per-prefix
+ * bitmaps and the S3-FIFO ghost ring live in the workspace and are not
+ * counted. */
+#define PC_LAYOUT_LDS 0
+#define PC_LAYOUT_HYBRID 1
+#define PC_LAYOUT_WS 2
 int32_t pc_replay_state_bytes(const pc_trace_desc *traces, int32_t n_traces,
                               const pc_instance_desc *inst, int32_t n_inst,
-                              int64_t *bytes_out, int32_t *in_lds_out);
+                              int64_t *bytes_out, int32_t *layout_out);
 
 /* Replay every instance over its trace, one workgroup per instance; queued
- * on `stream`.  Per request it runs the hooks of Alg. 1 (OnRequest, OnTouch
+ * on `stream` (instances of different LDS footprints run as separate
+ * launches on library streams that fork from and join back into it).  Per request it runs the hooks of Alg. 1 (OnRequest, OnTouch
  * with the debt gate of Eq. 4, OnCacheFullBlocks metering Eqs. 1-3) and,
  * when the cache is full, the reclamation of Alg. 2 (PrefixShield: Eqs. 5-9;
  * LRU, S3-FIFO and StaticQuota: the baselines of Sec. V-A) under the same

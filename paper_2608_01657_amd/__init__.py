@@ -28,6 +28,8 @@ PC_MAX_GROUPS, PC_MAX_CONTRACTS, PC_MAX_CAPACITY = 64, 4, 32767
 PC_LRU, PC_S3FIFO, PC_PREFIXSHIELD, PC_STATICQUOTA = 0, 1, 2, 3
 PC_FLAG_NO_SEGMENTATION, PC_FLAG_NO_DEBT_GATE = 1, 2
 PC_STATS_RECORD_BYTES = 64 * 136 + 64
+PC_LAYOUT_LDS, PC_LAYOUT_HYBRID, PC_LAYOUT_WS = 0, 1, 2
+LAYOUT_NAMES = {PC_LAYOUT_LDS: "lds", PC_LAYOUT_HYBRID: "hybrid", PC_LAYOUT_WS: "workspace"}
 
 GROUP_FIELDS = ["requests", "probes", "hits", "misses", "charged", "evicted_owned",
                 "evictions_caused", "promotions", "gated", "orphans", "dups", "truncated",
@@ -187,13 +189,13 @@ def pc_replay_workspace_bytes(traces: Sequence[pc_trace_desc], instances: Sequen
 
 
 def pc_replay_state_bytes(traces: Sequence[pc_trace_desc], instances: Sequence[pc_instance_desc]):
-    """Per-instance state bytes and whether each instance keeps it in LDS."""
+    """Per-instance state bytes and layout (PC_LAYOUT_LDS / _HYBRID / _WS)."""
     T, I = _descs(traces, instances)
     n = len(instances)
     b = (ctypes.c_int64 * max(n, 1))()
     f = (ctypes.c_int32 * max(n, 1))()
     _check(lib().pc_replay_state_bytes(T, len(traces), I, n, b, f))
-    return [int(b[i]) for i in range(n)], [bool(f[i]) for i in range(n)]
+    return [int(b[i]) for i in range(n)], [int(f[i]) for i in range(n)]
 
 
 def pc_replay_batch(traces, instances, workspace, stats, per_request=None, stream=None):

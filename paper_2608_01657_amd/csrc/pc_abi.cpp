@@ -41,29 +41,57 @@ int ceil_log2(int64_t v) {
 }
 int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
-// Usable dynamic LDS per workgroup on the current device (cached per device).
-int64_t lds_limit() {
+// LDS of one CU on the current device (cached per device): the most one
+// workgroup may allocate.  Without a device (host-only planning), that of
+// gfx950, the one target of this library: 160 KiB.
+constexpr int64_t kGfx950LdsPerCu = 160 * 1024;
+int64_t lds_per_cu() {
     static std::mutex mu;
     static int64_t cache[64] = {0};
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 65536 - pcr::replay_static_lds_bytes() - 256;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return kGfx950LdsPerCu;
     std::lock_guard<std::mutex> lk(mu);
     if (cache[dev] == 0) {
         int v = 0;
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
-            v = 65536;
+            v = (int)kGfx950LdsPerCu;
         cache[dev] = v;
     }
-    // the replay kernel's static exchange area shares the same LDS
-    return cache[dev] - pcr::replay_static_lds_bytes() - 256;
+    return cache[dev];
 }
+
+// Compute units of the current device (cached per device); without a
+// device, the 256 of an MI355X.
+int64_t cu_count() {
+    static std::mutex mu;
+    static int64_t cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    std::lock_guard<std::mutex> lk(mu);
+    if (cache[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+        cache[dev] = v;
+    }
+    return cache[dev];
+}
+
+// One kernel launch: instances of one layout whose LDS footprints allow the
+// same number of workgroups per CU, with the LDS of the largest of them.
+struct Launch {
+    int layout = pcr::kLayLds;
+    int per_cu = 0;
+    int32_t lds_bytes = 0;
+    int32_t first = 0, count = 0;    // range of Plan::order
+    double cost = 0;                 // of its costliest instance
+};
 
 struct Plan {
     std::vector<pcr::DevInst> di;
     std::vector<pcr::DevTrace> dt;
-    std::vector<int32_t> order;      // LDS launch first, then the workspace launch
-    int32_t n_lds = 0;
-    int32_t lds_bytes = 0;
+    std::vector<int32_t> order;      // instances, launch by launch, costliest first
+    std::vector<Launch> launches;    // costliest launch (and fewest per CU) first
+    int32_t lds_bytes = 0;           // largest dynamic LDS of any launch
     int64_t hdr_bytes = 0;
     int64_t ws_bytes = 0;
 };
@@ -72,7 +100,7 @@ constexpr int64_t kMaxRho = (int64_t)1 << 40;
 constexpr int64_t kMaxBeta = (int64_t)1 << 50;
 
 int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst,
-                          int32_t n_inst, int64_t lds_cap, Plan &P) {
+                          int32_t n_inst, int64_t lds_cu, int64_t n_cu, Plan &P) {
     if (n_traces < 0 || n_inst < 0) return fail(PC_EINVAL, "negative count");
     if ((n_traces > 0 && !traces) || (n_inst > 0 && !inst)) return fail(PC_EINVAL, "null descriptor array");
     P.dt.resize(n_traces);
@@ -109,8 +137,9 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
     off = align_up(off + (int64_t)sizeof(int32_t) * n_inst, 256);
     P.hdr_bytes = off;
     int64_t per_req = 0;
-    std::vector<int32_t> lds_ids, glb_ids;
     std::vector<double> cost(n_inst, 0.0);
+    std::vector<int> per_cu(n_inst, 0);
+    std::vector<pcr::StatePlan> plan_lds(n_inst), plan_hyb(n_inst), plan_ws(n_inst);
     for (int i = 0; i < n_inst; ++i) {
         const pc_instance_desc &s = inst[i];
         if (s.trace < 0 || s.trace >= n_traces) return fail(PC_EINVAL, "instance %d: trace index %d", i, s.trace);
@@ -164,72 +193,99 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
             d.move_thr == pcr::kFixMoveThr)
             maxn = pcr::kFixMaxn;
         d.maxn = (int32_t)maxn;
-        // main table: 8-entry buckets, load <= 2/3
-        d.nb_log2 = std::max(1, ceil_log2((int64_t)s.capacity * 3 / 16 + 1));
         d.log_log2 = ceil_log2(s.capacity + maxn + 128);
-        if (s.policy == PC_S3FIFO && d.g_cap > 0) {
+        const bool ghost = s.policy == PC_S3FIFO && d.g_cap > 0;
+        if (ghost) {
             d.gnb_log2 = std::max(1, ceil_log2((int64_t)d.g_cap * 3 / 16 + 1));
             // ghost ring: 4 g_cap + 256 positions (at most 2^16), see the ghost
             // sweep: any ring of at least 2 g_cap + 256 gives the same ghost; a
             // longer one (HBM) lets each scan batch sweep fewer table entries
             d.gr_log2 = std::min(16, ceil_log2(4 * (int64_t)d.g_cap + 256));
         }
-        // request duplicate set: 8-entry buckets, at most half full; between
-        // lookups it also holds the per-bucket claim counters of both tables
-        d.rs_log2 = std::max({6, ceil_log2(2 * maxn), d.nb_log2, d.gnb_log2});
         d.n_prefix_words = (int32_t)((t.n_prefix + 31) / 32);
-        // state region (identical layout in LDS or in the workspace)
-        int64_t so = 0;
-        auto take = [&](int64_t bytes) { int64_t o = so; so = align_up(so + bytes, 16); return (int32_t)o; };
-        const int64_t C = s.capacity;
-        const int64_t mx = std::max<int64_t>(maxn, 1);
-        d.o_key = take(8 * C);
-        d.o_stamp = take(4 * C);
-        d.o_meta = take(4 * C);
-        d.o_table = take(32LL << d.nb_log2);
-        d.o_log = take(2LL << d.log_log2);
-        d.o_rkeys = take(8 * mx);
-        d.o_rset = take(4LL << d.rs_log2);
-        d.o_posslot = take(2 * mx);
-        d.o_vlist = take(2 * mx);
-        d.o_rcnt = take(4LL << (d.rs_log2 - 3));
-        d.o_res = take(4LL * 64);
-        if (s.policy == PC_PREFIXSHIELD) d.o_pfx = take(4 * C);
-        if (s.policy == PC_PREFIXSHIELD || s.policy == PC_STATICQUOTA) {   // per-(group, segment) queues
-            d.o_cnt = take(4LL * 192);
-            d.o_cur = take(4LL * 196);
-        }
-        if (s.policy == PC_STATICQUOTA) d.o_fstack = take(2 * C);   // free-slot stack
-        if (s.policy == PC_S3FIFO && d.g_cap > 0) d.o_gtable = take(32LL << d.gnb_log2);
-        d.state_bytes = (int32_t)so;
-        d.in_lds = so <= lds_cap ? 1 : 0;
-        {   // the kernel's compile-time copy for the default 4096-block layout
-            const bool s3 = s.policy == PC_S3FIFO;
-            const pcr::FixOffsets f = pcr::fix_offsets(s.policy);
-            const bool offs = d.o_key == f.o_key && d.o_stamp == f.o_stamp && d.o_meta == f.o_meta &&
-                              d.o_table == f.o_table && d.o_log == f.o_log && d.o_rkeys == f.o_rkeys &&
-                              d.o_rset == f.o_rset && d.o_posslot == f.o_posslot && d.o_vlist == f.o_vlist &&
-                              d.o_rcnt == f.o_rcnt && d.o_res == f.o_res && d.o_pfx == f.o_pfx &&
-                              d.o_cnt == f.o_cnt && d.o_cur == f.o_cur && d.o_fstack == f.o_fstack &&
-                              d.o_gtable == f.o_gtable && d.state_bytes == f.end;
-            const bool fix = offs && d.in_lds && s.capacity == pcr::kFixC && d.s_cap == pcr::kFixScap &&
-                             s.n_contracts == 1 && s.eps_q16 == 0 && s.flags == 0 &&
-                             d.g_cap == pcr::kFixGcap && d.move_thr == pcr::kFixMoveThr &&
-                             d.nb_log2 == pcr::kFixNbLog2 && d.rs_log2 == pcr::kFixRsLog2 &&
-                             d.log_log2 == pcr::kFixLogLog2 && d.gnb_log2 == (s3 ? pcr::kFixGnbLog2S3 : 0) &&
-                             d.gr_log2 == (s3 ? pcr::kFixGrLog2S3 : 0);
-            d.fixc = fix ? pcr::kFixC : 0;
-        }
-        (d.in_lds ? lds_ids : glb_ids).push_back(i);
-        if (d.in_lds) P.lds_bytes = std::max(P.lds_bytes, d.state_bytes);
+        // the state in each layout (table size, offsets, instances per CU)
+        plan_lds[i] = pcr::plan_state(pcr::kLayLds, s.policy, s.capacity, maxn, d.log_log2, d.gnb_log2, ghost, lds_cu);
+        plan_hyb[i] = pcr::plan_state(pcr::kLayHybrid, s.policy, s.capacity, maxn, d.log_log2, d.gnb_log2, ghost,
+                                      lds_cu);
+        plan_ws[i] = pcr::plan_state(pcr::kLayWs, s.policy, s.capacity, maxn, d.log_log2, d.gnb_log2, ghost, lds_cu);
+        if (plan_ws[i].f.end > INT32_MAX) return fail(PC_EINVAL, "instance %d: state too large", i);
+        // first the layout that lets the most instances share a CU
+        // (all-LDS on a tie: its probes read no HBM)
+        const int nl = plan_lds[i].per_cu, nh = plan_hyb[i].per_cu;
+        d.layout = nl > 0 && nl >= nh ? pcr::kLayLds : nh > 0 ? pcr::kLayHybrid : pcr::kLayWs;
+        per_cu[i] = d.layout == pcr::kLayLds ? nl : d.layout == pcr::kLayHybrid ? nh : pcr::kMaxWgPerCu;
         cost[i] = (double)t.n_keys * (s.policy == PC_LRU ? 1.0 : 1.4) + (double)t.n_req * 16.0;
         d.per_req_off = per_req;
         per_req += 4 * t.n_req;
     }
+    // When the whole batch fits the CUs at once, instances whose densest
+    // layout is the hybrid one take the all-LDS layout instead (it reads no
+    // HBM per probe), costliest first, as long as the batch still fits:
+    // with free CUs a request's latency is what counts.
+    {
+        double demand = 0;
+        for (int i = 0; i < n_inst; ++i) demand += 1.0 / per_cu[i];
+        std::vector<int32_t> up;
+        for (int i = 0; i < n_inst; ++i)
+            if (P.di[i].layout != pcr::kLayLds && plan_lds[i].per_cu > 0) up.push_back(i);
+        std::stable_sort(up.begin(), up.end(), [&](int32_t a, int32_t b) { return cost[a] > cost[b]; });
+        for (int32_t i : up) {
+            const double extra = 1.0 / plan_lds[i].per_cu - 1.0 / per_cu[i];
+            if (demand + extra > (double)n_cu) break;
+            demand += extra;
+            P.di[i].layout = pcr::kLayLds;
+            per_cu[i] = plan_lds[i].per_cu;
+        }
+    }
+    // state offsets of the chosen layout; the kernel's compile-time copy
+    for (int i = 0; i < n_inst; ++i) {
+        const pc_instance_desc &s = inst[i];
+        pcr::DevInst &d = P.di[i];
+        const pcr::StatePlan &pl = d.layout == pcr::kLayLds ? plan_lds[i]
+                                   : d.layout == pcr::kLayHybrid ? plan_hyb[i] : plan_ws[i];
+        const pcr::StateOffsets &f = pl.f;
+        d.nb = pl.nb;
+        d.rs_log2 = pl.rs_log2;
+        d.o_key = f.o_key; d.o_stamp = f.o_stamp; d.o_meta = f.o_meta; d.o_table = f.o_table; d.o_log = f.o_log;
+        d.o_rkeys = f.o_rkeys; d.o_rset = f.o_rset; d.o_posslot = f.o_posslot; d.o_vlist = f.o_vlist;
+        d.o_rcnt = f.o_rcnt; d.o_res = f.o_res; d.o_pfx = f.o_pfx; d.o_cnt = f.o_cnt; d.o_cur = f.o_cur;
+        d.o_fstack = f.o_fstack; d.o_gtable = f.o_gtable;
+        d.state_bytes = (int32_t)f.end;
+        d.fixc = 0;
+        if (d.layout != pcr::kLayWs) {
+            const bool s3 = s.policy == PC_S3FIFO;
+            const pcr::StatePlan x = pcr::fix_plan(d.layout, s.policy);
+            const pcr::StateOffsets &g = x.f;
+            const bool offs = f.o_key == g.o_key && f.o_stamp == g.o_stamp && f.o_meta == g.o_meta &&
+                              f.o_table == g.o_table && f.o_log == g.o_log && f.o_rkeys == g.o_rkeys &&
+                              f.o_rset == g.o_rset && f.o_posslot == g.o_posslot && f.o_vlist == g.o_vlist &&
+                              f.o_rcnt == g.o_rcnt && f.o_res == g.o_res && f.o_pfx == g.o_pfx &&
+                              f.o_cnt == g.o_cnt && f.o_cur == g.o_cur && f.o_fstack == g.o_fstack &&
+                              f.o_gtable == g.o_gtable && f.end == g.end;
+            const bool fix = offs && s.capacity == pcr::kFixC && d.maxn == pcr::kFixMaxn &&
+                             d.s_cap == pcr::kFixScap && s.n_contracts == 1 && s.eps_q16 == 0 && s.flags == 0 &&
+                             d.g_cap == pcr::kFixGcap && d.move_thr == pcr::kFixMoveThr && d.nb == x.nb &&
+                             d.rs_log2 == x.rs_log2 && d.log_log2 == pcr::kFixLogLog2 &&
+                             d.gnb_log2 == (s3 ? pcr::kFixGnbLog2S3 : 0) && d.gr_log2 == (s3 ? pcr::kFixGrLog2S3 : 0);
+            d.fixc = fix ? pcr::kFixC : 0;
+        }
+    }
     // global regions per instance
     for (int i = 0; i < n_inst; ++i) {
         pcr::DevInst &d = P.di[i];
-        if (!d.in_lds) { d.ws_state = off; off = align_up(off + d.state_bytes, 256); }
+        if (d.layout == pcr::kLayWs) { d.ws_state = off; off = align_up(off + d.state_bytes, 256); }
+        if (d.layout == pcr::kLayHybrid) {
+            d.ws_key = off;
+            off = align_up(off + 8LL * d.capacity, 256);
+            if (d.policy == PC_PREFIXSHIELD) {
+                d.ws_pfx = off;
+                off = align_up(off + 4LL * d.capacity, 256);
+            }
+            if (d.policy == PC_S3FIFO && d.g_cap > 0) {
+                d.ws_gtable = off;
+                off = align_up(off + (32LL << d.gnb_log2), 256);
+            }
+        }
         d.ws_bits = off;
         off = align_up(off + 8LL * d.n_prefix_words, 256);
         if (d.policy == PC_S3FIFO && d.g_cap > 0) {
@@ -238,12 +294,40 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         }
     }
     P.ws_bytes = std::max<int64_t>(off, 256);
-    auto by_cost = [&](int32_t a, int32_t b) { return cost[a] > cost[b] || (cost[a] == cost[b] && a < b); };
-    std::sort(lds_ids.begin(), lds_ids.end(), by_cost);
-    std::sort(glb_ids.begin(), glb_ids.end(), by_cost);
-    P.order = lds_ids;
-    P.order.insert(P.order.end(), glb_ids.begin(), glb_ids.end());
-    P.n_lds = (int32_t)lds_ids.size();
+    // launches: one per (layout, instances per CU), each sized to its
+    // largest LDS state; instances inside a launch costliest first, and the
+    // launches that take whole CUs first, then by cost
+    std::vector<int32_t> ids(n_inst);
+    for (int i = 0; i < n_inst; ++i) ids[i] = i;
+    auto key_of = [&](int32_t i) { return std::make_pair(P.di[i].layout, per_cu[i]); };
+    std::sort(ids.begin(), ids.end(), [&](int32_t a, int32_t b) {
+        if (key_of(a) != key_of(b)) return key_of(a) < key_of(b);
+        return cost[a] > cost[b] || (cost[a] == cost[b] && a < b);
+    });
+    for (int32_t k = 0; k < n_inst;) {
+        Launch L;
+        L.layout = P.di[ids[k]].layout;
+        L.per_cu = per_cu[ids[k]];
+        L.first = k;
+        L.cost = cost[ids[k]];
+        while (k < n_inst && key_of(ids[k]) == key_of(ids[L.first])) {
+            if (L.layout != pcr::kLayWs) L.lds_bytes = std::max(L.lds_bytes, P.di[ids[k]].state_bytes);
+            ++k;
+        }
+        L.count = k - L.first;
+        P.lds_bytes = std::max(P.lds_bytes, L.lds_bytes);
+        P.launches.push_back(L);
+    }
+    std::stable_sort(P.launches.begin(), P.launches.end(), [](const Launch &a, const Launch &b) {
+        const int pa = a.layout == pcr::kLayWs ? 99 : a.per_cu, pb = b.layout == pcr::kLayWs ? 99 : b.per_cu;
+        return pa != pb ? pa < pb : a.cost > b.cost;
+    });
+    P.order.clear();
+    for (Launch &L : P.launches) {
+        const int32_t f = (int32_t)P.order.size();
+        P.order.insert(P.order.end(), ids.begin() + L.first, ids.begin() + L.first + L.count);
+        L.first = f;
+    }
     return PC_OK;
 }
 
@@ -293,21 +377,25 @@ int32_t pc_hash_blocks(const int32_t *d_tokens, int64_t n_tokens, const int64_t 
 int64_t pc_replay_workspace_bytes(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst,
                                   int32_t n_inst) {
     Plan P;
-    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_limit(), P);
+    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_per_cu(), cu_count(), P);
     if (rc != PC_OK) return rc;
     ok();
     return P.ws_bytes;
 }
 
 int32_t pc_replay_state_bytes(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst,
-                              int32_t n_inst, int64_t *bytes_out, int32_t *in_lds_out) {
-    if (n_inst > 0 && (!bytes_out || !in_lds_out)) return fail(PC_EINVAL, "null output");
+                              int32_t n_inst, int64_t *bytes_out, int32_t *layout_out) {
+    if (n_inst > 0 && (!bytes_out || !layout_out)) return fail(PC_EINVAL, "null output");
     Plan P;
-    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_limit(), P);
+    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_per_cu(), cu_count(), P);
     if (rc != PC_OK) return rc;
     for (int i = 0; i < n_inst; ++i) {
         bytes_out[i] = P.di[i].state_bytes;
-        in_lds_out[i] = P.di[i].in_lds;
+        const pcr::DevInst &d = P.di[i];
+        if (d.layout == pcr::kLayHybrid)   // keys, prefix ids, ghost table in the workspace
+            bytes_out[i] += 8LL * d.capacity + (d.policy == PC_PREFIXSHIELD ? 4LL * d.capacity : 0) +
+                            (d.policy == PC_S3FIFO && d.g_cap > 0 ? (32LL << d.gnb_log2) : 0);
+        layout_out[i] = d.layout;
     }
     return ok();
 }
@@ -327,24 +415,83 @@ void fill_header(const Plan &P, int32_t n_traces, int32_t n_inst, uint8_t *h) {
     std::memcpy(h + o_ord, P.order.data(), sizeof(int32_t) * n_inst);
 }
 
+// Library streams (default priority) that the launches of one batch fork
+// onto, so that launches of different footprints run side by side; joined
+// back into the caller's stream with events.  One set per device.
+constexpr int kForkStreams = 4;
+struct ForkStreams {
+    std::mutex mu;
+    bool ready[64] = {};
+    hipStream_t s[64][kForkStreams] = {};
+    hipEvent_t fork[64] = {}, join[64][kForkStreams] = {};
+};
+ForkStreams g_fork;
+
+int32_t fork_streams(int dev) {
+    if (g_fork.ready[dev]) return PC_OK;
+    hipError_t e;
+    for (int k = 0; k < kForkStreams; ++k) {
+        e = hipStreamCreateWithFlags(&g_fork.s[dev][k], hipStreamNonBlocking);
+        if (e != hipSuccess) return hip_fail(e, "library stream");
+        e = hipEventCreateWithFlags(&g_fork.join[dev][k], hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(e, "library event");
+    }
+    e = hipEventCreateWithFlags(&g_fork.fork[dev], hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "library event");
+    g_fork.ready[dev] = true;
+    return PC_OK;
+}
+
 // Launches of a planned batch whose header is already queued for upload to
-// the start of `ws`.
+// the start of `ws` on stream s.  With `fork`, launches go round-robin onto
+// the library streams (after s reaches this point) and s waits for all of
+// them; else they run one after another on s.
 int32_t launch_planned(const Plan &P, int32_t n_traces, int32_t n_inst, uint8_t *ws, void *d_stats,
-                       int32_t *d_per_request, hipStream_t s) {
+                       int32_t *d_per_request, hipStream_t s, bool fork) {
     const size_t o_tr = align_up((int64_t)sizeof(pcr::DevInst) * n_inst, 256);
     const size_t o_ord = align_up((int64_t)o_tr + (int64_t)sizeof(pcr::DevTrace) * n_traces, 256);
     const pcr::DevInst *d_inst = (const pcr::DevInst *)ws;
     const pcr::DevTrace *d_tr = (const pcr::DevTrace *)(ws + o_tr);
     const int32_t *d_ord = (const int32_t *)(ws + o_ord);
     hipError_t e;
-    if (P.n_lds > 0) {
-        e = pcr::launch_replay(d_inst, d_tr, d_ord, P.n_lds, P.lds_bytes, true, ws, (int64_t *)d_stats, d_per_request, s);
-        if (e != hipSuccess) return hip_fail(e, "replay launch (LDS)");
+    if (P.lds_bytes > 0) {
+        e = pcr::replay_set_lds_limit(P.lds_bytes);
+        if (e != hipSuccess) return hip_fail(e, "replay LDS limit");
     }
-    if (n_inst - P.n_lds > 0) {
-        e = pcr::launch_replay(d_inst, d_tr, d_ord + P.n_lds, n_inst - P.n_lds, 0, false, ws, (int64_t *)d_stats,
-                               d_per_request, s);
-        if (e != hipSuccess) return hip_fail(e, "replay launch (workspace)");
+    const int nl = (int)P.launches.size();
+    if (!fork || nl < 2) {
+        for (const Launch &L : P.launches) {
+            e = pcr::launch_replay(d_inst, d_tr, d_ord + L.first, L.count, L.lds_bytes, L.layout, ws,
+                                   (int64_t *)d_stats, d_per_request, s);
+            if (e != hipSuccess) return hip_fail(e, "replay launch");
+        }
+        return ok();
+    }
+    int dev = 0;
+    e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "current device");
+    if (dev < 0 || dev >= 64) return fail(PC_EUNSUPPORTED, "device %d (at most 64 devices)", dev);
+    std::lock_guard<std::mutex> lk(g_fork.mu);
+    int32_t rc = fork_streams(dev);
+    if (rc != PC_OK) return rc;
+    e = hipEventRecord(g_fork.fork[dev], s);
+    if (e != hipSuccess) return hip_fail(e, "fork event");
+    const int used = std::min(nl, kForkStreams);
+    for (int k = 0; k < used; ++k) {
+        e = hipStreamWaitEvent(g_fork.s[dev][k], g_fork.fork[dev], 0);
+        if (e != hipSuccess) return hip_fail(e, "fork wait");
+    }
+    for (int l = 0; l < nl; ++l) {
+        const Launch &L = P.launches[l];
+        e = pcr::launch_replay(d_inst, d_tr, d_ord + L.first, L.count, L.lds_bytes, L.layout, ws, (int64_t *)d_stats,
+                               d_per_request, g_fork.s[dev][l % kForkStreams]);
+        if (e != hipSuccess) return hip_fail(e, "replay launch");
+    }
+    for (int k = 0; k < used; ++k) {
+        e = hipEventRecord(g_fork.join[dev][k], g_fork.s[dev][k]);
+        if (e != hipSuccess) return hip_fail(e, "join event");
+        e = hipStreamWaitEvent(s, g_fork.join[dev][k], 0);
+        if (e != hipSuccess) return hip_fail(e, "join wait");
     }
     return ok();
 }
@@ -373,7 +520,7 @@ int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces, const pc_
                         void *d_workspace, int64_t workspace_bytes, void *d_stats, int32_t *d_per_request,
                         void *stream) {
     Plan P;
-    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_limit(), P);
+    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_per_cu(), cu_count(), P);
     if (rc != PC_OK) return rc;
     if (n_inst == 0) return ok();
     if (!d_workspace || !d_stats) return fail(PC_EINVAL, "null workspace or stats");
@@ -410,13 +557,13 @@ int32_t pc_replay_batch(const pc_trace_desc *traces, int32_t n_traces, const pc_
         if (e != hipSuccess) return hip_fail(e, "event record");
         g_stage.pending = true;
     }
-    return launch_planned(P, n_traces, n_inst, ws, d_stats, d_per_request, s);
+    return launch_planned(P, n_traces, n_inst, ws, d_stats, d_per_request, s, true);
 }
 
 int32_t pc_replay_batch_static(const pc_trace_desc *traces, int32_t n_traces, const pc_instance_desc *inst,
                                int32_t n_inst, void *d_stats, int32_t *d_per_request, void *stream) {
     Plan P;
-    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_limit(), P);
+    int32_t rc = validate_and_plan(traces, n_traces, inst, n_inst, lds_per_cu(), cu_count(), P);
     if (rc != PC_OK) return rc;
     if (n_inst == 0) return ok();
     if (!d_stats) return fail(PC_EINVAL, "null stats");
@@ -442,7 +589,7 @@ int32_t pc_replay_batch_static(const pc_trace_desc *traces, int32_t n_traces, co
     fill_header(P, n_traces, n_inst, g_static.host.data());
     e = hipMemcpyAsync(ws, g_static.host.data(), nbytes, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "descriptor upload");
-    return launch_planned(P, n_traces, n_inst, ws, d_stats, d_per_request, s);
+    return launch_planned(P, n_traces, n_inst, ws, d_stats, d_per_request, s, false);
 }
 
 int32_t pc_get_stats(const void *d_stats, int32_t n_inst, int32_t instance, pc_group_stats *groups_out,

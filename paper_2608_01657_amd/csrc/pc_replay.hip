@@ -26,16 +26,20 @@
 // one barrier), which gives every thread block-wide counts and ranks.
 //
 // State of one instance (capacity C, largest request n_max):
-//   key[C] u64, stamp[C] u32, meta[C] u32     -- one slot per cached block
+//   key[C] u64, stamp[C], meta[C] u32      -- one slot per cached block
 //   table[8*NB] u32  2-choice bucketized hash, entry = tag16 | slot16
 //   log[R] u16       free-queue log: the slot of each appended entry; an
 //                    entry at absolute position q is live iff its slot has
-//                    the in-log bit and stamp == q
+//                    the in-log bit and stamp == q (stamps are 16-bit when
+//                    the state is in LDS: R <= 2^16, and every position a
+//                    scan compares lies in the live window of R)
 //   rkeys, rset, posslot, vlist   per-request keys, duplicate set,
 //                    position -> slot, victims' slots
 //   pfx[C] (PrefixShield), ghost table (S3-FIFO), per-group counters
-// All of it sits in dynamic LDS when it fits (C up to 4096 blocks), else in
-// the workspace; the code is the same, instantiated twice.  The ghost ring
+// Three layouts, the same code instantiated for each: everything in
+// dynamic LDS; the hybrid one, with the block keys, prefix ids and request
+// keys in the workspace (HBM) and the rest in LDS, so that two 4096-block
+// instances share a CU; or everything in the workspace.  The ghost ring
 // (keys of S3-FIFO's ghost entries) and the prefix bitmaps stay in HBM.
 //
 // Victims of one request are chosen in bulk: LRU takes the first e live log
@@ -46,6 +50,7 @@
 // where the one-at-a-time rule would switch queues.  Each shortcut
 // reproduces the one-victim-at-a-time definition exactly.
 #include <cstddef>
+#include <type_traits>
 
 #include "pc_internal.h"
 
@@ -266,14 +271,17 @@ struct Coll {
 };
 static_assert(offsetof(Coll, qf) == offsetof(Coll, novf) + 4 && offsetof(Coll, novf) % 8 == 0,
               "novf and qf are read together as one 64-bit word");
+static_assert(sizeof(Coll) <= kStaticLdsReserve, "the host plans LDS with this much static LDS per workgroup");
 
-// Key -> two table buckets, 16-bit tag (never 0xFFFF, so empty entries never
-// match a tag), two duplicate-set buckets.  Keys are usually hash outputs
-// already, but the ABI accepts any uint64, so mix with 32-bit ops.
+// Key -> two table buckets out of nb (even, any size: the bucket is the
+// high word of a 32x32-bit product), a 16-bit tag from the other half of
+// the first mix (never 0xFFFF, so empty entries never match a tag), two
+// duplicate-set buckets.  Keys are usually hash outputs already, but the
+// ABI accepts any uint64, so mix with 32-bit ops.
 struct TH {
     uint32_t b1, b2, tag, r1, r2;
 };
-DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rbmask) {
+DEV TH thash(uint64_t k, uint32_t nb, uint32_t rbmask) {
     const uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
     uint32_t x = lo * 0x85EBCA6Bu ^ hi;
     x ^= x >> 15;
@@ -284,13 +292,13 @@ DEV TH thash(uint64_t k, uint32_t nbmask, uint32_t rbmask) {
     y *= 0x9E3779B1u;
     y ^= x >> 7;
     TH h;
-    h.b1 = x & nbmask;
-    h.b2 = y & nbmask;
+    h.b1 = __umulhi(x, nb);
+    h.b2 = __umulhi(y, nb);
     if (h.b2 == h.b1) h.b2 = h.b1 ^ 1u;
-    const uint32_t t = y >> 16;
+    const uint32_t t = x & 0xFFFFu;
     h.tag = t == 0xFFFFu ? 0xFFFEu : t;
-    h.r1 = (x >> 11) & rbmask;
-    h.r2 = (y >> 3) & rbmask;
+    h.r1 = y & rbmask;
+    h.r2 = (y >> 13) & rbmask;
     if (h.r2 == h.r1) h.r2 = h.r1 ^ 1u;
     return h;
 }
@@ -336,12 +344,13 @@ struct Req {
 
 // Parameters derived from an instance's capacity and S3-FIFO settings.
 // kFix = 0: read from its descriptor.  kFix = kFixC: the default 4096-block
-// layout, by the same formulas from constants, so that they fold into the
-// instructions instead of holding scalar registers.
-template <int kPol, int kFix>
+// layout in layout kLay, by the host's own planning function evaluated at
+// compile time, so that they fold into the instructions instead of holding
+// scalar registers.
+template <int kLay, int kPol, int kFix>
 struct Params {
     int C;
-    uint32_t nbmask, rsmask, rbmask, lmask, R, gnbmask, grmask;
+    uint32_t nb, rsmask, rbmask, lmask, R, gnb, gnbmask, grmask;
     int32_t s_cap, g_cap, move_thr;
     uint32_t gne, gspan;      // ghost table entries; sweep span (ring - g_cap - 256)
     uint64_t gsrate;          // ceil(gne * 2^16 / gspan): entries swept per insertion, Q16
@@ -353,12 +362,13 @@ struct Params {
         nseg = (kPol == kPS && !(flags & kFlagNoSeg)) ? 3 : 1;
         eps = I.eps;
         C = I.capacity;
-        nbmask = (1u << I.nb_log2) - 1u;
+        nb = (uint32_t)I.nb;
         rsmask = (1u << I.rs_log2) - 1u;
         rbmask = rsmask >> 3;
         R = 1u << I.log_log2;
         lmask = R - 1u;
-        gnbmask = (1u << I.gnb_log2) - 1u;
+        gnb = 1u << I.gnb_log2;
+        gnbmask = gnb - 1u;
         grmask = (1u << I.gr_log2) - 1u;
         gne = 8u << I.gnb_log2;
         gspan = (grmask + 1u) - (uint32_t)I.g_cap - (uint32_t)kB;
@@ -368,13 +378,14 @@ struct Params {
         move_thr = I.move_thr;
     }
 };
-template <int kPol>
-struct Params<kPol, kFixC> {
+template <int kLay, int kPol>
+struct Params<kLay, kPol, kFixC> {
     static constexpr int32_t kGnb = kPol == kS3 ? kFixGnbLog2S3 : 0, kGr = kPol == kS3 ? kFixGrLog2S3 : 0;
+    static constexpr StatePlan kPlan = fix_plan(kLay, kPol);
     static constexpr int C = kFixC;
-    static constexpr uint32_t nbmask = (1u << kFixNbLog2) - 1u, rsmask = (1u << kFixRsLog2) - 1u;
+    static constexpr uint32_t nb = (uint32_t)kPlan.nb, rsmask = (1u << kPlan.rs_log2) - 1u;
     static constexpr uint32_t rbmask = rsmask >> 3, R = 1u << kFixLogLog2, lmask = R - 1u;
-    static constexpr uint32_t gnbmask = (1u << kGnb) - 1u, grmask = (1u << kGr) - 1u;
+    static constexpr uint32_t gnb = 1u << kGnb, gnbmask = gnb - 1u, grmask = (1u << kGr) - 1u;
     static constexpr int32_t s_cap = kFixScap, g_cap = kFixGcap, move_thr = kFixMoveThr;
     static constexpr uint32_t gne = 8u << kGnb, gspan = (grmask + 1u) - (uint32_t)g_cap - (uint32_t)kB;
     static constexpr uint64_t gsrate = g_cap > 0 ? (((uint64_t)gne << 16) + gspan - 1) / gspan : 0;
@@ -386,15 +397,25 @@ struct Params<kPol, kFixC> {
 
 // kPol is the instance's policy: each policy gets its own specialized copy
 // of the request loop (no runtime policy tests, fewer live registers).
-template <bool kLds, int kPol, int kFix = 0>
-struct Replayer : Params<kPol, kFix> {
-    using Pm = Params<kPol, kFix>;
+// kLay is where the state lives (kLayLds, kLayHybrid, kLayWs).
+template <int kLay, int kPol, int kFix = 0>
+struct Replayer : Params<kLay, kPol, kFix> {
+    using Pm = Params<kLay, kPol, kFix>;
+    // barriers fence LDS only while the state (all but the hybrid layout's
+    // keys and prefix ids) is in LDS
+    static constexpr bool kLds = kLay != kLayWs;
+    static constexpr bool kHyb = kLay == kLayHybrid;
+    using KeyPtr = typename std::conditional<kHyb, GLOBAL uint64_t *, uint64_t *>::type;
+    using PfxPtr = typename std::conditional<kHyb, GLOBAL uint32_t *, uint32_t *>::type;
+    using GtPtr = PfxPtr;     // the S3-FIFO ghost table
+    using StampT = typename std::conditional<kLay == kLayWs, uint32_t, uint16_t>::type;
     using Pm::C;
-    using Pm::nbmask;
+    using Pm::nb;
     using Pm::rsmask;
     using Pm::rbmask;
     using Pm::lmask;
     using Pm::R;
+    using Pm::gnb;
     using Pm::gnbmask;
     using Pm::grmask;
     using Pm::s_cap;
@@ -420,8 +441,12 @@ struct Replayer : Params<kPol, kFix> {
     int room;                 // most blocks one request may hold: C, or the StaticQuota partition
     int64_t rho[4], beta[4], invw[4];   // kept in VGPRs
     // ---------------- arrays
-    uint64_t *key, *rkeys;
-    uint32_t *stamp, *meta, *table, *rset, *rcnt, *cnt, *cur, *res, *pfx, *gtable;
+    KeyPtr key;
+    PfxPtr pfx;
+    uint64_t *rkeys;          // (not in the hybrid layout: the trace's keys are read instead)
+    StampT *stamp;
+    uint32_t *meta, *table, *rset, *rcnt, *cnt, *cur, *res;
+    GtPtr gtable;
     uint16_t *log, *posslot, *vlist, *fstack;
     GLOBAL uint32_t *bits;
     GLOBAL uint64_t *gring;
@@ -471,18 +496,25 @@ struct Replayer : Params<kPol, kFix> {
         // the default-layout copy takes its array offsets as constants (the
         // host marks an instance for it only when they equal its own)
         constexpr bool fx = kFix == kFixC;
-        constexpr FixOffsets F = fix_offsets(kPol);
-        key = reinterpret_cast<uint64_t *>(sbase + (fx ? F.o_key : I.o_key));
-        rkeys = reinterpret_cast<uint64_t *>(sbase + (fx ? F.o_rkeys : I.o_rkeys));
-        stamp = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_stamp : I.o_stamp));
+        constexpr StateOffsets F = fix_plan(kLay, kPol).f;
+        if constexpr (kHyb) {
+            key = gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_key));
+            pfx = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_pfx));
+            gtable = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_gtable));
+            rkeys = nullptr;
+        } else {
+            key = reinterpret_cast<uint64_t *>(sbase + (fx ? F.o_key : I.o_key));
+            pfx = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_pfx : I.o_pfx));
+            gtable = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_gtable : I.o_gtable));
+            rkeys = reinterpret_cast<uint64_t *>(sbase + (fx ? F.o_rkeys : I.o_rkeys));
+        }
+        stamp = reinterpret_cast<StampT *>(sbase + (fx ? F.o_stamp : I.o_stamp));
         meta = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_meta : I.o_meta));
         table = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_table : I.o_table));
         rset = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_rset : I.o_rset));
         cnt = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_cnt : I.o_cnt));
         cur = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_cur : I.o_cur));
         res = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_res : I.o_res));
-        pfx = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_pfx : I.o_pfx));
-        gtable = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_gtable : I.o_gtable));
         log = reinterpret_cast<uint16_t *>(sbase + (fx ? F.o_log : I.o_log));
         posslot = reinterpret_cast<uint16_t *>(sbase + (fx ? F.o_posslot : I.o_posslot));
         vlist = reinterpret_cast<uint16_t *>(sbase + (fx ? F.o_vlist : I.o_vlist));
@@ -587,11 +619,19 @@ struct Replayer : Params<kPol, kFix> {
     }
 
     // ============================================================ tables
-    DEV void load_buckets(const uint32_t *tb, const TH &h, uint32_t e[16]) const {
-        const uint4 *t4 = reinterpret_cast<const uint4 *>(tb);
-        const uint4 a0 = t4[2 * h.b1], a1 = t4[2 * h.b1 + 1], c0 = t4[2 * h.b2], c1 = t4[2 * h.b2 + 1];
+    // both buckets of h (two 16-byte loads each), from LDS or global memory
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    template <typename P4>
+    DEV static void unpack_buckets(P4 t4, const TH &h, uint32_t e[16]) {
+        const u32x4 a0 = t4[2 * h.b1], a1 = t4[2 * h.b1 + 1], c0 = t4[2 * h.b2], c1 = t4[2 * h.b2 + 1];
         e[0] = a0.x; e[1] = a0.y; e[2] = a0.z; e[3] = a0.w; e[4] = a1.x; e[5] = a1.y; e[6] = a1.z; e[7] = a1.w;
         e[8] = c0.x; e[9] = c0.y; e[10] = c0.z; e[11] = c0.w; e[12] = c1.x; e[13] = c1.y; e[14] = c1.z; e[15] = c1.w;
+    }
+    DEV void load_buckets(const uint32_t *tb, const TH &h, uint32_t e[16]) const {
+        unpack_buckets(reinterpret_cast<const u32x4 *>(tb), h, e);
+    }
+    DEV void load_buckets(const GLOBAL uint32_t *tb, const TH &h, uint32_t e[16]) const {
+        unpack_buckets(reinterpret_cast<const GLOBAL u32x4 *>(tb), h, e);
     }
     DEV uint32_t epos(const TH &h, int i) const { return i < 8 ? 8 * h.b1 + i : 8 * h.b2 + (i - 8); }
     // Probe both buckets of k.  Returns the number of tag matches; `cand` is
@@ -649,11 +689,13 @@ struct Replayer : Params<kPol, kFix> {
     // the counters used, which tclaim_reset puts back to kEmpty after the
     // next barrier.  Returns the entry's index, or kEmpty when both buckets
     // are full.
-    DEV uint32_t tclaim(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, const uint32_t (&e)[16],
+    template <typename TP>
+    DEV uint32_t tclaim(TP tb, uint32_t *ctr, uint32_t val, const TH &h, const uint32_t (&e)[16],
                         uint32_t &touched, bool ghost = false, uint32_t gref = 0) {
         return tclaim_m(tb, ctr, val, h, free_mask(e, ghost, gref), touched);
     }
-    DEV uint32_t tclaim_m(uint32_t *tb, uint32_t *ctr, uint32_t val, const TH &h, uint32_t fm, uint32_t &touched) {
+    template <typename TP>
+    DEV uint32_t tclaim_m(TP tb, uint32_t *ctr, uint32_t val, const TH &h, uint32_t fm, uint32_t &touched) {
         const uint32_t m1 = fm & 0xFFu, m2 = fm >> 8;
         const bool sec = __builtin_popcount(m2) > __builtin_popcount(m1);
         touched = 0;
@@ -687,13 +729,14 @@ struct Replayer : Params<kPol, kFix> {
     DEV void set_tpos(uint32_t s, uint32_t p) { meta[s] = (meta[s] & kLowMeta) | (p << kTposShift); }
     // Serial cuckoo displacement, one thread.  gref: ghost sequence that
     // decides which ghost entries are still live.
-    DEV bool kick(uint32_t *tb, bool main, uint32_t val, uint64_t k, uint32_t gref) {
-        const uint32_t msk = main ? nbmask : gnbmask;
+    template <typename TP>
+    DEV bool kick(TP tb, bool main, uint32_t val, uint64_t k, uint32_t gref) {
+        const uint32_t nbk = main ? nb : gnb;
         uint32_t cv = val;
         uint64_t ck = k;
         uint32_t from = 0xFFFFFFFFu;
         for (int it = 0; it < 512; ++it) {
-            const TH h = thash(ck, msk, rbmask);
+            const TH h = thash(ck, nbk, rbmask);
             for (int i = 0; i < 16; ++i) {
                 const uint32_t p = epos(h, i);
                 if (main ? tb[p] == kEmpty : !glive(tb[p], gref)) {
@@ -718,10 +761,15 @@ struct Replayer : Params<kPol, kFix> {
     DEV void kick_pending(uint32_t gref = 0) {
         const uint32_t nk = rfl(X.novf);
         if (nk == 0) return;
+        // the walk reads the keys of table entries, which this request may
+        // just have written (hybrid layout: in global memory)
+        if constexpr (kHyb) gsync();
         if (tid == 0) {
             for (uint32_t i = 0; i < nk; ++i) {
                 const bool main = X.kmain[i] != 0;
-                if (!kick(main ? table : gtable, main, X.kval[i], X.kkey[i], gref)) X.kerr = kErrInternal;
+                const bool placed = main ? kick(table, true, X.kval[i], X.kkey[i], gref)
+                                         : kick(gtable, false, X.kval[i], X.kkey[i], gref);
+                if (!placed) X.kerr = kErrInternal;
             }
             X.novf = 0;
         }
@@ -797,13 +845,14 @@ struct Replayer : Params<kPol, kFix> {
             const uint32_t pos = p0 + tid;
             const bool valid = pos < tail;
             const uint32_t s = slot_at(pos, valid);
-            const uint32_t mt = meta[s], st = stamp[s];
-            const bool live = valid && (mt & kInLog) && st == pos;
+            const uint32_t mt = meta[s];
+            const StampT st = stamp[s];
+            const bool live = valid && (mt & kInLog) && st == (StampT)pos;
             const BMask lm = bballot1(live);   // every read of this step is done
             if (live) {
                 const uint32_t np = nw + (uint32_t)lm.rank(wid);
                 log[np & lmask] = (uint16_t)s;
-                stamp[s] = np;
+                stamp[s] = (StampT)np;
             }
             nw += (uint32_t)lm.count();
             bsync();
@@ -836,8 +885,9 @@ struct Replayer : Params<kPol, kFix> {
             const uint32_t pos = head + tid;
             const bool valid = pos < tail;
             const uint32_t s = slot_at(pos, valid);
-            const uint32_t mt = meta[s], st = stamp[s];
-            const bool live = valid && (mt & kInLog) && st == pos;
+            const uint32_t mt = meta[s];
+            const StampT st = stamp[s];
+            const bool live = valid && (mt & kInLog) && st == (StampT)pos;
             const uint32_t loc = victim_entry(live, mt);
             const BMask lm = bballot1(live);
             const int rk = lm.rank(wid);
@@ -867,8 +917,9 @@ struct Replayer : Params<kPol, kFix> {
             const uint32_t pos = c + tid;
             const bool valid = pos < tail;
             const uint32_t sl = slot_at(pos, valid);
-            const uint32_t mt = meta[sl], st = stamp[sl];
-            const bool live = valid && (mt & kInLog) && st == pos;
+            const uint32_t mt = meta[sl];
+            const StampT st = stamp[sl];
+            const bool live = valid && (mt & kInLog) && st == (StampT)pos;
             const bool match = live && (x < 0 || (int)owner_of(mt) == x) && (s < 0 || (int)cls_of(mt) == s);
             const uint32_t loc = victim_entry(match, mt);
             const BMask mm = bballot1(match);
@@ -900,8 +951,9 @@ struct Replayer : Params<kPol, kFix> {
             const uint32_t pos = c + tid;
             const bool valid = pos < tail;
             const uint32_t sl = slot_at(pos, valid);
-            const uint32_t mt = meta[sl], st = stamp[sl];
-            const bool live = valid && (mt & kInLog) && st == pos;
+            const uint32_t mt = meta[sl];
+            const StampT st = stamp[sl];
+            const bool live = valid && (mt & kInLog) && st == (StampT)pos;
             const bool match = live && (int)owner_of(mt) == x && (s < 0 || (int)cls_of(mt) == s);
             const BMask mm = bballot1(match);
             if (mm.any()) { found = c + (uint32_t)mm.first(); c = found; break; }
@@ -1006,7 +1058,7 @@ struct Replayer : Params<kPol, kFix> {
     // this request's own reclamation hold its victims' keys, never the key
     // of one of its new blocks, and are skipped without reading the ring.
     DEV bool ghost_take(uint64_t k) {
-        const TH h = thash(k, gnbmask, rbmask);
+        const TH h = thash(k, gnb, rbmask);
         uint32_t e[16];
         load_buckets(gtable, h, e);
         // entries with the key's tag first (branch-free): a match is rare,
@@ -1113,9 +1165,10 @@ struct Replayer : Params<kPol, kFix> {
             // a small-queue victim is remembered by the ghost: its key is
             // read with the metadata and stamp, in the same round trip
             const bool gho = useS && g_cap > 0;
-            const uint32_t mt = meta[sl], st = stamp[sl];
+            const uint32_t mt = meta[sl];
+            const StampT st = stamp[sl];
             const uint64_t kv = gho ? key[sl] : 0ull;
-            const bool live = valid && (mt & kInLog) && st == pos;
+            const bool live = valid && (mt & kInLog) && st == (StampT)pos;
             const bool inQ = live && (useS ? !(mt & kQMain) : (mt & kQMain) != 0);
             const bool cand = inQ && !(mt & kPin);
             const uint32_t f = freq_of(mt);
@@ -1129,7 +1182,7 @@ struct Replayer : Params<kPol, kFix> {
             uint32_t gfree = 0;
             if (gho) {
                 if (maybe_ev) {
-                    hg = thash(vk, gnbmask, rbmask);
+                    hg = thash(vk, gnb, rbmask);
                     uint32_t eg[16];
                     load_buckets(gtable, hg, eg);
                     gfree = free_mask(eg, true, gseq);
@@ -1169,7 +1222,7 @@ struct Replayer : Params<kPol, kFix> {
             if (proc && mv) {
                 const uint32_t np = tail + (uint32_t)pmm.rank(wid);
                 log[np & lmask] = (uint16_t)sl;
-                stamp[sl] = np;
+                stamp[sl] = (StampT)np;
                 uint32_t m2 = mt & ~(3u << kFreqShift);
                 if (useS) m2 |= kQMain;
                 else m2 |= (f - 1) << kFreqShift;
@@ -1207,7 +1260,10 @@ struct Replayer : Params<kPol, kFix> {
             const uint32_t adv = stop < kB ? (uint32_t)stop : ((lim - sp) < (uint32_t)kB ? (lim - sp) : (uint32_t)kB);
             if (adv == 0) err = kErrInternal;   // a scan that cannot advance is a bug, never a hang
             if (useS) spS = sp + adv; else spM = sp + adv;
-            bsync();
+            // the next batch's bucket snapshot must see this batch's ghost
+            // claims (hybrid layout: the ghost table is in global memory)
+            if constexpr (kHyb && kPol == kS3) gsync();
+            else bsync();
             if (useS) {
                 if (gho && nev > 0) {
                     tclaim_reset(rset, hg, gtouched);
@@ -1262,6 +1318,12 @@ struct Replayer : Params<kPol, kFix> {
         int32_t *o = preq + 4 * i;
         o[0] = last_h; o[1] = last_m; o[2] = last_e; o[3] = last_o;
         pr_next = i + 1;
+    }
+    // key at position j of the request whose keys start at ko: the copy in
+    // LDS, or in the hybrid layout the trace's own (read-only) keys
+    DEV uint64_t rkey(int64_t ko, uint32_t j) const {
+        if constexpr (kHyb) return tkeys[ko + j];
+        else return rkeys[j];
     }
     DEV Req load_req(int64_t r) const {
         Req q;
@@ -1325,7 +1387,7 @@ struct Replayer : Params<kPol, kFix> {
             const bool act = j < n;
             const uint64_t k = kcur;
             if (base + kB < n) kcur = (j + kB < n) ? tkeys[ko + j + kB] : 0ull;   // next step in flight
-            const TH h = thash(k, nbmask, rbmask);
+            const TH h = thash(k, nb, rbmask);
             // the table buckets load first: their latency overlaps the
             // duplicate-set claim below
             uint32_t te[16];
@@ -1334,7 +1396,7 @@ struct Replayer : Params<kPol, kFix> {
             // bucket with room along r1, r2, r2+1, ... (a claim counter each)
             uint32_t rpos = 0, nhop = 0;
             if (act) {
-                rkeys[j] = k;
+                if constexpr (!kHyb) rkeys[j] = k;
                 uint32_t b = h.r1;
                 for (;;) {
                     const uint32_t r = atomicAdd(&rcnt[b], 1u);
@@ -1378,7 +1440,7 @@ struct Replayer : Params<kPol, kFix> {
                     if (tm != 0u) {
 #pragma unroll
                         for (int i = 0; i < 8; ++i)
-                            if ((tm >> i) & 1u) dup = dup || rkeys[ev[i] & 0xFFFFu] == k;
+                            if ((tm >> i) & 1u) dup = dup || rkey(ko, ev[i] & 0xFFFFu) == k;
                     }
                     if (dup || cn <= 8u) break;
                     b = hop == 0 ? h.r2 : ((b + 1u) & rbmask);
@@ -1618,7 +1680,7 @@ struct Replayer : Params<kPol, kFix> {
                 if (c_new) {
                     const uint32_t np = tail + (uint32_t)(m - 1 - c_rkNew);
                     log[np & lmask] = (uint16_t)slot;
-                    stamp[slot] = np;
+                    stamp[slot] = (StampT)np;
                     meta[slot] = mt | kInLog | (gh ? kQMain : 0u);
                 } else if (c_rl) {
                     meta[slot] = mt & ~kPin;
@@ -1628,7 +1690,7 @@ struct Replayer : Params<kPol, kFix> {
             } else if (c_rl) {
                 const uint32_t np = tail + (uint32_t)(nrel - 1 - c_rkRl);
                 log[np & lmask] = (uint16_t)slot;
-                stamp[slot] = np;
+                stamp[slot] = (StampT)np;
                 meta[slot] = (mt & ~kPin) | kInLog | kRes;
             }
             if constexpr (kQueues) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), c_rl, 1);
@@ -1646,8 +1708,8 @@ struct Replayer : Params<kPol, kFix> {
             uint64_t kk = 0;
             uint32_t e[16];
             if (isN) {
-                kk = rkeys[j];
-                hh = thash(kk, nbmask, rbmask);
+                kk = rkey(ko, (uint32_t)j);
+                hh = thash(kk, nb, rbmask);
                 load_buckets(table, hh, e);
             }
             bool pa[4] = {isN, rl, isNew, rl && !isNew && (mt & kQMain) != 0};
@@ -1681,7 +1743,7 @@ struct Replayer : Params<kPol, kFix> {
                 if (isNew) {
                     const uint32_t np = tail + (uint32_t)(m - 1 - (seen_new + ma[2].rank(wid)));
                     log[np & lmask] = (uint16_t)slot;
-                    stamp[slot] = np;
+                    stamp[slot] = (StampT)np;
                     meta[slot] = mt | kInLog | (gh ? kQMain : 0u);
                 } else if (rl) {
                     meta[slot] = mt & ~kPin;
@@ -1692,7 +1754,7 @@ struct Replayer : Params<kPol, kFix> {
             } else if (rl) {
                 const uint32_t np = tail + (uint32_t)(nrel - 1 - (seen + ma[1].rank(wid)));
                 log[np & lmask] = (uint16_t)slot;
-                stamp[slot] = np;
+                stamp[slot] = (StampT)np;
                 meta[slot] = (mt & ~kPin) | kInLog | kRes;
             }
             if constexpr (kQueues) wave_add(cnt, 3 * owner_of(mt) + (nseg == 1 ? 0u : cls_of(mt)), rl, 1);
@@ -1748,14 +1810,17 @@ struct Replayer : Params<kPol, kFix> {
             const uint32_t nb = 1u << (nx.p & 31);
             X.qf = ((nref & nb) ? 1u : 0u) | ((nadm & nb) ? 2u : 0u);
         }
-        bsync();   // X.qf and all state of this request are visible
+        // X.qf and all state of this request are visible (hybrid layout: the
+        // new blocks' keys and prefix ids too, which the next lookup reads)
+        if constexpr (kHyb) gsync();
+        else bsync();
         PROF_MARK(5);
         return true;
     }
 
     // ============================================================ run
     DEV void init() {
-        const uint32_t nte = 8u * (nbmask + 1u);
+        const uint32_t nte = 8u * nb;
         for (uint32_t i = tid; i < nte; i += kB) table[i] = kEmpty;
         for (int i = tid; i < C; i += kB) meta[i] = 0;
         for (int i = tid; i < 64; i += kB) res[i] = 0u;
@@ -1764,7 +1829,7 @@ struct Replayer : Params<kPol, kFix> {
             for (int i = tid; i < 196; i += kB) { if (i < 192) cnt[i] = 0u; cur[i] = 0u; }
         for (int i = tid; i < 2 * I.n_prefix_words; i += kB) bits[i] = 0u;
         if (policy == kS3 && g_cap > 0) {
-            const uint32_t nge = 8u * (gnbmask + 1u);
+            const uint32_t nge = 8u * gnb;
             for (uint32_t i = tid; i < nge; i += kB) gtable[i] = kEmpty;
         }
         if (tid == 0) { X.novf = 0; X.nghost = 0; X.kerr = 0; X.qf = 0; }
@@ -1879,59 +1944,68 @@ struct Replayer : Params<kPol, kFix> {
 };
 
 // One instance: the compile-time copy for the default 4096-block layout when
-// the host marked it (LDS state only), else the general one.
-template <bool kLds, int kPol>
+// the host marked it (in that layout's kernel), else the general one.
+template <int kLay, int kPol>
 DEV void run_instance(Coll &coll, const DevInst &I, const DevTrace &T, uint8_t *sbase, uint8_t *ws, int64_t *st,
                       int32_t *per_req) {
-    if constexpr (kLds) {
+    if constexpr (kLay != kLayWs) {
         if (I.fixc == kFixC) {
-            Replayer<kLds, kPol, kFixC> rp(coll, I, T, sbase, ws);
+            Replayer<kLay, kPol, kFixC> rp(coll, I, T, sbase, ws);
             rp.run(st, per_req);
             return;
         }
     }
-    Replayer<kLds, kPol, 0> rp(coll, I, T, sbase, ws);
+    Replayer<kLay, kPol, 0> rp(coll, I, T, sbase, ws);
     rp.run(st, per_req);
 }
 
-template <bool kLds>
-__global__ __launch_bounds__(kB) void replay_kernel(const DevInst *__restrict__ insts,
-                                                    const DevTrace *__restrict__ traces,
-                                                    const int32_t *__restrict__ order, uint8_t *ws,
-                                                    int64_t *stats, int32_t *per_req) {
+// One workgroup per instance.  Every kernel asks for two waves per SIMD (at
+// most 256 registers per lane), so that two instances share a CU when their
+// LDS state fits.
+template <int kLay>
+__global__ __launch_bounds__(kB) __attribute__((amdgpu_waves_per_eu(2)))
+void replay_kernel(const DevInst *__restrict__ insts, const DevTrace *__restrict__ traces,
+                   const int32_t *__restrict__ order, uint8_t *ws, int64_t *stats, int32_t *per_req) {
     extern __shared__ __align__(16) uint8_t smem[];
     __shared__ Coll coll;
     const int id = order[blockIdx.x];
     const DevInst &I = insts[id];
     const DevTrace &T = traces[I.trace];
     uint8_t *sbase;
-    if constexpr (kLds) sbase = smem;
-    else sbase = ws + I.ws_state;
+    if constexpr (kLay == kLayWs) sbase = ws + I.ws_state;
+    else sbase = smem;
     int64_t *st = stats + (int64_t)id * kRecordWords;
-    if (I.policy == kLRU) run_instance<kLds, kLRU>(coll, I, T, sbase, ws, st, per_req);
-    else if (I.policy == kS3) run_instance<kLds, kS3>(coll, I, T, sbase, ws, st, per_req);
-    else if (I.policy == kSQ) run_instance<kLds, kSQ>(coll, I, T, sbase, ws, st, per_req);
-    else run_instance<kLds, kPS>(coll, I, T, sbase, ws, st, per_req);
+    if (I.policy == kLRU) run_instance<kLay, kLRU>(coll, I, T, sbase, ws, st, per_req);
+    else if (I.policy == kS3) run_instance<kLay, kS3>(coll, I, T, sbase, ws, st, per_req);
+    else if (I.policy == kSQ) run_instance<kLay, kSQ>(coll, I, T, sbase, ws, st, per_req);
+    else run_instance<kLay, kPS>(coll, I, T, sbase, ws, st, per_req);
 }
 
 }  // namespace
 
 int32_t replay_static_lds_bytes() { return (int32_t)sizeof(Coll); }
 
+hipError_t replay_set_lds_limit(int32_t lds_bytes) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel<kLayLds>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+    if (e != hipSuccess) return e;
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel<kLayHybrid>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+}
+
 hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order, int32_t n_launch,
-                         int32_t lds_bytes, bool in_lds, uint8_t *ws, int64_t *stats, int32_t *per_req,
+                         int32_t lds_bytes, int layout, uint8_t *ws, int64_t *stats, int32_t *per_req,
                          hipStream_t s) {
     if (n_launch <= 0) return hipSuccess;
-    if (in_lds) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel<true>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(replay_kernel<true>, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s, d_inst,
+    if (layout == kLayLds)
+        hipLaunchKernelGGL(replay_kernel<kLayLds>, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s, d_inst,
                            d_traces, d_order, ws, stats, per_req);
-    } else {
-        hipLaunchKernelGGL(replay_kernel<false>, dim3((unsigned)n_launch), dim3(kB), 0, s, d_inst, d_traces,
+    else if (layout == kLayHybrid)
+        hipLaunchKernelGGL(replay_kernel<kLayHybrid>, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s,
+                           d_inst, d_traces, d_order, ws, stats, per_req);
+    else
+        hipLaunchKernelGGL(replay_kernel<kLayWs>, dim3((unsigned)n_launch), dim3(kB), 0, s, d_inst, d_traces,
                            d_order, ws, stats, per_req);
-    }
     return hipGetLastError();
 }
 

@@ -31,8 +31,27 @@ def assert_same(gpu_res, orc_res, label=""):
     assert inst == orc_res.inst, f"{label}: gpu {inst} != oracle {orc_res.inst}"
 
 
-def run_key_traces(kts, instances_per_trace, per_request=True):
-    """Replay key traces on both sides; every instance compared in full."""
+# Instances that fill the batch beyond what the GPU's CUs hold at once, so
+# that the planner lays every instance out for the most instances per CU
+# (the hybrid layout for large capacities) as in a large batch; they replay
+# an empty trace.
+N_DENSE_PAD = 600
+
+
+def _pad_trace():
+    return tg.KeyTrace(np.zeros(0, np.uint64), np.zeros(1, np.int64), np.zeros(0, np.uint8), np.zeros(0, np.uint8),
+                       np.zeros(0, np.uint32), 1, 1)
+
+
+def run_key_traces(kts, instances_per_trace, per_request=True, dense=False):
+    """Replay key traces on both sides; every instance compared in full.
+    dense: in a batch padded beyond the GPU's CUs (see N_DENSE_PAD)."""
+    kts = list(kts)
+    instances_per_trace = list(instances_per_trace)
+    n_real = sum(len(x) for x in instances_per_trace)
+    if dense:
+        kts.append(_pad_trace())
+        instances_per_trace.append([tg.Instance(0, tg.POLICY_PREFIXSHIELD, 4096) for _ in range(N_DENSE_PAD)])
     dts = [dv.upload_keys(kt) for kt in kts]
     insts = []
     for ti, lst in enumerate(instances_per_trace):
@@ -40,6 +59,7 @@ def run_key_traces(kts, instances_per_trace, per_request=True):
             inst.trace = ti
             insts.append(inst)
     res, pr = replay_gpu(dts, insts, per_request=per_request)
+    res, insts = res[:n_real], insts[:n_real]
     for k, inst in enumerate(insts):
         kt = kts[inst.trace]
         o = oracle.replay_key_trace(kt, inst, per_request=per_request)

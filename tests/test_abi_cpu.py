@@ -155,15 +155,15 @@ def test_product_path_has_no_fallback(monkeypatch):
 def test_state_bytes_on_the_host():
     """Per-instance state size: grows with capacity, the S3-FIFO ghost table
     and PrefixShield's per-block prefix ids add to it, and C = 16384 does not
-    fit the 64 KiB the planner assumes without a device."""
+    fit LDS at all (gfx950: 160 KiB per CU)."""
     T = [_trace()]
     I = [_inst(policy=0, capacity=512), _inst(policy=0, capacity=4096), _inst(policy=1, capacity=4096),
          _inst(policy=2, capacity=4096), _inst(policy=2, capacity=16384)]
-    b, lds = P.pc_replay_state_bytes(T, I)
+    b, lay = P.pc_replay_state_bytes(T, I)
     assert b[0] < b[1] < b[3] and b[1] < b[2]
-    assert b[1] >= 4096 * (8 + 4 + 4)          # key, stamp, meta per block at least
+    assert b[1] >= 4096 * (8 + 2 + 4)          # key, stamp, meta per block at least
     assert b[3] - b[1] >= 4096 * 4             # prefix id per block
-    assert not lds[4]
+    assert lay[4] == P.PC_LAYOUT_WS
     lib = P.lib()
     bad = (P.pc_instance_desc * 1)(_inst(capacity=0))
     out_b = (ctypes.c_int64 * 1)()
@@ -171,19 +171,58 @@ def test_state_bytes_on_the_host():
     assert lib.pc_replay_state_bytes((P.pc_trace_desc * 1)(_trace()), 1, bad, 1, out_b, out_f) == P.PC_EINVAL
 
 
+LDS_CU, STATIC_RESERVE = 160 * 1024, 5120
+
+
+def _lds_part(b, pol, C=4096, ghost_bytes=32 << 10):
+    """LDS bytes of a hybrid instance: its block keys, PrefixShield's prefix
+    ids and S3-FIFO's ghost table are in the workspace."""
+    return b - 8 * C - (4 * C if pol == 2 else 0) - (ghost_bytes if pol == 1 else 0)
+
+
+def test_layout_lets_two_4096_block_instances_share_a_cu():
+    """In a batch too large to run at once, the planner keeps a 4096-block
+    LRU, S3-FIFO or PrefixShield instance's block keys (and prefix ids,
+    ghost table) in the workspace -- the hybrid layout -- which brings its LDS
+    state to half of a CU's 160 KiB, so two share a CU; StaticQuota (free-slot
+    stack) stays whole in LDS, one per CU.  When the batch fits the 256 CUs
+    at once, every instance keeps its whole state in LDS.  Small capacities
+    stay in LDS, 16,384 blocks go to the workspace."""
+    t = _trace(max_req_blocks=512)
+    b, lay = P.pc_replay_state_bytes([t], [_inst(policy=p, capacity=4096) for p in range(4)] * 150)
+    assert lay[:4] == [P.PC_LAYOUT_HYBRID, P.PC_LAYOUT_HYBRID, P.PC_LAYOUT_HYBRID, P.PC_LAYOUT_LDS]
+    for pol in range(3):
+        x = _lds_part(b[pol], pol)
+        assert 2 * (((x + STATIC_RESERVE + 511) // 512) * 512) <= LDS_CU, (pol, x)
+    assert b[3] + STATIC_RESERVE <= LDS_CU < 2 * (b[3] + STATIC_RESERVE)
+    b, lay = P.pc_replay_state_bytes([t], [_inst(policy=p, capacity=4096) for p in range(4)] * 12)
+    assert lay == [P.PC_LAYOUT_LDS] * 48
+    b, lay = P.pc_replay_state_bytes([_trace(max_req_blocks=1024)], [_inst(policy=p, capacity=1024) for p in range(4)])
+    assert lay == [P.PC_LAYOUT_LDS] * 4
+    b, lay = P.pc_replay_state_bytes([_trace(max_req_blocks=1024)], [_inst(policy=p, capacity=16384) for p in range(4)])
+    assert lay == [P.PC_LAYOUT_WS] * 4
+
+
 def test_default_4096_layout_is_sized_for_512_block_requests():
     """A 4096-block instance with default S3-FIFO settings is a candidate for
     the kernel's compile-time copy, so the planner lays it out for requests
     of 512 blocks whatever its trace's longest request (the buffers that
     depend on it only grow); other settings keep the trace's own sizing.
-    The sizes are those of the layout's allocation order: 125,696 bytes for
-    LRU, 158,464 for S3-FIFO, 143,632 for PrefixShield."""
+    The sizes are those of the layouts' allocation order with the table at
+    load 1/2 (all in LDS: 117,504 bytes for LRU, 150,272 for S3-FIFO,
+    135,440 for PrefixShield), or at the largest size that keeps two
+    instances per CU (hybrid: 109,568 / 142,336 / 125,904 bytes, of which
+    76,800 / 76,800 / 76,752 in LDS)."""
     short = _trace(max_req_blocks=100)
     full = _trace(max_req_blocks=512)
-    for pol, want in ((0, 125696), (1, 158464), (2, 143632)):
-        b, _ = P.pc_replay_state_bytes([short, full], [_inst(policy=pol, capacity=4096, trace=0),
-                                                       _inst(policy=pol, capacity=4096, trace=1)])
-        assert list(b) == [want, want]
+    for pol, want in ((0, 117504), (1, 150272), (2, 135440)):
+        b, lay = P.pc_replay_state_bytes([short, full], [_inst(policy=pol, capacity=4096, trace=0),
+                                                         _inst(policy=pol, capacity=4096, trace=1)])
+        assert list(b) == [want, want] and lay == [P.PC_LAYOUT_LDS] * 2
+    for pol, want, lds in ((0, 109568, 76800), (1, 142336, 76800), (2, 125904, 76752)):
+        b, lay = P.pc_replay_state_bytes([short, full], [_inst(policy=pol, capacity=4096, trace=k % 2)
+                                                         for k in range(600)])
+        assert set(b) == {want} and set(lay) == {P.PC_LAYOUT_HYBRID} and _lds_part(want, pol) == lds
     # a non-default small queue, or another capacity, keeps the short sizing
     b, _ = P.pc_replay_state_bytes([short, full], [_inst(policy=1, capacity=4096, trace=0, s3_small_permille=250),
                                                    _inst(policy=1, capacity=4096, trace=1, s3_small_permille=250),

@@ -499,13 +499,17 @@ def test_replay_capacity_at_most_groups():
                 assert istats["resident_max"] == 0
 
 
-def test_replay_default_4096_layout():
+@pytest.mark.parametrize("dense", [False, True])
+def test_replay_default_4096_layout(dense):
     """4096-block instances with default S3-FIFO settings, one contract,
     eps = 0 and no flags, on traces of at most 512 blocks per request, run
     the kernel's copy compiled for that layout; with other settings,
     contracts or capacities they run the general one.  Both against the
     oracle on crafted traces that overflow the cache (duplicates, orphans,
-    requests past one lookup step), every policy."""
+    requests past one lookup step), every policy.  dense: in a batch larger
+    than the GPU holds at once, where the planner takes the hybrid layout
+    (keys, prefix ids and ghost table in HBM; compile-time copies of that
+    layout too)."""
     kts, per = [], []
     for seed in range(3):
         rng = np.random.default_rng(6100 + seed)
@@ -539,7 +543,7 @@ def test_replay_default_4096_layout():
         per.append([tg.Instance(0, pol, 4096, contracts=two) for pol in POLICIES] +
                    [tg.Instance(0, tg.POLICY_S3FIFO, 4096, contracts=two, s3_small_permille=250),
                     tg.Instance(0, tg.POLICY_S3FIFO, 4096, contracts=two, s3_move_threshold=2)])
-    res = run_key_traces(kts, per)
+    res = run_key_traces(kts, per, dense=dense)
     assert sum(inst["evictions"] for _, inst, _ in res) > 0
 
 def test_replay_is_deterministic_and_order_free():
@@ -570,3 +574,33 @@ def test_replay_is_deterministic_and_order_free():
         assert rs[j] == r1[k], f"instance {k} ({insts[k].label}) differs when launched at position {j}"
         assert np.array_equal(ps[j], p1[k])
     assert all(st == 0 for _, _, st in r1)
+
+
+@pytest.mark.parametrize("dense", [False, True])
+def test_replay_large_capacities_both_layouts(dense):
+    """Capacities of 1,500 to 9,000 blocks on crafted traces with hits,
+    orphans, duplicates and requests past one lookup step, every policy and
+    ablation, 1-3 contracts, S3-FIFO settings: alone, their state is whole in
+    LDS (or in the workspace beyond its size); in a batch larger than the
+    GPU holds at once, the planner takes the hybrid layout wherever it fits
+    more instances per CU.  Per-request outputs too."""
+    kts, per = [], []
+    for seed in range(4):
+        rng = np.random.default_rng(4400 + seed)
+        nc = 1 + seed % 3
+        kt = tg.random_key_trace(4400 + seed, n_req=160, max_blocks=700, n_groups=5, n_prefix=40, n_contracts=nc,
+                                 key_universe=6000, with_ticks=bool(seed % 2))
+        insts = []
+        for pol in POLICIES:
+            for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                contracts = [(int(rng.integers(tg.Q16 // 4, 4 * tg.Q16)), int(rng.integers(0, 64)) * tg.Q16)
+                             for _ in range(nc)]
+                insts.append(tg.Instance(0, pol, int(rng.choice([1500, 2048, 3000, 4096, 6000, 9000])),
+                                         contracts=contracts, flags=flags,
+                                         s3_small_permille=int(rng.choice([0, 100, 250, 1000])),
+                                         s3_move_threshold=int(rng.choice([0, 1, 2]))))
+        kts.append(kt)
+        per.append(insts)
+    res = run_key_traces(kts, per, dense=dense)
+    assert sum(g["orphans"] for groups, _, _ in res for g in groups) > 0
+    assert sum(i["evictions"] for _, i, _ in res) > 0

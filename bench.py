@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--workload", default="scale1024")
     ap.add_argument("--seeds", type=int, default=None, help="number of traces (default: the workload's)")
     ap.add_argument("--requests", type=int, default=None, help="requests per trace (default: the workload's)")
+    ap.add_argument("--capacities", default=None,
+                    help="comma-separated capacities in blocks (workloads with a capacity sweep, e.g. chat)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-requests", type=int, default=0,
                     help="requests per trace in the oracle baseline (0: all of them)")
@@ -147,7 +149,10 @@ def main():
 
     t0 = time.time()
     seeds = list(range(args.seeds)) if args.seeds else None
-    traces, insts = tg.workload(args.workload, seeds=seeds, n_requests=args.requests)
+    kw = {}
+    if args.capacities:
+        kw["capacities"] = [int(c) for c in args.capacities.split(",")]
+    traces, insts = tg.workload(args.workload, seeds=seeds, n_requests=args.requests, **kw)
     gen_s = time.time() - t0
     print(f"[bench] generated {len(traces)} traces, {len(insts)} instances in {gen_s:.1f}s", file=sys.stderr,
           flush=True)
@@ -201,7 +206,12 @@ def main():
     hash_bytes = n_blocks_hash * HASH_BYTES_PER_BLOCK + n_req_hash * HASH_BYTES_PER_REQ
     hash_gbs = hash_bytes / (hash_ms * 1e-3) / 1e9
     dominant = "replay" if replay_ms >= hash_ms else "hash"
-    roof = {"kernel": "replay_kernel<true>" if dominant == "replay" else "hash_kernel",
+    # the replay kernel of the layout most instances use (one launch per
+    # footprint class; a single class runs on the caller's stream)
+    _, layouts = P.pc_replay_state_bytes(batch.tdesc, batch.idesc)
+    lay = max(set(layouts), key=layouts.count)
+    roof = {"kernel": f"replay_kernel<{lay}> ({P.LAYOUT_NAMES[lay]} layout)" if dominant == "replay" else "hash_kernel",
+            "layout_instances": {P.LAYOUT_NAMES[x]: layouts.count(x) for x in sorted(set(layouts))},
             "bound": "hbm",
             "achieved": round(replay_gbs if dominant == "replay" else hash_gbs, 3),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",

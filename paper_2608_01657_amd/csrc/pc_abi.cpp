@@ -84,6 +84,7 @@ struct Launch {
     int32_t lds_bytes = 0;
     int32_t first = 0, count = 0;    // range of Plan::order
     double cost = 0;                 // of its costliest instance
+    double est = 0;                  // estimated duration (cost units), see validate_and_plan
 };
 
 struct Plan {
@@ -295,8 +296,8 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
     }
     P.ws_bytes = std::max<int64_t>(off, 256);
     // launches: one per (layout, instances per CU), each sized to its
-    // largest LDS state; instances inside a launch costliest first, and the
-    // launches that take whole CUs first, then by cost
+    // largest LDS state; instances inside a launch costliest first, the
+    // longest launch first
     std::vector<int32_t> ids(n_inst);
     for (int i = 0; i < n_inst; ++i) ids[i] = i;
     auto key_of = [&](int32_t i) { return std::make_pair(P.di[i].layout, per_cu[i]); };
@@ -310,17 +311,22 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         L.per_cu = per_cu[ids[k]];
         L.first = k;
         L.cost = cost[ids[k]];
+        double total = 0;
         while (k < n_inst && key_of(ids[k]) == key_of(ids[L.first])) {
             if (L.layout != pcr::kLayWs) L.lds_bytes = std::max(L.lds_bytes, P.di[ids[k]].state_bytes);
+            total += cost[ids[k]];
             ++k;
         }
         L.count = k - L.first;
+        // duration: its costliest instance, or its work spread over every
+        // slot of the GPU, whichever is longer; state in HBM makes every
+        // request several times slower
+        L.est = std::max(L.cost, total / ((double)L.per_cu * (double)n_cu)) * (L.layout == pcr::kLayWs ? 3.0 : 1.0);
         P.lds_bytes = std::max(P.lds_bytes, L.lds_bytes);
         P.launches.push_back(L);
     }
     std::stable_sort(P.launches.begin(), P.launches.end(), [](const Launch &a, const Launch &b) {
-        const int pa = a.layout == pcr::kLayWs ? 99 : a.per_cu, pb = b.layout == pcr::kLayWs ? 99 : b.per_cu;
-        return pa != pb ? pa < pb : a.cost > b.cost;
+        return a.est > b.est;
     });
     P.order.clear();
     for (Launch &L : P.launches) {
@@ -481,10 +487,17 @@ int32_t launch_planned(const Plan &P, int32_t n_traces, int32_t n_inst, uint8_t 
         e = hipStreamWaitEvent(g_fork.s[dev][k], g_fork.fork[dev], 0);
         if (e != hipSuccess) return hip_fail(e, "fork wait");
     }
+    // longest launch first, each onto the stream with the least estimated
+    // work queued so far
+    double load[kForkStreams] = {};
     for (int l = 0; l < nl; ++l) {
         const Launch &L = P.launches[l];
+        int k = 0;
+        for (int j = 1; j < used; ++j)
+            if (load[j] < load[k]) k = j;
+        load[k] += L.est;
         e = pcr::launch_replay(d_inst, d_tr, d_ord + L.first, L.count, L.lds_bytes, L.layout, ws, (int64_t *)d_stats,
-                               d_per_request, g_fork.s[dev][l % kForkStreams]);
+                               d_per_request, g_fork.s[dev][k]);
         if (e != hipSuccess) return hip_fail(e, "replay launch");
     }
     for (int k = 0; k < used; ++k) {

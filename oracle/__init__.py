@@ -60,6 +60,9 @@ def lib():
         L.orc_replay.restype = ctypes.c_int
         L.orc_replay.argtypes = [P, P, P, P, P, P, i64, i32, i64, i32, i64, i32, i32,
                                  P, P, i64, i32, i32, P, P, P]
+        L.orc_replay_timed.restype = ctypes.c_int
+        L.orc_replay_timed.argtypes = [P, P, P, P, P, P, i64, i32, i64, i32, i64, i32, i32,
+                                       P, P, i64, i32, i32, P, P, P, P]
         _lib = L
     return _lib
 
@@ -114,11 +117,14 @@ class ReplayResult:
     groups: List[Dict[str, int]]
     inst: Dict[str, int]
     per_request: Optional[np.ndarray]   # [R, 4]: hits, new blocks, evictions, orphans
+    reclaim_ns: Optional[np.ndarray] = None   # [R]: wall-clock ns of each request's reclamation (0: none)
 
 
 def replay(keys, key_off, group, contract, prefix, n_groups, n_prefix, inst,
-           tick=None, per_request=False) -> ReplayResult:
-    """Replay one instance (`inst` has the attributes of tracegen.Instance)."""
+           tick=None, per_request=False, time_reclaim=False) -> ReplayResult:
+    """Replay one instance (`inst` has the attributes of tracegen.Instance).
+    time_reclaim: also return each request's reclamation time (Alg. 2 as
+    the oracle runs it: one victim selection at a time)."""
     keys = np.ascontiguousarray(keys, np.uint64)
     if keys.size == 0:
         keys = np.zeros(1, np.uint64)
@@ -134,15 +140,18 @@ def replay(keys, key_off, group, contract, prefix, n_groups, n_prefix, inst,
     gs = np.zeros((n_groups, len(GROUP_FIELDS)), np.int64)
     st = np.zeros(len(INST_FIELDS), np.int64)
     pr = np.zeros((R, 4), np.int32) if per_request else None
-    rc = lib().orc_replay(_ptr(keys), _ptr(key_off), _ptr(group), _ptr(contract), _ptr(prefix),
-                          _ptr(tick), R, n_groups, n_prefix, inst.policy, inst.capacity,
-                          inst.flags, K, _ptr(rho), _ptr(beta), inst.eps_q16,
-                          inst.s3_small_permille, inst.s3_move_threshold,
-                          _ptr(gs), _ptr(st), _ptr(pr))
+    ns = np.zeros(max(R, 1), np.int64) if time_reclaim else None
+    args = (_ptr(keys), _ptr(key_off), _ptr(group), _ptr(contract), _ptr(prefix),
+            _ptr(tick), R, n_groups, n_prefix, inst.policy, inst.capacity,
+            inst.flags, K, _ptr(rho), _ptr(beta), inst.eps_q16,
+            inst.s3_small_permille, inst.s3_move_threshold,
+            _ptr(gs), _ptr(st), _ptr(pr))
+    rc = lib().orc_replay_timed(*args, _ptr(ns)) if time_reclaim else lib().orc_replay(*args)
     if rc != 0:
         raise ValueError(f"oracle replay rejected the input (rc={rc})")
     groups = [dict(zip(GROUP_FIELDS, map(int, row))) for row in gs]
-    return ReplayResult(groups=groups, inst=dict(zip(INST_FIELDS, map(int, st))), per_request=pr)
+    return ReplayResult(groups=groups, inst=dict(zip(INST_FIELDS, map(int, st))), per_request=pr,
+                        reclaim_ns=None if ns is None else ns[:R])
 
 
 def replay_key_trace(kt, inst, per_request=False) -> ReplayResult:
@@ -150,6 +159,6 @@ def replay_key_trace(kt, inst, per_request=False) -> ReplayResult:
                   kt.n_prefix, inst, tick=kt.tick, per_request=per_request)
 
 
-def replay_trace(trace, keys, key_off, inst, per_request=False) -> ReplayResult:
+def replay_trace(trace, keys, key_off, inst, per_request=False, time_reclaim=False) -> ReplayResult:
     return replay(keys, key_off, trace.group, trace.contract, trace.prefix, trace.n_groups,
-                  trace.n_prefix, inst, tick=trace.tick, per_request=per_request)
+                  trace.n_prefix, inst, tick=trace.tick, per_request=per_request, time_reclaim=time_reclaim)

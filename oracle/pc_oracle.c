@@ -39,9 +39,11 @@
  * S3-FIFO internals follow this build's reading of the paper's one-line
  * description and are pinned only by invariants and a brute force.
  */
+#define _POSIX_C_SOURCE 199309L   /* clock_gettime (reclamation timing only) */
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#include <time.h>
 
 /* ------------------------------------------------------------------------ */
 /* PCH64 block keys                                                          */
@@ -409,15 +411,20 @@ static void account_all(Inst *s, int64_t t) {
  *   rho_q16/beta_q16 [n_contracts]
  *   group_stats_out [n_groups][17], inst_stats_out [7]
  *   per_req_out (optional) [n_req][4]: hits, new blocks, evictions, orphans
+ *   reclaim_ns_out (optional) [n_req]: wall-clock nanoseconds of the
+ *     request's reclamation (Alg. 2's victim selection and removal), 0 when
+ *     it evicted nothing -- a measurement of the plain selector, nothing
+ *     else changes
  * Returns 0, or a negative value for invalid input.
  */
-int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *group,
-               const uint8_t *contract, const uint32_t *prefix, const int64_t *tick,
-               int64_t n_req, int32_t n_groups, int64_t n_prefix,
-               int32_t policy, int64_t capacity, int32_t flags, int32_t n_contracts,
-               const int64_t *rho_q16, const int64_t *beta_q16, int64_t eps_q16,
-               int32_t s3_small_permille, int32_t s3_move_threshold,
-               int64_t *group_stats_out, int64_t *inst_stats_out, int32_t *per_req_out) {
+static int replay_impl(const uint64_t *keys, const int64_t *key_off, const uint8_t *group,
+                       const uint8_t *contract, const uint32_t *prefix, const int64_t *tick,
+                       int64_t n_req, int32_t n_groups, int64_t n_prefix,
+                       int32_t policy, int64_t capacity, int32_t flags, int32_t n_contracts,
+                       const int64_t *rho_q16, const int64_t *beta_q16, int64_t eps_q16,
+                       int32_t s3_small_permille, int32_t s3_move_threshold,
+                       int64_t *group_stats_out, int64_t *inst_stats_out, int32_t *per_req_out,
+                       int64_t *reclaim_ns_out) {
     if (policy < 0 || policy > 3 || capacity < 1 || n_groups < 1 || n_groups > 64 ||
         n_contracts < 1 || n_contracts > 4 || eps_q16 < 0 || n_req < 0 || n_prefix < 0)
         return -1;
@@ -579,6 +586,11 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
         int64_t e = m - free_now;
         if (e < 0) e = 0;
         int64_t P[64], D[64];
+        struct timespec ts0 = {0, 0}, ts1 = {0, 0};
+        if (reclaim_ns_out) {
+            reclaim_ns_out[r] = 0;
+            if (e > 0) clock_gettime(CLOCK_MONOTONIC, &ts0);
+        }
         if (policy == ORC_PS && e > 0)
             for (int x = 0; x < s->G; x++) { P[x] = norm_debt(s, x, t); D[x] = debt_decrement(s, x, t); }
         for (int64_t i = 0; i < e; i++) {
@@ -593,6 +605,10 @@ int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *grou
             o[G_EVICTIONS_CAUSED]++;
             s->is[I_EVICTIONS]++;
             drop_block(s, v);
+        }
+        if (reclaim_ns_out && e > 0) {
+            clock_gettime(CLOCK_MONOTONIC, &ts1);
+            reclaim_ns_out[r] = (int64_t)(ts1.tv_sec - ts0.tv_sec) * 1000000000LL + (ts1.tv_nsec - ts0.tv_nsec);
         }
 
         /* Alg. 1 OnCacheFullBlocks: charge n_r = m new full blocks (Eq. 2),
@@ -668,3 +684,29 @@ out:
 
 int orc_group_fields(void) { return G_NFIELDS; }
 int orc_inst_fields(void) { return I_NFIELDS; }
+
+int orc_replay(const uint64_t *keys, const int64_t *key_off, const uint8_t *group,
+               const uint8_t *contract, const uint32_t *prefix, const int64_t *tick,
+               int64_t n_req, int32_t n_groups, int64_t n_prefix,
+               int32_t policy, int64_t capacity, int32_t flags, int32_t n_contracts,
+               const int64_t *rho_q16, const int64_t *beta_q16, int64_t eps_q16,
+               int32_t s3_small_permille, int32_t s3_move_threshold,
+               int64_t *group_stats_out, int64_t *inst_stats_out, int32_t *per_req_out) {
+    return replay_impl(keys, key_off, group, contract, prefix, tick, n_req, n_groups, n_prefix, policy, capacity,
+                       flags, n_contracts, rho_q16, beta_q16, eps_q16, s3_small_permille, s3_move_threshold,
+                       group_stats_out, inst_stats_out, per_req_out, NULL);
+}
+
+/* orc_replay that also times each request's reclamation (reclaim_ns_out). */
+int orc_replay_timed(const uint64_t *keys, const int64_t *key_off, const uint8_t *group,
+                     const uint8_t *contract, const uint32_t *prefix, const int64_t *tick,
+                     int64_t n_req, int32_t n_groups, int64_t n_prefix,
+                     int32_t policy, int64_t capacity, int32_t flags, int32_t n_contracts,
+                     const int64_t *rho_q16, const int64_t *beta_q16, int64_t eps_q16,
+                     int32_t s3_small_permille, int32_t s3_move_threshold,
+                     int64_t *group_stats_out, int64_t *inst_stats_out, int32_t *per_req_out,
+                     int64_t *reclaim_ns_out) {
+    return replay_impl(keys, key_off, group, contract, prefix, tick, n_req, n_groups, n_prefix, policy, capacity,
+                       flags, n_contracts, rho_q16, beta_q16, eps_q16, s3_small_permille, s3_move_threshold,
+                       group_stats_out, inst_stats_out, per_req_out, reclaim_ns_out);
+}

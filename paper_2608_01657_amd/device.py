@@ -163,3 +163,74 @@ class ReplayBatch:
             out.append(host[off:off + 4 * n].reshape(n, 4))
             off += 4 * n
         return out
+
+
+@dataclass
+class TraceView:
+    """One trace of a TraceSet as the replay reads it: its requests' rows of
+    the set's arrays, with key offsets into the set's whole key buffer."""
+    keys: torch.Tensor
+    key_off: torch.Tensor
+    group: torch.Tensor
+    contract: torch.Tensor
+    prefix: torch.Tensor
+    tick: Optional[torch.Tensor]
+    n_groups: int
+    n_prefix: int
+    max_req_blocks: int
+    n_keys: int
+
+
+class TraceSet:
+    """Several traces in one set of device buffers, so that block offsets and
+    keys of all of them take one pc_block_offsets and one pc_hash_blocks
+    call.  Requests keep their own trace's namespace (group) and token view;
+    `views` are what ReplayBatch takes, one per trace."""
+
+    def __init__(self, traces: Sequence, device="cuda"):
+        dev = torch.device(device)
+        tok_base = np.cumsum([0] + [int(tr.tokens.size) for tr in traces[:-1]], dtype=np.int64)
+        self.req_base = np.cumsum([0] + [tr.n_req for tr in traces], dtype=np.int64)
+        cat = lambda xs, dt: torch.from_numpy(np.ascontiguousarray(np.concatenate(xs), dt)).to(dev)
+        any_tick = any(tr.tick is not None for tr in traces)
+        self.dt = DeviceTrace(
+            tokens=cat([tr.tokens for tr in traces], np.int32),
+            tok_off=cat([np.asarray(tr.tok_off, np.int64) + b for tr, b in zip(traces, tok_base)], np.int64),
+            length=cat([tr.length for tr in traces], np.int32),
+            ns=cat([tr.group for tr in traces], np.int32),
+            group=cat([tr.group for tr in traces], np.uint8),
+            contract=cat([tr.contract for tr in traces], np.uint8),
+            prefix=cat([np.asarray(tr.prefix, np.uint32).view(np.int32) for tr in traces], np.int32),
+            # a trace without ticks counts time in requests (tick = request index)
+            tick=cat([tr.tick if tr.tick is not None else np.arange(tr.n_req, dtype=np.int64) for tr in traces],
+                     np.int64) if any_tick else None,
+            n_groups=max(int(tr.n_groups) for tr in traces), n_prefix=max(int(tr.n_prefix) for tr in traces),
+            max_req_blocks=max(int(tr.length.max() // 16) if tr.n_req else 0 for tr in traces))
+        self.meta = [(int(tr.n_groups), int(tr.n_prefix), int(tr.length.max() // 16) if tr.n_req else 0)
+                     for tr in traces]
+        self.views: List[TraceView] = []
+
+    def hash(self, stream=None):
+        """Offsets and keys of every trace (one call each); views are made on
+        the first call."""
+        t = self.dt
+        cut_and_hash(t, n_keys=t.n_keys if t.keys is not None else None, stream=stream)
+        if not self.views:
+            for j, (ng, npfx, mx) in enumerate(self.meta):
+                r0, r1 = int(self.req_base[j]), int(self.req_base[j + 1])
+                self.views.append(TraceView(
+                    keys=t.keys[:t.n_keys] if t.n_keys else t.keys[:0], key_off=t.key_off[r0:r1 + 1],
+                    group=t.group[r0:r1], contract=t.contract[r0:r1], prefix=t.prefix[r0:r1],
+                    tick=None if t.tick is None else t.tick[r0:r1], n_groups=ng, n_prefix=npfx, max_req_blocks=mx,
+                    n_keys=t.n_keys))
+        return self
+
+    def trace_keys(self, j) -> np.ndarray:
+        """Keys of trace j (host copy)."""
+        k0, k1 = int(self.dt.key_off[int(self.req_base[j])].item()), int(self.dt.key_off[int(self.req_base[j + 1])].item())
+        return self.dt.keys[k0:k1].cpu().numpy().view(np.uint64)
+
+    def trace_key_off(self, j) -> np.ndarray:
+        """Key offsets of trace j relative to its own first key (host copy)."""
+        o = self.dt.key_off[int(self.req_base[j]):int(self.req_base[j + 1]) + 1].cpu().numpy()
+        return o - o[0]

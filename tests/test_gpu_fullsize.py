@@ -101,13 +101,15 @@ class _Requests:
     n_req: int
 
 
-def _full_workload(name, n_seeds, policies=tg.ALL_POLICIES):
+def _full_workload(name, n_seeds, policies=tg.ALL_POLICIES, as_set=False):
     """Every seed of workload `name`: keys on both sides (compared in full),
     all instances replayed in one GPU launch and every one compared with the
-    oracle.  Returns the number of instances compared."""
+    oracle.  as_set: the traces are keyed together in one call, as bench.py
+    does (host memory then holds every trace's tokens until then).  Returns
+    the number of instances compared."""
     t0 = time.time()
     pool = ThreadPoolExecutor(WORKERS)
-    dts, reqs, insts, key_futs, orc_futs = [], [], [], [], []
+    dts, reqs, insts, key_futs, orc_futs, kept = [], [], [], [], [], []
 
     def oracle_replay(k, spec):
         okeys, ooff = key_futs[spec.trace].result()
@@ -117,12 +119,15 @@ def _full_workload(name, n_seeds, policies=tg.ALL_POLICIES):
         for i in range(n_seeds):
             trs, its = tg.workload(name, seeds=[i], policies=policies)
             tr = trs[0]
-            ti = len(dts)
-            t = dv.upload(tr)
-            dv.cut_and_hash(t)
+            ti = len(reqs)
             key_futs.append(pool.submit(oracle.hash_trace, tr))
-            t.tokens = t.tokens[:0]          # keys are made: the replay never reads tokens
-            dts.append(t)
+            if as_set:
+                kept.append(tr)
+            else:
+                t = dv.upload(tr)
+                dv.cut_and_hash(t)
+                t.tokens = t.tokens[:0]      # keys are made: the replay never reads tokens
+                dts.append(t)
             reqs.append(_Requests(tr.name, tr.group, tr.contract, tr.prefix, tr.n_groups, tr.n_prefix, tr.tick,
                                   tr.n_req))
             del tr, trs
@@ -132,8 +137,19 @@ def _full_workload(name, n_seeds, policies=tg.ALL_POLICIES):
                 orc_futs.append(pool.submit(oracle_replay, k, insts[k]))
             if i % 8 == 7 or i == n_seeds - 1:
                 _log(f"{name}: {i + 1}/{n_seeds} seeds generated and keyed ({time.time() - t0:.0f}s)")
+        if as_set:
+            ts = dv.TraceSet(kept).hash()
+            kept.clear()
+            torch.cuda.synchronize()
+            assert int(ts.dt.status.item()) == 0, f"{name}: hash status"
+            for i in range(len(reqs)):
+                okeys, ooff = key_futs[i].result()
+                assert np.array_equal(ts.trace_key_off(i), ooff), f"{name} seed {i}: key offsets differ"
+                bad = np.flatnonzero(ts.trace_keys(i) != okeys)
+                assert bad.size == 0, f"{name} seed {i}: {bad.size} keys differ, first at {bad[:5]}"
+            dts = ts.views
         torch.cuda.synchronize()
-        for i, t in enumerate(dts):
+        for i, t in enumerate(dts if not as_set else []):
             assert int(t.status.item()) == 0, f"{name} seed {i}: hash status"
             okeys, ooff = key_futs[i].result()
             assert np.array_equal(t.key_off.cpu().numpy(), ooff), f"{name} seed {i}: key offsets differ"
@@ -160,7 +176,7 @@ def _full_workload(name, n_seeds, policies=tg.ALL_POLICIES):
 @pytest.mark.timeout(900)
 def test_onetouch4096_bench_batch_all_instances():
     """Config 2: 16 seeds x 3 policies = 48 concurrent 4096-block instances."""
-    assert _full_workload("onetouch4096", 16) == 48
+    assert _full_workload("onetouch4096", 16, as_set=True) == 48
 
 
 @pytest.mark.timeout(900)
@@ -188,8 +204,9 @@ def test_chat_all_instances():
 @pytest.mark.timeout(900)
 def test_scale1024_all_instances():
     """1,024 concurrent 4096-block instances (16 traces x LRU, S3-FIFO and
-    PrefixShield at 62 refill rates), as bench.py times them."""
-    assert _full_workload("scale1024", 16) == 1024
+    PrefixShield at 62 refill rates), keyed and replayed as bench.py times
+    them."""
+    assert _full_workload("scale1024", 16, as_set=True) == 1024
 
 
 def test_chat_staticquota_full_length():

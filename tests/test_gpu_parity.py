@@ -604,3 +604,28 @@ def test_replay_large_capacities_both_layouts(dense):
     res = run_key_traces(kts, per, dense=dense)
     assert sum(g["orphans"] for groups, _, _ in res for g in groups) > 0
     assert sum(i["evictions"] for _, i, _ in res) > 0
+
+
+def test_trace_set_hashes_and_replays_like_separate_traces():
+    """Traces hashed together (one block-offsets and one hash call over a
+    shared token buffer, as bench.py does) give every trace's keys, and a
+    replay over the set's per-trace views gives the oracle's records --
+    traces with and without ticks, of different group counts, mixed."""
+    traces = (tg.workload("tiny", seeds=[0], n_requests=900)[0] + tg.workload("chat_bursty", seeds=[1], n_requests=1500)[0]
+              + tg.workload("onetouch4096", seeds=[2], n_requests=700)[0] + tg.workload("tiers", seeds=[0], n_requests=800)[0])
+    ts = dv.TraceSet(traces).hash()
+    assert int(ts.dt.status.item()) == 0
+    okeys = [oracle.hash_trace(tr) for tr in traces]
+    for j, (k, off) in enumerate(okeys):
+        assert np.array_equal(ts.trace_keys(j), k), f"trace {j}: keys differ"
+        assert np.array_equal(ts.trace_key_off(j), off), f"trace {j}: key offsets differ"
+    insts = []
+    for j, tr in enumerate(traces):
+        for pol in POLICIES:
+            insts.append(tg.Instance(j, pol, [256, 2048, 4096, 1024][j],
+                                     contracts=list(tg.TIER_CONTRACTS) if j == 3 else [(tg.DEFAULT_RHO_Q16, tg.DEFAULT_BETA_Q16)]))
+    res, pr = replay_gpu(ts.views, insts, per_request=True)
+    for k, spec in enumerate(insts):
+        o = oracle.replay_trace(traces[spec.trace], okeys[spec.trace][0], okeys[spec.trace][1], spec, per_request=True)
+        assert_same(res[k], o, f"trace {spec.trace} {tg.POLICY_NAMES[spec.policy]}")
+        assert np.array_equal(pr[k], o.per_request)

@@ -490,3 +490,18 @@ def test_staticquota_truncates_at_the_partition():
     res = oracle.replay_key_trace(kt, tg.Instance(0, SQ, 1))   # quota 0
     assert all(g["probes"] == 0 and g["resident_max"] == 0 for g in res.groups)
     assert res.groups[0]["truncated"] == 20
+
+
+def test_reclamation_timing_changes_nothing():
+    """The timed replay (the oracle's selector measured per request) gives
+    the same counters and per-request outputs, and a positive time exactly
+    for the requests that evicted."""
+    trs, insts = tg.workload("selector512x8", seeds=[0], n_requests=600)
+    k, off = oracle.hash_trace(trs[0])
+    for spec in insts:
+        a = oracle.replay_trace(trs[0], k, off, spec, per_request=True)
+        b = oracle.replay_trace(trs[0], k, off, spec, per_request=True, time_reclaim=True)
+        assert a.groups == b.groups and a.inst == b.inst
+        assert np.array_equal(a.per_request, b.per_request)
+        ev = b.per_request[:, 2] > 0
+        assert ev.any() and np.all((b.reclaim_ns > 0) == ev)

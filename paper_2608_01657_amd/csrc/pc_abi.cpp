@@ -467,7 +467,7 @@ int32_t launch_planned(const Plan &P, int32_t n_traces, int32_t n_inst, uint8_t 
     const int nl = (int)P.launches.size();
     if (!fork || nl < 2) {
         for (const Launch &L : P.launches) {
-            e = pcr::launch_replay(d_inst, d_tr, d_ord + L.first, L.count, L.lds_bytes, L.layout, ws,
+            e = pcr::launch_replay(d_inst, d_tr, d_ord + L.first, L.count, L.lds_bytes, L.layout, L.per_cu, ws,
                                    (int64_t *)d_stats, d_per_request, s);
             if (e != hipSuccess) return hip_fail(e, "replay launch");
         }
@@ -496,8 +496,8 @@ int32_t launch_planned(const Plan &P, int32_t n_traces, int32_t n_inst, uint8_t 
         for (int j = 1; j < used; ++j)
             if (load[j] < load[k]) k = j;
         load[k] += L.est;
-        e = pcr::launch_replay(d_inst, d_tr, d_ord + L.first, L.count, L.lds_bytes, L.layout, ws, (int64_t *)d_stats,
-                               d_per_request, g_fork.s[dev][k]);
+        e = pcr::launch_replay(d_inst, d_tr, d_ord + L.first, L.count, L.lds_bytes, L.layout, L.per_cu, ws,
+                               (int64_t *)d_stats, d_per_request, g_fork.s[dev][k]);
         if (e != hipSuccess) return hip_fail(e, "replay launch");
     }
     for (int k = 0; k < used; ++k) {

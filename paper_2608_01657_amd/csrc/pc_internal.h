@@ -229,9 +229,10 @@ int32_t replay_static_lds_bytes();
 // Raise the dynamic-LDS limit of the LDS-state kernels to lds_bytes (once
 // per batch, before its launches).
 hipError_t replay_set_lds_limit(int32_t lds_bytes);
-// One launch of n_launch instances d_order[0..n_launch) of one layout.
+// One launch of n_launch instances d_order[0..n_launch) of one layout,
+// planned for per_cu instances per CU.
 hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order,
-                         int32_t n_launch, int32_t lds_bytes, int layout, uint8_t *ws,
+                         int32_t n_launch, int32_t lds_bytes, int layout, int per_cu, uint8_t *ws,
                          int64_t *stats, int32_t *per_req, hipStream_t s);
 
 }  // namespace pcr

@@ -1959,13 +1959,10 @@ DEV void run_instance(Coll &coll, const DevInst &I, const DevTrace &T, uint8_t *
     rp.run(st, per_req);
 }
 
-// One workgroup per instance.  Every kernel asks for two waves per SIMD (at
-// most 256 registers per lane), so that two instances share a CU when their
-// LDS state fits.
+// One workgroup per instance.
 template <int kLay>
-__global__ __launch_bounds__(kB) __attribute__((amdgpu_waves_per_eu(2)))
-void replay_kernel(const DevInst *__restrict__ insts, const DevTrace *__restrict__ traces,
-                   const int32_t *__restrict__ order, uint8_t *ws, int64_t *stats, int32_t *per_req) {
+DEV void replay_body(const DevInst *__restrict__ insts, const DevTrace *__restrict__ traces,
+                     const int32_t *__restrict__ order, uint8_t *ws, int64_t *stats, int32_t *per_req) {
     extern __shared__ __align__(16) uint8_t smem[];
     __shared__ Coll coll;
     const int id = order[blockIdx.x];
@@ -1980,6 +1977,22 @@ void replay_kernel(const DevInst *__restrict__ insts, const DevTrace *__restrict
     else if (I.policy == kSQ) run_instance<kLay, kSQ>(coll, I, T, sbase, ws, st, per_req);
     else run_instance<kLay, kPS>(coll, I, T, sbase, ws, st, per_req);
 }
+// Two instances per CU: two waves per SIMD, so at most 256 registers per
+// lane.
+template <int kLay>
+__global__ __launch_bounds__(kB) __attribute__((amdgpu_waves_per_eu(2)))
+void replay_kernel(const DevInst *__restrict__ insts, const DevTrace *__restrict__ traces,
+                   const int32_t *__restrict__ order, uint8_t *ws, int64_t *stats, int32_t *per_req) {
+    replay_body<kLay>(insts, traces, order, ws, stats, per_req);
+}
+// An instance whose LDS state takes the whole CU: no occupancy target, so
+// the compiler schedules for one wave per SIMD (about 5 % less time per
+// request than the same code built for two).
+__global__ __launch_bounds__(kB)
+void replay_kernel_solo(const DevInst *__restrict__ insts, const DevTrace *__restrict__ traces,
+                        const int32_t *__restrict__ order, uint8_t *ws, int64_t *stats, int32_t *per_req) {
+    replay_body<kLayLds>(insts, traces, order, ws, stats, per_req);
+}
 
 }  // namespace
 
@@ -1989,15 +2002,21 @@ hipError_t replay_set_lds_limit(int32_t lds_bytes) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel<kLayLds>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
     if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel_solo),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+    if (e != hipSuccess) return e;
     return hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel<kLayHybrid>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
 }
 
 hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order, int32_t n_launch,
-                         int32_t lds_bytes, int layout, uint8_t *ws, int64_t *stats, int32_t *per_req,
+                         int32_t lds_bytes, int layout, int per_cu, uint8_t *ws, int64_t *stats, int32_t *per_req,
                          hipStream_t s) {
     if (n_launch <= 0) return hipSuccess;
-    if (layout == kLayLds)
+    if (layout == kLayLds && per_cu == 1)
+        hipLaunchKernelGGL(replay_kernel_solo, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s, d_inst,
+                           d_traces, d_order, ws, stats, per_req);
+    else if (layout == kLayLds)
         hipLaunchKernelGGL(replay_kernel<kLayLds>, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s, d_inst,
                            d_traces, d_order, ws, stats, per_req);
     else if (layout == kLayHybrid)

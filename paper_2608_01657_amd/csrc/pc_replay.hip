@@ -1003,8 +1003,13 @@ struct Replayer : Params<kLay, kPol, kFix> {
             const int ag = (int)bcast32(avail, gs);
             const int64_t p2 = wave_max64((inE && lane != gs) ? P : -1);
             const int64_t thr = p2 > eps ? p2 : eps;
-            // g* keeps winning strictly while P - i*D > max(second, eps)
-            const int64_t k1 = Pg > thr ? (int64_t)udiv64((uint64_t)(Pg - thr) + (uint64_t)Dg - 1, (uint64_t)Dg) : 0;
+            // g* keeps winning strictly while P - i*D > max(second, eps); with
+            // one contract the decrement is exactly one block (a shift)
+            int64_t k1 = 0;
+            if (Pg > thr) {
+                const uint64_t num = (uint64_t)(Pg - thr) + (uint64_t)Dg - 1;
+                k1 = K == 1 ? (int64_t)(num >> 16) : (int64_t)udiv64(num, (uint64_t)Dg);
+            }
             int64_t k = k1 > 1 ? k1 : 1;
             if (k > rem) k = rem;
             if (k > ag) k = ag;
@@ -1554,16 +1559,20 @@ struct Replayer : Params<kLay, kPol, kFix> {
         }
         // the next request's first keys and prefix bits, and the descriptor
         // after it, go in flight now; stores follow the loads so that waiting
-        // for the loads never waits for a store
+        // for the loads never waits for a store.  The bitmap words go first:
+        // their address needs the next request's prefix id, loaded a request
+        // ago, and the compiler's wait for that load (the vector-memory
+        // counter, counted in order) would otherwise also wait for the key
+        // loads issued just before it.
         uint64_t knext = 0;
         uint32_t nref = 0, nadm = 0;
         if (has_next) {
-            knext = (tid < nx.nfull()) ? tkeys[nx.ko + tid] : 0ull;
             if (tid == 0) {
                 const uint32_t nwd = nx.p >> 5;
                 nref = bits[nwd];
                 nadm = bits[npw + nwd];
             }
+            knext = (tid < nx.nfull()) ? tkeys[nx.ko + tid] : 0ull;
         }
         if (r + 2 < n_req) nn = load_req(r + 2);
         if (tid == 0) {

@@ -215,7 +215,12 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         const int nl = plan_lds[i].per_cu, nh = plan_hyb[i].per_cu;
         d.layout = nl > 0 && nl >= nh ? pcr::kLayLds : nh > 0 ? pcr::kLayHybrid : pcr::kLayWs;
         per_cu[i] = d.layout == pcr::kLayLds ? nl : d.layout == pcr::kLayHybrid ? nh : pcr::kMaxWgPerCu;
-        cost[i] = (double)t.n_keys * (s.policy == PC_LRU ? 1.0 : 1.4) + (double)t.n_req * 16.0;
+        // replay time of the instance, in LRU probe units: cycles per request
+        // measured with the phase-counter build relative to LRU's (S3-FIFO
+        // 1.7-1.8x, PrefixShield 1.5x), plus a per-request share; the
+        // costliest instances start first
+        const double per_probe = s.policy == PC_S3FIFO ? 1.75 : s.policy == PC_PREFIXSHIELD ? 1.5 : 1.0;
+        cost[i] = (double)t.n_keys * per_probe + (double)t.n_req * 16.0;
         d.per_req_off = per_req;
         per_req += 4 * t.n_req;
     }

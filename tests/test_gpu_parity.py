@@ -302,6 +302,75 @@ def test_hash_out_of_range_requests_are_skipped():
         assert np.array_equal(keys[a:b], want), f"request {r}"
 
 
+def _many_request_trace(n_req, seed, shared):
+    """n_req requests: mostly blockless or one- and two-block requests, some
+    of hundreds of tokens, a few of thousands, and a stretch of 300
+    consecutive blockless requests.  shared: the requests read overlapping
+    windows of one 2 M-token buffer at any int32 offset (token reuse: the
+    4-wave key kernel); else each request has its own tokens, laid out back
+    to back with gaps of 0-3 tokens (streaming: the 16-wave key kernel)."""
+    rng = np.random.default_rng(seed)
+    u = rng.random(n_req)
+    lens = np.where(u < 0.90, rng.integers(0, 48, n_req),
+                    np.where(u < 0.999, rng.integers(48, 400, n_req), rng.integers(400, 5000, n_req)))
+    a = n_req // 3
+    lens[a:a + 300] = rng.integers(0, 16, 300)
+    lens = lens.astype(np.int32)
+    if shared:
+        n_tok = 2_000_000
+        offs = (rng.random(n_req) * (n_tok - lens)).astype(np.int64)
+    else:
+        gaps = rng.integers(0, 4, n_req)
+        offs = np.cumsum(gaps + lens) - lens
+        n_tok = int(offs[-1] + lens[-1])
+    toks = rng.integers(-2**31, 2**31, n_tok, dtype=np.int64).astype(np.int32)
+    ns = rng.integers(0, 256, n_req).astype(np.uint8)
+    blocks = int((lens // 16).sum())
+    assert (blocks <= 2 * (n_tok // 16)) != shared, "the trace does not take the intended key kernel"
+    return tg.Trace("many", toks, offs.astype(np.int64), lens, ns, np.zeros(n_req, np.uint8),
+                    np.zeros(n_req, np.uint32), 256, n_req)
+
+
+@pytest.mark.parametrize("n_req,shared", [(131_109, True), (1_507_339, False), (4_194_341, True)])
+def test_hash_many_requests(n_req, shared):
+    """Grids of 8 K to 1 M workgroups, with a ragged last workgroup, on both
+    key kernels: every key of every request."""
+    _check_hash(_many_request_trace(n_req, seed=n_req % 1000, shared=shared))
+
+
+@pytest.mark.parametrize("n_req,shared", [(131_077, False), (4_194_309, True)])
+def test_hash_bad_requests_among_many(n_req, shared):
+    """Requests that fail the bounds check scattered through a large grid:
+    the status is PC_EINVAL, they write nothing, and their neighbours in the
+    same workgroup still get their keys."""
+    import torch
+    import paper_2608_01657_amd as P
+    tr = _many_request_trace(n_req, seed=200 + n_req % 1000, shared=shared)
+    okeys, ooff = oracle.hash_trace(tr)
+    offs = tr.tok_off.copy()
+    lens = tr.length
+    withkeys = np.nonzero(lens >= 16)[0]
+    rng = np.random.default_rng(7)
+    bad = np.sort(rng.choice(withkeys, 12, replace=False))
+    offs[bad[:6]] = -3                                  # negative offset
+    offs[bad[6:]] = len(tr.tokens) - 5                  # runs past the token buffer
+    dev = torch.device("cuda")
+    sentinel = 0x5A5A5A5A5A5A5A5A
+    n_keys = int(ooff[-1])
+    d_keys = torch.full((n_keys,), sentinel, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    P.pc_hash_blocks(torch.from_numpy(tr.tokens).to(dev), torch.from_numpy(offs).to(dev),
+                     torch.from_numpy(lens).to(dev), torch.from_numpy(tr.group.astype(np.int32)).to(dev),
+                     torch.from_numpy(ooff).to(dev), d_keys, status, None)
+    assert int(status.item()) == P.PC_EINVAL
+    keys = d_keys.cpu().numpy().view(np.uint64)
+    want = okeys.copy()
+    for r in bad:
+        want[ooff[r]:ooff[r + 1]] = np.uint64(sentinel)
+    diff = np.nonzero(keys != want)[0]
+    assert diff.size == 0, f"{diff.size} keys differ, first at {diff[:5]}"
+
+
 def _prefix_trace(kt, k):
     """The first k requests of key trace kt."""
     return tg.KeyTrace(kt.keys[:int(kt.key_off[k])], kt.key_off[:k + 1].copy(), kt.group[:k].copy(),

@@ -67,13 +67,15 @@ int32_t pc_block_offsets(const int32_t *d_req_len, int64_t n_req, int32_t block_
  *
  *   d_tokens   [n_tokens] int32, 4-byte aligned (else PC_EINVAL); a
  *              request may start at any token, and requests may alias.
- *   d_req_tok_off, d_req_len, d_req_ns  [n_req]: start, length, namespace.
+ *   d_req_tok_off, d_req_len, d_req_ns  [n_req]: start, length, namespace;
+ *              a request holds fewer than 2^30 tokens (4 GiB).
  *   d_key_off  [n_req+1] output of pc_block_offsets (or any offsets with
  *              room for floor(len/16) keys per request).
  *   d_keys     [n_keys] output.
  *   d_status   one int32 in device memory, set to PC_EINVAL by the kernel if
- *              any request's token or key range falls outside the buffers
- *              (that request is skipped); the caller zeroes it beforehand.
+ *              any request's token or key range falls outside the buffers,
+ *              or its length is negative or 2^30 or more (that request is
+ *              skipped); the caller zeroes it beforehand.
  * ------------------------------------------------------------------------ */
 int32_t pc_hash_blocks(const int32_t *d_tokens, int64_t n_tokens,
                        const int64_t *d_req_tok_off, const int32_t *d_req_len,

@@ -228,7 +228,7 @@ __device__ __forceinline__ void issue(Step &S, const GLOBAL int32_t *__restrict_
     for (int q = 0; q < 4; ++q) {
         int32_t blk = it + 16 * q + bq;
         blk = blk < nb ? blk : nb - 1;
-        // byte offset < 2^31: a request holds fewer than 2^31 tokens
+        // byte offset < 2^32: the kernel skips requests of 2^30 tokens or more
         const uint32_t byte = (uint32_t)blk * 64u + (uint32_t)r4 * 16u;
         S.v[q] = *reinterpret_cast<const GLOBAL u32x4_a4 *>(reinterpret_cast<const GLOBAL uint8_t *>(tok) + byte);
     }
@@ -299,7 +299,8 @@ __global__ __launch_bounds__(64 * kWaves) void hash_kernel(
     const int32_t len = req_len[r];
     const int64_t ko = key_off[r];
     const int64_t nb = len > 0 ? len / 16 : 0;
-    if (len < 0 || off < 0 || off + (int64_t)len > n_tokens || ko < 0 || ko + nb > n_keys) {
+    // a request of 2^30 tokens or more would take byte offsets past 2^32
+    if (len < 0 || len >= (1 << 30) || off < 0 || off + (int64_t)len > n_tokens || ko < 0 || ko + nb > n_keys) {
         if (lane == 0) atomicExch(status, -1);
         return;
     }

@@ -371,6 +371,39 @@ def test_hash_bad_requests_among_many(n_req, shared):
     assert diff.size == 0, f"{diff.size} keys differ, first at {diff[:5]}"
 
 
+def test_hash_request_length_limit():
+    """A request of 2^30 tokens (4 GiB) or more is skipped with PC_EINVAL;
+    one of 2^30 - 1 tokens, the longest allowed, gets all of its 2^26 - 1
+    keys, equal to the oracle's."""
+    import torch
+    import paper_2608_01657_amd as P
+    dev = torch.device("cuda")
+    n_tok = (1 << 30) + 4096
+    g = torch.Generator(device=dev).manual_seed(31)
+    d_toks = torch.randint(-2**31, 2**31, (n_tok,), dtype=torch.int32, device=dev, generator=g)
+    offs = np.array([0, 7, 123_456], np.int64)
+    lens = np.array([1 << 30, (1 << 30) - 1, 5000], np.int32)
+    ns = np.array([3, 4, 5], np.int32)
+    key_off = oracle.block_offsets(lens)
+    n_keys = int(key_off[-1])
+    sentinel = 0x5A5A5A5A5A5A5A5A
+    d_keys = torch.full((n_keys,), sentinel, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    P.pc_hash_blocks(d_toks, torch.from_numpy(offs).to(dev), torch.from_numpy(lens).to(dev),
+                     torch.from_numpy(ns).to(dev), torch.from_numpy(key_off).to(dev), d_keys, status, None)
+    assert int(status.item()) == P.PC_EINVAL
+    keys = d_keys.cpu().numpy().view(np.uint64)
+    del d_keys
+    toks = d_toks.cpu().numpy()
+    del d_toks
+    assert np.all(keys[key_off[0]:key_off[1]] == np.uint64(sentinel)), "the 2^30-token request wrote keys"
+    for r in (1, 2):
+        want = oracle.hash_request(toks[offs[r]:offs[r] + lens[r]], int(ns[r]))
+        got = keys[key_off[r]:key_off[r + 1]]
+        bad = np.flatnonzero(got != want)
+        assert bad.size == 0, f"request {r}: {bad.size} keys differ, first at {bad[:5]}"
+
+
 def _prefix_trace(kt, k):
     """The first k requests of key trace kt."""
     return tg.KeyTrace(kt.keys[:int(kt.key_off[k])], kt.key_off[:k + 1].copy(), kt.group[:k].copy(),

@@ -190,8 +190,10 @@ def main():
         step(evs[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    hash_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    replay_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    hash_each = [e[0].elapsed_time(e[1]) for e in evs]
+    replay_each = [e[1].elapsed_time(e[2]) for e in evs]
+    hash_ms = float(np.mean(hash_each))
+    replay_ms = float(np.mean(replay_each))
     step_ms = wall * 1000.0 / args.steps
 
     res = batch.results()
@@ -251,6 +253,8 @@ def main():
         "replay_probes_per_s": probes / (replay_ms * 1e-3),
         "replay_requests_per_s": n_req_total / (replay_ms * 1e-3),
         "hash_ms": hash_ms, "replay_ms": replay_ms,
+        "hash_ms_median_min_max": [float(np.median(hash_each)), float(min(hash_each)), float(max(hash_each))],
+        "replay_ms_median_min_max": [float(np.median(replay_each)), float(min(replay_each)), float(max(replay_each))],
         "probes_per_step": probes, "hits_per_step": hits, "requests_per_step": n_req_total,
         "roofline": roof,
         "roofline_hash": roof_hash,
@@ -263,16 +267,19 @@ def main():
 
 def phase_report(batch, insts, traces, replay_ms):
     """Per policy: mean cycles per request of each phase, the reclamation
-    cycles of a request that evicts (converted to microseconds with the clock
-    rate implied by the slowest instance, whose cycles span the launch), and
-    state bytes per cached block."""
+    cycles of a request that evicts (converted to microseconds with the
+    shader clock's rate, measured by every instance as its span in shader
+    cycles over its span on the 100 MHz real-time clock), and state bytes
+    per cached block."""
     import paper_2608_01657_amd as P
     from paper_2608_01657_amd import tracegen as tg
     pcs = batch.phase_counters()
     totals = [sum(pc[f"cycles_{n}"] for n in P.PHASE_NAMES) for pc in pcs]
-    mhz = max(totals) / (replay_ms * 1e3)   # cycles per microsecond
+    mhz = sum(pc["span_cycles"] for pc in pcs) / (sum(pc["span_ticks_100mhz"] for pc in pcs) / 100.0)
     sbytes, layout = P.pc_replay_state_bytes(batch.tdesc, batch.idesc)
-    rep = {"clock_cycles_per_us": round(mhz, 1)}
+    rep = {"clock_cycles_per_us": round(mhz, 1),
+           "instance_span_ms_mean": round(float(np.mean([pc["span_ticks_100mhz"] for pc in pcs])) / 1e5, 3),
+           "replay_ms": round(replay_ms, 3)}
     for pol in sorted({i.policy for i in insts}):
         ks = [k for k, i in enumerate(insts) if i.policy == pol]
         nreq = sum(traces[insts[k].trace].n_req for k in ks)
@@ -354,17 +361,32 @@ def cpu_baseline(traces, insts, sample_requests, sample_traces):
     threads = max(1, min(nproc, len(sample)))
     t0 = time.perf_counter()
     c0 = time.process_time()
+    def timed(f, *a):
+        t = time.perf_counter()
+        r = f(*a)
+        return r, time.perf_counter() - t
+
     with ThreadPoolExecutor(max_workers=threads) as ex:
-        hashed = list(ex.map(oracle.hash_trace, sub))
-        results = list(ex.map(lambda i: oracle.replay_trace(sub[i.trace], hashed[i.trace][0],
-                                                             hashed[i.trace][1], i), sample))
+        hashed_t = list(ex.map(lambda tr: timed(oracle.hash_trace, tr), sub))
+        hashed = [h for h, _ in hashed_t]
+        rep_t = list(ex.map(lambda i: timed(oracle.replay_trace, sub[i.trace], hashed[i.trace][0],
+                                            hashed[i.trace][1], i), sample))
     wall = time.perf_counter() - t0
     cpu_s = time.process_time() - c0
+    results = [r for r, _ in rep_t]
     probes = sum(sum(g["probes"] for g in r.groups) for r in results)
     reqs = sum(sub[i.trace].n_req for i in sample)
+    # each call runs on one thread: per-instance replay rates, hashed tokens
+    # (full blocks) per second of one thread
+    per_inst = [sum(g["probes"] for g in r.groups) / dt for r, dt in rep_t if dt > 0]
+    hashed_tokens = sum(int((tr.length.astype(np.int64) // 16).sum()) * 16 for tr in sub)
+    hash_s = sum(dt for _, dt in hashed_t)
     return {"value": probes / wall, "unit": "probes/s", "cores": threads, "kind": "oracle",
             "nproc": nproc, "cpu_model": cpu_model(),
             "requests_per_s": reqs / wall, "probes_per_s_per_thread": probes / cpu_s if cpu_s > 0 else None,
+            "instance_probes_per_s_median": float(np.median(per_inst)) if per_inst else None,
+            "hash_tokens_per_s_per_thread": hashed_tokens / hash_s if hash_s > 0 else None,
+            "wall_s": wall,
             "sample": f"{'all' if all(s.n_req == t.n_req for s, t in zip(sub, traces)) else 'the first'} "
                       f"{sub[0].n_req} requests of trace{'s' if n_tr > 1 else ''} 0"
                       f"{'-' + str(n_tr - 1) if n_tr > 1 else ''} of {len(traces)}, all {len(sample)} of their "

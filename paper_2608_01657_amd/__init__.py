@@ -97,6 +97,8 @@ def phase_counters(groups) -> dict:
     g = groups[63]
     vals = [g[f] for f in GROUP_FIELDS]
     out = {f"cycles_{n}": int(vals[i]) for i, n in enumerate(PHASE_NAMES)}
+    out["span_cycles"] = int(vals[6])          # the instance's span on the shader clock
+    out["span_ticks_100mhz"] = int(vals[7])    # and on the 100 MHz real-time clock
     out.update({n: int(vals[8 + i]) for i, n in enumerate(PHASE_EVENTS)})
     return out
 

@@ -266,6 +266,7 @@ struct Coll {
 #ifdef PC_PROFILE
     uint64_t prof[8];                 // cycles per request phase (thread 0)
     uint64_t prof_last;
+    uint64_t prof_t0, prof_rt0;       // shader clock and 100 MHz real-time clock at the instance's start
     uint64_t pcnt[8];                 // event counts (thread 0)
 #endif
 };
@@ -313,8 +314,10 @@ DEV uint32_t freq_of(uint32_t mt) { return (mt >> kFreqShift) & 3u; }
 //   0 request start (descriptor checks, OnRequest)   1 lookup (+ prefetch)
 //   2 reclamation   3 charge   4 insert + release   5 accounting
 // and counts: 0 requests that evicted, 1 log compactions, 2 S3-FIFO scan
-// batches, 3 PrefixShield queue takes.  The totals replace the record of
-// group 63 in the stats.  The counters cost a few percent; nothing of the
+// batches, 3 PrefixShield queue takes.  The instance's whole span is also
+// taken on the shader clock and on the 100 MHz real-time clock, which gives
+// the shader clock's rate.  The totals replace the record of group 63 in the
+// stats.  The counters cost a few percent; nothing of the
 // replay itself is skipped or changed.
 // PROF_MARK(i) adds the cycles since the previous mark to counter i.
 #ifdef PC_PROFILE
@@ -1868,7 +1871,10 @@ struct Replayer : Params<kLay, kPol, kFix> {
         last_h = last_m = last_e = last_o = 0;
 #ifdef PC_PROFILE
         if (tid < 8) { X.prof[tid] = 0; X.pcnt[tid] = 0; }
-        if (tid == 0) X.prof_last = __builtin_amdgcn_s_memtime();
+        if (tid == 0) {
+            X.prof_last = X.prof_t0 = __builtin_amdgcn_s_memtime();
+            X.prof_rt0 = __builtin_amdgcn_s_memrealtime();
+        }
 #endif
         gsync();
     }
@@ -1917,6 +1923,13 @@ struct Replayer : Params<kLay, kPol, kFix> {
         // while the request after them ran)
         if (preq && tid == 0 && done > pr_next) put_per_request(done - 1);
         X.kkey[tid] = evw;   // per-wavefront eviction counts, summed below
+#ifdef PC_PROFILE
+        // the instance's span on both clocks: their ratio is the shader clock
+        if (tid == 0) {
+            X.prof[6] = __builtin_amdgcn_s_memtime() - X.prof_t0;
+            X.prof[7] = __builtin_amdgcn_s_memrealtime() - X.prof_rt0;
+        }
+#endif
         gsync();
         if (wid != 0) return;
         // stats record: 64 groups x 17 int64, then the instance block
@@ -1945,8 +1958,9 @@ struct Replayer : Params<kLay, kPol, kFix> {
         }
 #ifdef PC_PROFILE
         // phase build: the record of group 63 carries the 6 phase cycle
-        // totals, then (fields 8-11) the event counts
-        if (G < 64 && lane < 6) st[63 * kGroupFields + lane] = (int64_t)X.prof[lane];
+        // totals, the instance's span in shader cycles and in 100 MHz
+        // real-time ticks, then (fields 8-11) the event counts
+        if (G < 64 && lane < 8) st[63 * kGroupFields + lane] = (int64_t)X.prof[lane];
         if (G < 64 && lane < 4) st[63 * kGroupFields + 8 + lane] = (int64_t)X.pcnt[lane];
 #endif
     }

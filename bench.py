@@ -33,7 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 PROFILES = os.path.join(ROOT, "profiles")
 # what the replay kernel is built from: its sources and its compiler flags
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_01657_amd", *f) for f in
-                  (("csrc", "pc_replay.hip"), ("csrc", "pc_replay_hybrid.hip"), ("csrc", "pc_internal.h"),
+                  (("csrc", "pc_replay.hip"), ("csrc", "pc_replay_global.hip"), ("csrc", "pc_internal.h"),
                    ("build.py",))]
 HASH_BYTES_PER_BLOCK = 64 + 8  # 16 int32 tokens in, one uint64 key out
 HASH_BYTES_PER_REQ = 8 + 4 + 4 + 8 + 8   # tok_off, len, ns, key_off read, key_off write

@@ -19,26 +19,28 @@ LIB = os.path.join(HERE, "libpcreplay.so")
 LIB_PHASES = os.path.join(HERE, "libpcreplay_phases.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["pc_hash.hip", "pc_replay.hip", "pc_replay_hybrid.hip", "pc_abi.cpp"]
+SOURCES = ["pc_hash.hip", "pc_replay.hip", "pc_replay_global.hip", "pc_abi.cpp"]
 ARCH = os.environ.get("PC_OFFLOAD_ARCH", "gfx950")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
          # packed FP32 instructions stay off (none are needed: the path is integer)
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-result"]
 # Machine schedulers of the replay kernels, each the fastest measured for
-# its layout (results are identical under every one):
-#  - all-LDS and workspace layouts (pc_replay.hip): the scheduler that
-#    maximises instruction-level parallelism, 3.5 % less replay time than
-#    the default one on the one-touch C = 4096 batch (one instance per CU);
-#  - hybrid layout (pc_replay_hybrid.hip, two instances per CU): the
-#    iterative scheduler that keeps the occupancy target, 2.4 % less time
-#    than the ILP one on the 1,024-instance batch (it costs the all-LDS
-#    kernel 2.6 %, hence the separate translation unit).
+# its layouts (results are identical under every one):
+#  - all-LDS layout (pc_replay.hip): the scheduler that maximises
+#    instruction-level parallelism, 3.5 % less replay time than the default
+#    one on the one-touch C = 4096 batch (one instance per CU);
+#  - hybrid and workspace layouts (pc_replay_global.hip, two instances per
+#    CU, state partly or wholly in global memory): the iterative scheduler
+#    that keeps the occupancy target, 2.4 % less time than the ILP one on
+#    the 1,024-instance batch (hybrid) and 1.9 % on the C = 16,384 chat
+#    instances (workspace); it costs the all-LDS kernels 2.2-2.6 %, hence
+#    the separate translation unit.
 # The loops that must be unrolled say so (#pragma unroll); the compiler's
 # own unrolling of the others only lengthens the instruction stream and
 # raises register pressure (another 3.7 % less replay time without it).
 SOURCE_FLAGS = {"pc_replay.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp", "-fno-unroll-loops"],
-                "pc_replay_hybrid.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-maxocc", "-fno-unroll-loops"]}
+                "pc_replay_global.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-maxocc", "-fno-unroll-loops"]}
 
 
 def _hipcc() -> str:

@@ -234,10 +234,11 @@ hipError_t replay_set_lds_limit(int32_t lds_bytes);
 hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order,
                          int32_t n_launch, int32_t lds_bytes, int layout, int per_cu, uint8_t *ws,
                          int64_t *stats, int32_t *per_req, hipStream_t s);
-// the hybrid-layout kernel's own translation unit (pc_replay_hybrid.hip)
+// the translation unit of the kernels with state in global memory
+// (pc_replay_global.hip: hybrid and workspace layouts)
 hipError_t replay_hybrid_set_lds_limit(int32_t lds_bytes);
-hipError_t launch_replay_hybrid(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order,
-                                int32_t n_launch, int32_t lds_bytes, uint8_t *ws, int64_t *stats, int32_t *per_req,
-                                hipStream_t s);
+hipError_t launch_replay_global(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order,
+                                int32_t n_launch, int32_t lds_bytes, int layout, uint8_t *ws, int64_t *stats,
+                                int32_t *per_req, hipStream_t s);
 
 }  // namespace pcr

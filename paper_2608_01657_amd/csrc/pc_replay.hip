@@ -2008,7 +2008,7 @@ void replay_kernel(const DevInst *__restrict__ insts, const DevTrace *__restrict
                    const int32_t *__restrict__ order, uint8_t *ws, int64_t *stats, int32_t *per_req) {
     replay_body<kLay>(insts, traces, order, ws, stats, per_req);
 }
-#ifndef PC_REPLAY_HYBRID_TU
+#ifndef PC_REPLAY_GLOBAL_TU
 // An instance whose LDS state takes the whole CU: no occupancy target, so
 // the compiler schedules for one wave per SIMD (about 5 % less time per
 // request than the same code built for two).
@@ -2021,21 +2021,27 @@ void replay_kernel_solo(const DevInst *__restrict__ insts, const DevTrace *__res
 
 }  // namespace
 
-// The hybrid-layout kernel is built in a translation unit of its own
-// (pc_replay_hybrid.hip includes this file with PC_REPLAY_HYBRID_TU set),
-// under the machine scheduler that suits it; this one holds the others.
-#ifdef PC_REPLAY_HYBRID_TU
+// The kernels whose state is partly or wholly in global memory (hybrid and
+// workspace layouts) are built in a translation unit of their own
+// (pc_replay_global.hip includes this file with PC_REPLAY_GLOBAL_TU set),
+// under the machine scheduler that suits them; this one holds the all-LDS
+// kernels.
+#ifdef PC_REPLAY_GLOBAL_TU
 
 hipError_t replay_hybrid_set_lds_limit(int32_t lds_bytes) {
     return hipFuncSetAttribute(reinterpret_cast<const void *>(&replay_kernel<kLayHybrid>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
 }
 
-hipError_t launch_replay_hybrid(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order,
-                                int32_t n_launch, int32_t lds_bytes, uint8_t *ws, int64_t *stats, int32_t *per_req,
-                                hipStream_t s) {
-    hipLaunchKernelGGL(replay_kernel<kLayHybrid>, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s, d_inst,
-                       d_traces, d_order, ws, stats, per_req);
+hipError_t launch_replay_global(const DevInst *d_inst, const DevTrace *d_traces, const int32_t *d_order,
+                                int32_t n_launch, int32_t lds_bytes, int layout, uint8_t *ws, int64_t *stats,
+                                int32_t *per_req, hipStream_t s) {
+    if (layout == kLayHybrid)
+        hipLaunchKernelGGL(replay_kernel<kLayHybrid>, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s,
+                           d_inst, d_traces, d_order, ws, stats, per_req);
+    else
+        hipLaunchKernelGGL(replay_kernel<kLayWs>, dim3((unsigned)n_launch), dim3(kB), 0, s, d_inst, d_traces,
+                           d_order, ws, stats, per_req);
     return hipGetLastError();
 }
 
@@ -2057,17 +2063,14 @@ hipError_t launch_replay(const DevInst *d_inst, const DevTrace *d_traces, const 
                          int32_t lds_bytes, int layout, int per_cu, uint8_t *ws, int64_t *stats, int32_t *per_req,
                          hipStream_t s) {
     if (n_launch <= 0) return hipSuccess;
-    if (layout == kLayHybrid)
-        return launch_replay_hybrid(d_inst, d_traces, d_order, n_launch, lds_bytes, ws, stats, per_req, s);
-    if (layout == kLayLds && per_cu == 1)
+    if (layout != kLayLds)
+        return launch_replay_global(d_inst, d_traces, d_order, n_launch, lds_bytes, layout, ws, stats, per_req, s);
+    if (per_cu == 1)
         hipLaunchKernelGGL(replay_kernel_solo, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s, d_inst,
                            d_traces, d_order, ws, stats, per_req);
-    else if (layout == kLayLds)
+    else
         hipLaunchKernelGGL(replay_kernel<kLayLds>, dim3((unsigned)n_launch), dim3(kB), (size_t)lds_bytes, s, d_inst,
                            d_traces, d_order, ws, stats, per_req);
-    else
-        hipLaunchKernelGGL(replay_kernel<kLayWs>, dim3((unsigned)n_launch), dim3(kB), 0, s, d_inst, d_traces,
-                           d_order, ws, stats, per_req);
     return hipGetLastError();
 }
 

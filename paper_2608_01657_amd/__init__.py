@@ -19,6 +19,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpcreplay.so")
 # the same library with per-request-phase cycle counters (see phase_counters)
 PHASES_LIB_PATH = os.path.join(_HERE, "libpcreplay_phases.so")
+# the race-detection build: a pseudo-random per-wavefront delay after every
+# replay barrier (results must not change)
+JITTER_LIB_PATH = os.path.join(_HERE, "libpcreplay_jitter.so")
 PHASE_NAMES = ["request_start", "lookup", "reclamation", "charge", "insert_release", "accounting"]
 PHASE_EVENTS = ["evicting_requests", "log_compactions", "s3fifo_scan_batches", "prefixshield_queue_takes"]
 
@@ -90,6 +93,16 @@ def use_phase_counters(on: bool = True):
     if _lib is not None:
         raise RuntimeError("the library is already loaded")
     LIB_PATH = PHASES_LIB_PATH if on else os.path.join(_HERE, "libpcreplay.so")
+
+
+def use_jitter_build():
+    """Select the race-detection library (before the first call into the
+    library): same entry points and results, with shifted wavefront timing
+    inside every replay workgroup."""
+    global LIB_PATH
+    if _lib is not None:
+        raise RuntimeError("the library is already loaded")
+    LIB_PATH = JITTER_LIB_PATH
 
 
 def phase_counters(groups) -> dict:

@@ -1,6 +1,10 @@
 """Builds libpcreplay.so (the HIP library behind include/pc.h) for gfx950,
-and libpcreplay_phases.so, the same library with per-phase cycle counters
-(-DPC_PROFILE; the counters replace the stats record of group 63).
+and two test builds of the same sources:
+  - libpcreplay_phases.so, with per-phase cycle counters (-DPC_PROFILE; the
+    counters replace the stats record of group 63);
+  - libpcreplay_jitter.so, the race-detection build (-DPC_JITTER): every
+    replay barrier is followed by a pseudo-random per-wavefront delay, so
+    results that depend on wavefront timing differ from the oracle's.
 
     python -m paper_2608_01657_amd.build
 """
@@ -17,6 +21,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libpcreplay.so")
 LIB_PHASES = os.path.join(HERE, "libpcreplay_phases.so")
+LIB_JITTER = os.path.join(HERE, "libpcreplay_jitter.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["pc_hash.hip", "pc_replay.hip", "pc_replay_global.hip", "pc_abi.cpp"]
@@ -51,8 +56,12 @@ def _hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    _build_one(LIB, BUILD_DIR, [], verbose)
-    _build_one(LIB_PHASES, os.path.join(BUILD_DIR, "phases"), ["-DPC_PROFILE"], verbose)
+    variants = [(LIB, BUILD_DIR, []),
+                (LIB_PHASES, os.path.join(BUILD_DIR, "phases"), ["-DPC_PROFILE"]),
+                (LIB_JITTER, os.path.join(BUILD_DIR, "jitter"), ["-DPC_JITTER"])]
+    with ThreadPoolExecutor(max_workers=len(variants)) as ex:
+        for f in [ex.submit(_build_one, lib, d, extra, verbose) for lib, d, extra in variants]:
+            f.result()
     return LIB
 
 

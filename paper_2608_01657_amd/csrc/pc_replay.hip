@@ -540,6 +540,24 @@ struct Replayer : Params<kLay, kPol, kFix> {
     }
 
     // ============================================================ sync
+#ifdef PC_JITTER
+    // Race-detection build: after every barrier each wavefront waits a
+    // pseudo-random 0-7 x 128 cycles (from the shader clock, the workgroup
+    // and the wavefront), so the wavefronts of a workgroup enter each
+    // barrier interval in shifted order.  A result that depends on which
+    // wavefront gets there first (shared state read in the interval in
+    // which another wavefront writes it) shows up as a parity difference.
+    DEV void jitter() const {
+        uint64_t t = __builtin_amdgcn_s_memtime();
+        t ^= (uint64_t)(blockIdx.x * 0x9E3779B9u) ^ ((uint64_t)wid << 17);
+        t *= 0xff51afd7ed558ccdull;
+        t ^= t >> 33;
+        const uint32_t d = __builtin_amdgcn_readfirstlane((uint32_t)(t >> 5) & 7u);
+        for (uint32_t i = 0; i < d; ++i) __builtin_amdgcn_s_sleep(2);
+    }
+#else
+    DEV void jitter() const {}
+#endif
     // Barrier making state-memory writes visible to the workgroup.  With the
     // state in LDS, only LDS is fenced, so global prefetches stay in flight.
     DEV void bsync() {
@@ -550,9 +568,13 @@ struct Replayer : Params<kLay, kPol, kFix> {
         } else {
             __syncthreads();
         }
+        jitter();
     }
     // Barrier for global memory too (ghost ring, prefix bitmaps).
-    DEV void gsync() { __syncthreads(); }
+    DEV void gsync() {
+        __syncthreads();
+        jitter();
+    }
 
     template <int M>
     DEV void bballot(const bool (&p)[M], BMask (&out)[M]) {
@@ -764,9 +786,12 @@ struct Replayer : Params<kLay, kPol, kFix> {
     DEV void kick_pending(uint32_t gref = 0) {
         const uint32_t nk = rfl(X.novf);
         if (nk == 0) return;
-        // the walk reads the keys of table entries, which this request may
-        // just have written (hybrid layout: in global memory)
+        // every wavefront reads the count before thread 0 clears it (one
+        // that read it after would skip the barriers below); the walk reads
+        // the keys of table entries, which this request may just have
+        // written (hybrid layout: in global memory)
         if constexpr (kHyb) gsync();
+        else bsync();
         if (tid == 0) {
             for (uint32_t i = 0; i < nk; ++i) {
                 const bool main = X.kmain[i] != 0;
@@ -869,6 +894,13 @@ struct Replayer : Params<kLay, kPol, kFix> {
     DEV void ensure_room(uint32_t k) {
         if (tail + k - head <= R) return;
         if constexpr (kQueues) {   // lowest cursor of a non-empty queue bounds every live entry
+            // Every wavefront reads every queue count and keeps its own copy
+            // of head, so all must read the same counts: a request that
+            // evicted nothing reaches here with no barrier after its
+            // lookup's count updates (any wavefront may still be making
+            // them).  head, tail and k are uniform, so all wavefronts take
+            // this branch together.
+            bsync();
             uint32_t m = tail;
             for (int i = lane; i < 192; i += 64)
                 if (cnt[i] > 0 && cur[i] < m) m = cur[i];
@@ -1658,6 +1690,15 @@ struct Replayer : Params<kLay, kPol, kFix> {
         const int nfresh = C - hwm;
         int nalloc = 0, seen = 0, seen_new = 0;
         if (tid == 0) X.nghost = 0;
+        // A one-step insert claims table entries with counters kept in the
+        // duplicate set's words (tclaim), so every wavefront must see those
+        // words clear first: the lookup clears its entries after its last
+        // barrier, and S3-FIFO's reclamation clears its ghost-claim counters
+        // after its own last barrier.  (A longer request takes a barrier
+        // before its claims, and the other policies' reclamation is preceded
+        // by one.)  The barrier also orders thread 0's reset of the ghost-hit
+        // count before any wavefront adds to it.
+        if (n <= kB && m > 0 && (e == 0 || policy == kS3)) bsync();
         TH hh = {};
         uint32_t touched = 0;
         if (n <= kB && n > 0) {

@@ -67,3 +67,75 @@ def run_key_traces(kts, instances_per_trace, per_request=True, dense=False):
         if per_request:
             assert np.array_equal(pr[k], o.per_request), f"instance {k}: per-request outputs differ"
     return res
+
+
+POLICIES = [tg.POLICY_LRU, tg.POLICY_S3FIFO, tg.POLICY_PREFIXSHIELD, tg.POLICY_STATICQUOTA]
+
+
+def random_key_batch(chunk):
+    """25 crafted key traces (seeds 25*chunk ...) with frequent hits, orphans,
+    duplicates and truncation, each replayed by every policy and flag with
+    1-3 contracts, ticks, eps and S3-FIFO parameters drawn per instance.
+    Returns (key traces, instances per trace)."""
+    kts, per = [], []
+    for seed in range(chunk * 25, chunk * 25 + 25):
+        rng = np.random.default_rng(seed)
+        nc = int(rng.integers(1, 4))
+        kt = tg.random_key_trace(seed, n_req=int(rng.integers(1, 120)), max_blocks=int(rng.integers(1, 80)),
+                                 n_groups=int(rng.integers(1, 6)), n_prefix=12, n_contracts=nc,
+                                 key_universe=int(rng.integers(4, 200)), with_ticks=bool(seed % 2))
+        insts = []
+        for pol in POLICIES:
+            for flags in ([0, 1, 2, 3] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                cap = int(rng.integers(1, 90))
+                contracts = [(int(rng.integers(3, 3 * tg.Q16)), int(rng.integers(0, 40)) * tg.Q16)
+                             for _ in range(nc)]
+                # S3-FIFO also with a one-block small queue (0), no ghost
+                # (1000), every head moving (threshold 0) and none (4)
+                insts.append(tg.Instance(0, pol, cap, contracts=contracts, flags=flags,
+                                         eps_q16=int(rng.choice([0, tg.Q16 // 2, 3 * tg.Q16])),
+                                         s3_small_permille=int(rng.choice([0, 1, 100, 250, 500, 1000])),
+                                         s3_move_threshold=int(rng.choice([0, 1, 2, 4]))))
+        kts.append(kt)
+        per.append(insts)
+    return kts, per
+
+
+def step_boundary_batch():
+    """6 key traces of 40 requests of 255-257 and 511-513 blocks (both sides
+    of the 256-position lookup step) with shared prefixes, duplicates within
+    a request and keys reused across requests; every policy and PrefixShield
+    flag at capacities 200, 256, 300 and 700.  Returns (key traces,
+    instances per trace)."""
+    kts, per = [], []
+    for seed in range(6):
+        rng = np.random.default_rng(9000 + seed)
+        G = 3
+        reqs, groups = [], []
+        hist = []
+        for r in range(40):
+            n = int(rng.choice([255, 256, 257, 511, 512, 513]))
+            if hist and rng.random() < 0.6:
+                src = hist[int(rng.integers(0, len(hist)))]
+                ks = list(src[:int(rng.integers(0, len(src) + 1))])
+            else:
+                ks = []
+            while len(ks) < n:
+                ks.append(int(rng.integers(1, 1500)))    # small universe: reuse and duplicates
+            ks = ks[:n]
+            hist.append(ks)
+            reqs.append(ks)
+            groups.append(int(rng.integers(0, G)))
+        keys = np.array([k for r in reqs for k in r], dtype=np.uint64)
+        off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.int64)
+        R = len(reqs)
+        kts.append(tg.KeyTrace(keys, off, np.array(groups, np.uint8), (np.arange(R) % 2).astype(np.uint8),
+                               (np.array(groups) * 3 + np.arange(R) % 3).astype(np.uint32), G, 3 * G))
+        contracts = [(tg.Q16, 64 * tg.Q16), (tg.Q16 // 4, 16 * tg.Q16)]
+        insts = []
+        for pol in POLICIES:
+            for cap in (200, 256, 300, 700):
+                for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                    insts.append(tg.Instance(0, pol, cap, contracts=contracts, flags=flags))
+        per.append(insts)
+    return kts, per

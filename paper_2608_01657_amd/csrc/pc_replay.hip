@@ -542,17 +542,20 @@ struct Replayer : Params<kLay, kPol, kFix> {
     // ============================================================ sync
 #ifdef PC_JITTER
     // Race-detection build: after every barrier each wavefront waits a
-    // pseudo-random 0-7 x 128 cycles (from the shader clock, the workgroup
-    // and the wavefront), so the wavefronts of a workgroup enter each
-    // barrier interval in shifted order.  A result that depends on which
-    // wavefront gets there first (shared state read in the interval in
-    // which another wavefront writes it) shows up as a parity difference.
+    // pseudo-random time (from the shader clock, the workgroup and the
+    // wavefront): 0-7 x 128 cycles, or after one barrier in eight 0-63 x 128
+    // cycles, longer than most barrier intervals.  The wavefronts of a
+    // workgroup so enter each interval in shifted order, and a result that
+    // depends on which one gets somewhere first (shared state read in the
+    // interval in which another wavefront writes it) shows up as a parity
+    // difference.
     DEV void jitter() const {
         uint64_t t = __builtin_amdgcn_s_memtime();
         t ^= (uint64_t)(blockIdx.x * 0x9E3779B9u) ^ ((uint64_t)wid << 17);
         t *= 0xff51afd7ed558ccdull;
         t ^= t >> 33;
-        const uint32_t d = __builtin_amdgcn_readfirstlane((uint32_t)(t >> 5) & 7u);
+        const uint32_t r = (uint32_t)(t >> 5);
+        const uint32_t d = __builtin_amdgcn_readfirstlane(((r >> 3) & 7u) == 0u ? (r >> 6) & 63u : r & 7u);
         for (uint32_t i = 0; i < d; ++i) __builtin_amdgcn_s_sleep(2);
     }
 #else
@@ -895,16 +898,17 @@ struct Replayer : Params<kLay, kPol, kFix> {
         if (tail + k - head <= R) return;
         if constexpr (kQueues) {   // lowest cursor of a non-empty queue bounds every live entry
             // Every wavefront reads every queue count and keeps its own copy
-            // of head, so all must read the same counts: a request that
-            // evicted nothing reaches here with no barrier after its
-            // lookup's count updates (any wavefront may still be making
-            // them).  head, tail and k are uniform, so all wavefronts take
-            // this branch together.
+            // of head, so all must read the same counts: a barrier before the
+            // reads (a request that evicted nothing reaches here with none
+            // after its lookup's count updates) and one after them (the
+            // insert that follows changes counts).  head, tail and k are
+            // uniform, so all wavefronts take this branch together.
             bsync();
             uint32_t m = tail;
             for (int i = lane; i < 192; i += 64)
                 if (cnt[i] > 0 && cur[i] < m) m = cur[i];
             m = wave_min32(m);
+            bsync();
             if (m > head) head = m;
         } else if constexpr (policy == kS3) {
             const uint32_t m = curS < curM ? curS : curM;

@@ -139,3 +139,44 @@ def step_boundary_batch():
                     insts.append(tg.Instance(0, pol, cap, contracts=contracts, flags=flags))
         per.append(insts)
     return kts, per
+
+
+def many_groups_batch():
+    """6 key traces with 64 accounting groups and 4 contracts of different
+    refill rates (normalized debt, Eq. 5; ties in projected debt), every
+    policy and PrefixShield flag.  Returns (key traces, instances per
+    trace)."""
+    kts, per = [], []
+    for seed in range(6):
+        rng = np.random.default_rng(1000 + seed)
+        kt = tg.random_key_trace(1000 + seed, n_req=300, max_blocks=12, n_groups=64, n_prefix=128,
+                                 n_contracts=4, key_universe=60)
+        insts = []
+        for pol in POLICIES:
+            for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
+                contracts = [(tg.Q16 // (c + 1), int(rng.integers(0, 4)) * tg.Q16) for c in range(4)]
+                insts.append(tg.Instance(0, pol, int(rng.integers(8, 200)), contracts=contracts, flags=flags))
+        kts.append(kt)
+        per.append(insts)
+    return kts, per
+
+
+def workload_parity(name, seeds, n_requests, per_request=False, **kw):
+    """Keys and replay of a named workload on both sides, every key and every
+    instance compared.  Returns the number of instances."""
+    traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests, **kw)
+    dts, okeys = [], []
+    for tr in traces:
+        t, keys, off = gpu_hash(tr)
+        ok_, ooff = oracle.hash_trace(tr)
+        assert np.array_equal(keys, ok_) and np.array_equal(off, ooff)
+        dts.append(t)
+        okeys.append((ok_, ooff))
+    res, pr = replay_gpu(dts, insts, per_request=per_request)
+    for k, inst in enumerate(insts):
+        o = oracle.replay_trace(traces[inst.trace], okeys[inst.trace][0], okeys[inst.trace][1], inst,
+                                per_request=per_request)
+        assert_same(res[k], o, f"{name} instance {k} {inst.label}")
+        if per_request:
+            assert np.array_equal(pr[k], o.per_request), f"{name} instance {k}: per-request outputs differ"
+    return len(insts)

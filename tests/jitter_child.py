@@ -20,8 +20,8 @@ import paper_2608_01657_amd as P  # noqa: E402
 P.use_jitter_build()
 
 import oracle  # noqa: E402
-from gpu_util import (assert_same, gpu_hash, random_key_batch, replay_gpu, run_key_traces,  # noqa: E402
-                      step_boundary_batch)
+from gpu_util import (assert_same, gpu_hash, many_groups_batch, random_key_batch, replay_gpu,  # noqa: E402
+                      run_key_traces, step_boundary_batch, workload_parity)
 from paper_2608_01657_amd import tracegen as tg  # noqa: E402
 
 
@@ -45,6 +45,14 @@ for chunk in range(4):
     n = len(run_key_traces(*random_key_batch(chunk)))
     done["random"] = done.get("random", 0) + n
 log(f"random key traces: {done['random']} instances ({time.time() - t0:.0f}s)")
+# 64 groups on 4 contracts: ties in projected debt, many queues
+done["many_groups"] = len(run_key_traces(*many_groups_batch()))
+# contention from 8 / 32 indebted groups on every request, the attack
+# traces with every PrefixShield variant and StaticQuota, three contract tiers
+for name, n_req in (("selector512x8", None), ("selector4096x32", None), ("attack_onetouch", None),
+                    ("attack_lowslow", None), ("attack_replay", None), ("tiers", 20000)):
+    done[name] = workload_parity(name, [0], n_req, per_request=True)
+    log(f"{name}: {done[name]} instances ({time.time() - t0:.0f}s)")
 # conversational trace at full length, every capacity (all-LDS, hybrid or
 # workspace state) and policy
 traces, insts = tg.workload("chat", seeds=[0])

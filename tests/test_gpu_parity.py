@@ -7,8 +7,8 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import POLICIES, assert_same, gpu_hash, random_key_batch, replay_gpu, run_key_traces, \
-    step_boundary_batch
+from gpu_util import POLICIES, assert_same, gpu_hash, many_groups_batch, random_key_batch, replay_gpu, \
+    run_key_traces, step_boundary_batch, workload_parity
 from paper_2608_01657_amd import device as dv
 from paper_2608_01657_amd import tracegen as tg
 
@@ -75,39 +75,11 @@ def test_replay_random_key_traces(chunk):
 def test_replay_many_groups():
     """64 accounting groups, several contracts with different refill rates
     (normalized debt, Eq. 5), ties in projected debt."""
-    kts, per = [], []
-    for seed in range(6):
-        rng = np.random.default_rng(1000 + seed)
-        kt = tg.random_key_trace(1000 + seed, n_req=300, max_blocks=12, n_groups=64, n_prefix=128,
-                                 n_contracts=4, key_universe=60)
-        insts = []
-        for pol in POLICIES:
-            for flags in ([0, 1, 2] if pol == tg.POLICY_PREFIXSHIELD else [0]):
-                contracts = [(tg.Q16 // (c + 1), int(rng.integers(0, 4)) * tg.Q16) for c in range(4)]
-                insts.append(tg.Instance(0, pol, int(rng.integers(8, 200)), contracts=contracts, flags=flags))
-        kts.append(kt)
-        per.append(insts)
-    run_key_traces(kts, per)
+    run_key_traces(*many_groups_batch())
 
 
 def _workload_parity(name, seeds, n_requests, per_request=False, policies=tuple(POLICIES), **kw):
-    traces, insts = tg.workload(name, seeds=seeds, n_requests=n_requests, policies=policies, **kw)
-    dts = []
-    okeys = []
-    for tr in traces:
-        t, keys, off = gpu_hash(tr)
-        ok_, ooff = oracle.hash_trace(tr)
-        assert np.array_equal(keys, ok_) and np.array_equal(off, ooff)
-        dts.append(t)
-        okeys.append((ok_, ooff))
-    res, pr = replay_gpu(dts, insts, per_request=per_request)
-    for k, inst in enumerate(insts):
-        o = oracle.replay_trace(traces[inst.trace], okeys[inst.trace][0], okeys[inst.trace][1], inst,
-                                per_request=per_request)
-        assert_same(res[k], o, f"{name} instance {k} {inst.label}")
-        if per_request:
-            assert np.array_equal(pr[k], o.per_request)
-    return res
+    return workload_parity(name, seeds, n_requests, per_request=per_request, policies=policies, **kw)
 
 
 def test_replay_tiny_workload_full():

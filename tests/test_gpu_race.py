@@ -24,4 +24,6 @@ def test_replay_results_independent_of_wavefront_timing():
     assert r.returncode == 0, r.stderr[-4000:]
     done = json.loads(r.stdout.strip().splitlines()[-1])
     assert done["step_boundary"] == 3 * done["step_boundary_dense"] > 0
-    assert done["random"] > 0 and done["chat_full_length"] == 15
+    assert done["random"] > 0 and done["chat_full_length"] == 15 and done["many_groups"] > 0
+    assert all(done[n] > 0 for n in ("selector512x8", "selector4096x32", "attack_onetouch", "attack_lowslow",
+                                     "attack_replay", "tiers"))

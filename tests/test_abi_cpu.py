@@ -27,8 +27,12 @@ def test_header_declares_the_boundary():
         assert n in names
 
 
-def test_library_exports_every_declared_symbol():
-    lib = ctypes.CDLL(P.LIB_PATH)
+@pytest.mark.parametrize("path", [P.LIB_PATH, P.PHASES_LIB_PATH, P.JITTER_LIB_PATH],
+                         ids=["product", "phase_counters", "race_detection"])
+def test_library_exports_every_declared_symbol(path):
+    """The product library and both test builds of the same sources (phase
+    counters, race detection) load and export the whole boundary."""
+    lib = ctypes.CDLL(path)
     missing = [n for n in _declared() if not hasattr(lib, n)]
     assert not missing, missing
     assert sorted(P.EXPORTS) == sorted(_declared()), "binding and header disagree"

@@ -31,6 +31,7 @@ def log(msg):
 
 t0 = time.time()
 done = {}
+log("step boundary, launch 1 starting")
 # lookup-step boundaries at small capacities (the free-queue log fills and
 # is compacted often), replayed three times: each launch draws other delays
 for rep in range(3):
@@ -46,15 +47,18 @@ for chunk in range(4):
     done["random"] = done.get("random", 0) + n
 log(f"random key traces: {done['random']} instances ({time.time() - t0:.0f}s)")
 # 64 groups on 4 contracts: ties in projected debt, many queues
+log("many groups starting")
 done["many_groups"] = len(run_key_traces(*many_groups_batch()))
 # contention from 8 / 32 indebted groups on every request, the attack
 # traces with every PrefixShield variant and StaticQuota, three contract tiers
 for name, n_req in (("selector512x8", None), ("selector4096x32", None), ("attack_onetouch", None),
                     ("attack_lowslow", None), ("attack_replay", None), ("tiers", 20000)):
+    log(f"{name} starting")
     done[name] = workload_parity(name, [0], n_req, per_request=True)
     log(f"{name}: {done[name]} instances ({time.time() - t0:.0f}s)")
 # conversational trace at full length, every capacity (all-LDS, hybrid or
 # workspace state) and policy
+log("chat seed 0 starting")
 traces, insts = tg.workload("chat", seeds=[0])
 t, keys, off = gpu_hash(traces[0])
 okeys, ooff = oracle.hash_trace(traces[0])

@@ -282,10 +282,11 @@ int32_t validate_and_plan(const pc_trace_desc *traces, int32_t n_traces, const p
         if (d.layout == pcr::kLayWs) { d.ws_state = off; off = align_up(off + d.state_bytes, 256); }
         if (d.layout == pcr::kLayHybrid) {
             d.ws_key = off;
-            off = align_up(off + 8LL * d.capacity, 256);
-            if (d.policy == PC_PREFIXSHIELD) {
-                d.ws_pfx = off;
-                off = align_up(off + 4LL * d.capacity, 256);
+            if (d.policy == PC_PREFIXSHIELD) {   // key and prefix id in one 16-byte record per slot
+                d.ws_pfx = off + 8;
+                off = align_up(off + 16LL * d.capacity, 256);
+            } else {
+                off = align_up(off + 8LL * d.capacity, 256);
             }
             if (d.policy == PC_S3FIFO && d.g_cap > 0) {
                 d.ws_gtable = off;
@@ -404,7 +405,7 @@ int32_t pc_replay_state_bytes(const pc_trace_desc *traces, int32_t n_traces, con
         bytes_out[i] = P.di[i].state_bytes;
         const pcr::DevInst &d = P.di[i];
         if (d.layout == pcr::kLayHybrid)   // keys, prefix ids, ghost table in the workspace
-            bytes_out[i] += 8LL * d.capacity + (d.policy == PC_PREFIXSHIELD ? 4LL * d.capacity : 0) +
+            bytes_out[i] += (d.policy == PC_PREFIXSHIELD ? 16LL : 8LL) * d.capacity +
                             (d.policy == PC_S3FIFO && d.g_cap > 0 ? (32LL << d.gnb_log2) : 0);
         layout_out[i] = d.layout;
     }

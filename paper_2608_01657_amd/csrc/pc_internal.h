@@ -177,7 +177,10 @@ constexpr int kRecordWords = 64 * kGroupFields + 8;
 // from the instance's state base: dynamic LDS for kLayLds and kLayHybrid,
 // else the workspace region at ws_state.  The ghost ring and the prefix
 // bitmaps always live in the workspace, and so do the block keys and prefix
-// ids of a hybrid instance (ws_key, ws_pfx).
+// ids of a hybrid instance (ws_key, ws_pfx).  A hybrid PrefixShield instance
+// keeps a slot's key and prefix id together, in one 16-byte record per slot
+// (key at byte 0, prefix id at byte 8), so that a lookup reads both, and an
+// insert writes both, in one cache line.
 struct DevInst {
     int32_t trace, policy, capacity, flags;
     int32_t n_contracts, s_cap, g_cap, move_thr;
@@ -199,8 +202,8 @@ struct DevInst {
     int32_t pad;
     // workspace offsets (bytes from workspace base)
     int64_t ws_state;      // state region when layout == kLayWs
-    int64_t ws_key;        // uint64 [C] block keys (kLayHybrid)
-    int64_t ws_pfx;        // uint32 [C] prefix ids (kLayHybrid, PrefixShield)
+    int64_t ws_key;        // uint64 [C] block keys (kLayHybrid; PrefixShield: the 16-byte records)
+    int64_t ws_pfx;        // PrefixShield's prefix id of slot 0 (kLayHybrid): ws_key + 8, stride 16
     int64_t ws_gtable;     // uint32 [8 << gnb_log2] ghost table (kLayHybrid, S3-FIFO)
     int64_t ws_bits;       // uint32 [2 * n_prefix_words]: referenced, admitted
     int64_t ws_gring;      // uint64 [1 << gr_log2] (S3)

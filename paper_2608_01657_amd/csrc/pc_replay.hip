@@ -164,6 +164,18 @@ template <typename T>
 DEV const GLOBAL T *gptr(const T *p) { return (const GLOBAL T *)p; }
 template <typename T>
 DEV GLOBAL T *gptr_rw(T *p) { return (GLOBAL T *)p; }
+// One field of every record of a global array of records, read and written
+// as an array: element i is p[i * kStride] (in units of T).
+// Hybrid PrefixShield's per-slot record of block key and prefix id.
+struct alignas(16) KeyRec {
+    uint64_t key;
+    uint32_t pfx, pad;
+};
+template <typename T, int kStride>
+struct StridedGlobal {
+    GLOBAL T *p;
+    DEV GLOBAL T &operator[](uint32_t i) const { return p[(uint64_t)i * kStride]; }
+};
 
 // Block-wide ballot result: one 64-bit mask per wavefront.
 struct BMask {
@@ -408,9 +420,16 @@ struct Replayer : Params<kLay, kPol, kFix> {
     // keys and prefix ids) is in LDS
     static constexpr bool kLds = kLay != kLayWs;
     static constexpr bool kHyb = kLay == kLayHybrid;
-    using KeyPtr = typename std::conditional<kHyb, GLOBAL uint64_t *, uint64_t *>::type;
-    using PfxPtr = typename std::conditional<kHyb, GLOBAL uint32_t *, uint32_t *>::type;
-    using GtPtr = PfxPtr;     // the S3-FIFO ghost table
+    // hybrid PrefixShield: a slot's key and prefix id share one 16-byte
+    // record in global memory (key at byte 0, prefix id at byte 8)
+    static constexpr bool kPack = kHyb && kPol == kPS;
+    using KeyPtr = typename std::conditional<
+        kPack, StridedGlobal<uint64_t, 2>,
+        typename std::conditional<kHyb, GLOBAL uint64_t *, uint64_t *>::type>::type;
+    using PfxPtr = typename std::conditional<
+        kPack, StridedGlobal<uint32_t, 4>,
+        typename std::conditional<kHyb, GLOBAL uint32_t *, uint32_t *>::type>::type;
+    using GtPtr = typename std::conditional<kHyb, GLOBAL uint32_t *, uint32_t *>::type;   // S3-FIFO ghost table
     using StampT = typename std::conditional<kLay == kLayWs, uint32_t, uint16_t>::type;
     using Pm::C;
     using Pm::nb;
@@ -446,6 +465,7 @@ struct Replayer : Params<kLay, kPol, kFix> {
     // ---------------- arrays
     KeyPtr key;
     PfxPtr pfx;
+    const GLOBAL KeyRec *krec;   // the 16-byte records themselves (kPack)
     uint64_t *rkeys;          // (not in the hybrid layout: the trace's keys are read instead)
     StampT *stamp;
     uint32_t *meta, *table, *rset, *rcnt, *cnt, *cur, *res;
@@ -501,8 +521,15 @@ struct Replayer : Params<kLay, kPol, kFix> {
         constexpr bool fx = kFix == kFixC;
         constexpr StateOffsets F = fix_plan(kLay, kPol).f;
         if constexpr (kHyb) {
-            key = gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_key));
-            pfx = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_pfx));
+            if constexpr (kPack) {
+                key = KeyPtr{gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_key))};
+                pfx = PfxPtr{gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_key)) + 2};
+                krec = gptr(reinterpret_cast<const KeyRec *>(ws + I.ws_key));
+            } else {
+                key = gptr_rw(reinterpret_cast<uint64_t *>(ws + I.ws_key));
+                pfx = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_pfx));
+                krec = nullptr;
+            }
             gtable = gptr_rw(reinterpret_cast<uint32_t *>(ws + I.ws_gtable));
             rkeys = nullptr;
         } else {
@@ -510,6 +537,7 @@ struct Replayer : Params<kLay, kPol, kFix> {
             pfx = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_pfx : I.o_pfx));
             gtable = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_gtable : I.o_gtable));
             rkeys = reinterpret_cast<uint64_t *>(sbase + (fx ? F.o_rkeys : I.o_rkeys));
+            krec = nullptr;
         }
         stamp = reinterpret_cast<StampT *>(sbase + (fx ? F.o_stamp : I.o_stamp));
         meta = reinterpret_cast<uint32_t *>(sbase + (fx ? F.o_meta : I.o_meta));
@@ -1460,9 +1488,19 @@ struct Replayer : Params<kLay, kPol, kFix> {
             // before the barrier: nothing writes them between the probe and
             // the ballot, except an earlier step of this request, whose slots
             // a non-duplicate key never names (a duplicate ignores them)
-            const uint64_t ck = ntag == 1 ? key[cand] : 0ull;
+            uint64_t ck = 0ull;
+            uint32_t cp = 0u;
+            if constexpr (kPack) {   // key and prefix id: one 16-byte load
+                if (ntag == 1) {
+                    const GLOBAL KeyRec *rc = krec + cand;
+                    ck = rc->key;
+                    cp = rc->pfx;
+                }
+            } else {
+                ck = ntag == 1 ? key[cand] : 0ull;
+            }
             uint32_t mt = ntag == 1 ? meta[cand] : 0u;
-            const uint32_t cp = (policy == kPS && ntag == 1) ? pfx[cand] : 0u;
+            if constexpr (!kPack) cp = (policy == kPS && ntag == 1) ? pfx[cand] : 0u;
             bsync();
             // duplicate: an earlier position holds the same key.  It was filed
             // along the same bucket sequence, no later than the first bucket

@@ -179,9 +179,10 @@ LDS_CU, STATIC_RESERVE = 160 * 1024, 5120
 
 
 def _lds_part(b, pol, C=4096, ghost_bytes=32 << 10):
-    """LDS bytes of a hybrid instance: its block keys, PrefixShield's prefix
-    ids and S3-FIFO's ghost table are in the workspace."""
-    return b - 8 * C - (4 * C if pol == 2 else 0) - (ghost_bytes if pol == 1 else 0)
+    """LDS bytes of a hybrid instance: its block keys (PrefixShield: 16-byte
+    key and prefix-id records) and S3-FIFO's ghost table are in the
+    workspace."""
+    return b - (16 * C if pol == 2 else 8 * C) - (ghost_bytes if pol == 1 else 0)
 
 
 def test_layout_lets_two_4096_block_instances_share_a_cu():
@@ -215,7 +216,7 @@ def test_default_4096_layout_is_sized_for_512_block_requests():
     The sizes are those of the layouts' allocation order with the table at
     load 1/2 (all in LDS: 117,504 bytes for LRU, 150,272 for S3-FIFO,
     135,440 for PrefixShield), or at the largest size that keeps two
-    instances per CU (hybrid: 109,568 / 142,336 / 125,904 bytes, of which
+    instances per CU (hybrid: 109,568 / 142,336 / 142,288 bytes, of which
     76,800 / 76,800 / 76,752 in LDS)."""
     short = _trace(max_req_blocks=100)
     full = _trace(max_req_blocks=512)
@@ -223,7 +224,7 @@ def test_default_4096_layout_is_sized_for_512_block_requests():
         b, lay = P.pc_replay_state_bytes([short, full], [_inst(policy=pol, capacity=4096, trace=0),
                                                          _inst(policy=pol, capacity=4096, trace=1)])
         assert list(b) == [want, want] and lay == [P.PC_LAYOUT_LDS] * 2
-    for pol, want, lds in ((0, 109568, 76800), (1, 142336, 76800), (2, 125904, 76752)):
+    for pol, want, lds in ((0, 109568, 76800), (1, 142336, 76800), (2, 142288, 76752)):
         b, lay = P.pc_replay_state_bytes([short, full], [_inst(policy=pol, capacity=4096, trace=k % 2)
                                                          for k in range(600)])
         assert set(b) == {want} and set(lay) == {P.PC_LAYOUT_HYBRID} and _lds_part(want, pol) == lds

@@ -895,7 +895,14 @@ struct Replayer : Params<kLay, kPol, kFix> {
     }
 
     // Compaction of the free-queue log: live entries keep their order and
-    // are renumbered from `head`; all cursors restart at `head`.
+    // are renumbered from `head`; all cursors restart at `head`.  One
+    // barrier per 256-position step (its ballot): a step writes log
+    // positions below the next step's reads (nw <= p0, and fewer than R
+    // positions apart, so no two alias in the ring), metadata is not
+    // written at all, and a slot's stamp, which a step rewrites for its live
+    // entries, decides nothing in the next step whichever value that step
+    // reads -- a later position of the same slot is a stale copy, and
+    // neither the old nor the new stamp equals it.
     DEV void compact() {
         PROF_COUNT(1, 1);
         bsync();
@@ -914,7 +921,6 @@ struct Replayer : Params<kLay, kPol, kFix> {
                 stamp[s] = (StampT)np;
             }
             nw += (uint32_t)lm.count();
-            bsync();
         }
         tail = nw;
         if constexpr (kQueues)

@@ -164,13 +164,13 @@ template <typename T>
 DEV const GLOBAL T *gptr(const T *p) { return (const GLOBAL T *)p; }
 template <typename T>
 DEV GLOBAL T *gptr_rw(T *p) { return (GLOBAL T *)p; }
-// One field of every record of a global array of records, read and written
-// as an array: element i is p[i * kStride] (in units of T).
 // Hybrid PrefixShield's per-slot record of block key and prefix id.
 struct alignas(16) KeyRec {
     uint64_t key;
     uint32_t pfx, pad;
 };
+// One field of every record of a global array of records, read and written
+// as an array: element i is p[i * kStride] (in units of T).
 template <typename T, int kStride>
 struct StridedGlobal {
     GLOBAL T *p;
